@@ -1,0 +1,353 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix (CPU only).
+
+Each test names the passage it checks.  None of them re-types an oracle formula and compares
+the oracle with itself: they use brute force, closed-form completions from Sec. 2, textbook
+least squares, or invariants proved in the paper.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import scipy.sparse as sp
+
+from oracle import partition, salsa
+from workloads import gen
+
+
+def _rand_problem(m, n, r, density, seed, sign_init=True):
+    row_ptr, col, val = gen.random_sparse(m, n, density, seed)
+    S = salsa.csr_matrix(m, n, row_ptr, col, val)
+    if sign_init:
+        W, H = gen.sign_constrained_init(m, n, r, float(val.mean()), seed + 7)
+    else:
+        W, H = gen.gaussian_init(m, n, r, 0.5, seed + 7)
+    return S, W.astype(np.float64), H.astype(np.float64)
+
+
+def _exact_state_sweep(S, W, H, mode="deterministic", block=(7, 5)):
+    st = salsa.State(W, H)
+    ST = S.T.tocsr()
+    salsa.sweep(S, ST, st, block[0], block[1], seed=3, mode=mode)
+    return st
+
+
+# ---------------------------------------------------------------------------- P1: Z-update
+def test_z_update_is_elementwise_constrained_argmin():
+    """eq. updateZ: for fixed L, Z minimises ||Z - L|| subject to S = max(0, Z) (Sec. 3.2).
+    Brute force over a grid of candidates plus the analytic candidates {S_ij, L_ij, 0}."""
+    rng = np.random.default_rng(11)
+    grid = np.linspace(-4.0, 4.0, 10001)
+    for _ in range(25):
+        m, n = rng.integers(1, 7, 2)
+        S = np.where(rng.random((m, n)) < 0.4, np.round(rng.uniform(0.25, 3.0, (m, n)), 2), 0.0)
+        L = np.round(rng.uniform(-3.0, 3.0, (m, n)), 3)
+        Z = salsa.z_update(S, L)
+        for i in range(m):
+            for j in range(n):
+                cand = np.concatenate([grid, [S[i, j], L[i, j], 0.0]])
+                feas = cand[np.maximum(0.0, cand) == S[i, j]]
+                best = feas[np.argmin((feas - L[i, j]) ** 2)]
+                assert best == Z[i, j]
+                assert np.maximum(0.0, Z[i, j]) == S[i, j]
+
+
+# ------------------------------------------------------------------- P2 / P11: LS update forms
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_stochastic_step_equals_textbook_least_squares(seed):
+    """eq. lsqA_sto with eta = 1 and no momentum is the exact least-squares fit of the columns
+    J of Z (eq. updateZ) by A B_J^T: compare with numpy.linalg.lstsq (Sec. 3.2, eq. lsqA)."""
+    m, n, r = 37, 29, 4
+    S, W, H = _rand_problem(m, n, r, 0.2, seed, sign_init=(seed != 2))
+    A, B = W, H.T
+    j0, j1 = 5, 23
+    Sd = S.toarray()
+    Z = salsa.z_update(Sd[:, j0:j1], A @ B[j0:j1].T)
+    X_ls = np.linalg.lstsq(B[j0:j1], Z.T, rcond=None)[0].T
+    X, V = salsa.factor_step(S, A, B, j0, j1, 1.0, 0.0, np.zeros_like(A))
+    np.testing.assert_allclose(X, X_ls, rtol=1e-10, atol=1e-12 * np.abs(X_ls).max())
+    np.testing.assert_allclose(V, X_ls - A, rtol=1e-9, atol=1e-12 * np.abs(X_ls).max())
+
+
+def test_delta_form_matches_z_form():
+    """eq. Delta with Z from eq. updateZ equals eq. updateD with the '+ S_hat' sign, i.e. the
+    printed '- S_hat' of eqs. Delta_par/Delta_sto is a typo (the '+' reading)."""
+    rng = np.random.default_rng(5)
+    m, n, r = 23, 31, 5
+    S = np.where(rng.random((m, n)) < 0.3, rng.uniform(0.1, 2.0, (m, n)), 0.0)
+    A = rng.normal(size=(m, r))
+    B = rng.normal(size=(n, r))
+    L = A @ B.T
+    np.testing.assert_allclose(salsa.delta_update(S, A, B), salsa.z_update(S, L) - L, atol=1e-13)
+    minus_form = (S > 0) * (S - salsa.rectify(L) - L) - salsa.rectify(L)
+    assert np.abs(minus_form - (salsa.z_update(S, L) - L)).max() > 1e-3
+
+
+# ------------------------------------------------------------------- P3: monotone decrease
+@pytest.mark.parametrize("case", ["config1_small", "identity256", "random_gauss"])
+def test_deterministic_half_steps_never_increase_objective(case):
+    """Alternating minimisation decreases the objective monotonically (Sec. 3.2); checked
+    after every half-step for 20 sweeps."""
+    if case == "config1_small":
+        row_ptr, col, val, _ = gen.planted(300, 260, 8, 0.05, 1)
+        m, n, r = 300, 260, 8
+        W, H = gen.sign_constrained_init(m, n, r, float(val.mean()), 1001)
+    elif case == "identity256":
+        m = n = 256
+        r = 3
+        row_ptr, col, val = gen.identity(n)
+        W, H = gen.gaussian_init(m, n, r, 0.1, 1002)
+    else:
+        m, n, r = 120, 90, 6
+        row_ptr, col, val = gen.random_sparse(m, n, 0.1, 3)
+        W, H = gen.gaussian_init(m, n, r, 0.5, 1003)
+    S = salsa.csr_matrix(m, n, row_ptr, col, val)
+    ST = S.T.tocsr()
+    st = salsa.State(W, H)
+    f = salsa.objective(S, st.W, st.H)
+    for _ in range(20):
+        salsa.w_step(S, st, 0, n, 1.0, 0.0)
+        f1 = salsa.objective(S, st.W, st.H)
+        assert f1 <= f * (1 + 1e-12)
+        salsa.h_step(ST, st, 0, m, 1.0, 0.0)
+        f2 = salsa.objective(S, st.W, st.H)
+        assert f2 <= f1 * (1 + 1e-12)
+        f = f2
+
+
+# ------------------------------------------------- P4: identity and its rank-3 completion
+@pytest.mark.parametrize("n", [5, 64, 256])
+def test_identity_completion_closed_form(n):
+    """Corollary 1, eq. Omega: Omega_ij = (cos(2 pi (i-j)/n) - cos(2 pi/n)) / (1 - cos(2 pi/n))
+    has rank 3 and max(0, Omega) = I_n; the objective vanishes there."""
+    W, H = gen.identity_exact_factors(n)
+    i, j = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
+    c = math.cos(2 * math.pi / n)
+    Omega = (np.cos(2 * math.pi * (i - j) / n) - c) / (1 - c)
+    np.testing.assert_allclose(W @ H, Omega, atol=1e-9 * n * n)
+    sv = np.linalg.svd(Omega, compute_uv=False)
+    assert np.sum(sv > 1e-9 * sv[0]) == 3
+    np.testing.assert_allclose(np.maximum(0, Omega), np.eye(n), atol=1e-9)
+    S = salsa.csr_matrix(n, n, *gen.identity(n))
+    assert salsa.objective(S, W, H) < 1e-9
+
+
+def test_identity_completion_is_als_fixed_point_and_permutation():
+    """The exact completion is a fixed point of the deterministic sweep (Z = L there), and a
+    permuted identity P has the completion P Omega (Corollary 1)."""
+    n = 512
+    W, H = gen.identity_exact_factors(n)
+    S = salsa.csr_matrix(n, n, *gen.identity(n))
+    st = _exact_state_sweep(S, W, H)
+    assert np.linalg.norm(st.W - W) / np.linalg.norm(W) < 1e-9
+    assert np.linalg.norm(st.H - H) / np.linalg.norm(H) < 1e-9
+    perm = np.random.default_rng(0).permutation(n)
+    P = sp.csr_matrix((np.ones(n), (np.arange(n), perm)), shape=(n, n))
+    # row i of P has its one in column perm[i]: P = max(0, W[perm] H)
+    assert salsa.objective(P, W[perm], H) < 1e-9
+
+
+# ------------------------------------------------------------ P5: ring signless Laplacian
+@pytest.mark.parametrize("delta", [0.25, 0.5])
+def test_ring_completion(delta):
+    """Prop. 4: with tau (eq. tau) and r^2 (eq. r2), the thresholded similarities of
+    equispaced planar points (eqs. ringvecs, tsm-sym) reproduce eq. ring; Prop. 1 turns them
+    into a rank-3 completion, a zero of the objective and a fixed point of the sweep."""
+    n = 64
+    c = math.cos(2 * math.pi / n)
+    tau = (c - delta) / (1 - delta)
+    r2 = (1 - delta) / (1 - c)
+    th = 2 * math.pi * np.arange(n) / n
+    alpha = math.sqrt(r2) * np.stack([np.cos(th), np.sin(th)], 1)
+    nrm = np.linalg.norm(alpha, axis=1)
+    a = np.concatenate([alpha, (tau * nrm)[:, None]], 1)
+    b = np.concatenate([alpha, (-nrm)[:, None]], 1)
+    S = np.zeros((n, n))
+    for i in range(n):
+        S[i, i] = 1.0
+        S[i, (i + 1) % n] = delta
+        S[i, (i - 1) % n] = delta
+    np.testing.assert_allclose(np.maximum(0, a @ b.T), S, atol=1e-12)
+    Ssp = sp.csr_matrix(S)
+    assert salsa.objective(Ssp, a, b.T) < 1e-9
+    st = _exact_state_sweep(Ssp, a, b.T)
+    assert np.linalg.norm(st.W - a) / np.linalg.norm(a) < 1e-8
+
+
+# ------------------------------------------------------ P6: thresholded similarity matrix
+def test_thresholded_similarity_completion():
+    """Prop. 1: a_i = (alpha_i, tau |alpha_i|), b_j = (beta_j, -|beta_j|) complete eq. tsm
+    with rank d + 1; the objective is 0 and both update modes leave the factors unchanged."""
+    rng = np.random.default_rng(3)
+    m, n, d, tau = 90, 70, 4, 0.55
+    al = rng.normal(size=(m, d))
+    be = rng.normal(size=(n, d))
+    na = np.linalg.norm(al, axis=1)
+    nb = np.linalg.norm(be, axis=1)
+    S = np.maximum(0.0, al @ be.T - tau * np.outer(na, nb))
+    a = np.concatenate([al, (tau * na)[:, None]], 1)
+    b = np.concatenate([be, (-nb)[:, None]], 1)
+    np.testing.assert_allclose(np.maximum(0, a @ b.T), S, atol=1e-12)
+    Ssp = sp.csr_matrix(S)
+    assert salsa.objective(Ssp, a, b.T) < 1e-10
+    for mode in ("deterministic", "stochastic"):
+        st = salsa.State(a, b.T)
+        salsa.sweep(Ssp, Ssp.T.tocsr(), st, 30, 25, seed=9, mode=mode, eta=1.0, gamma=0.9)
+        assert np.linalg.norm(st.W - a) / np.linalg.norm(a) < 1e-9
+        assert np.linalg.norm(st.H - b.T) / np.linalg.norm(b) < 1e-9
+
+
+# ---------------------------------------------------------------------- P7: hypercube graph
+def test_hypercube_completion():
+    """Prop. 5: alpha_i = rho v_i with rho^2 = (1 - delta)/2 and tau = 1 - (2/d)(1 - delta)^-1
+    reproduce eq. hypercube (1 on the diagonal, delta between neighbours) with rank d + 1."""
+    d, delta = 8, 0.06
+    V = np.array([[1.0 if (k >> b) & 1 else -1.0 for b in range(d)] for k in range(2 ** d)])
+    rho = math.sqrt((1 - delta) / 2)
+    tau = 1 - (2.0 / d) / (1 - delta)
+    al = rho * V
+    nrm = np.linalg.norm(al, axis=1)
+    a = np.concatenate([al, (tau * nrm)[:, None]], 1)
+    b = np.concatenate([al, (-nrm)[:, None]], 1)
+    ham = (V[:, None, :] != V[None, :, :]).sum(-1)
+    S = np.where(ham == 0, 1.0, np.where(ham == 1, delta, 0.0))
+    np.testing.assert_allclose(np.maximum(0, a @ b.T), S, atol=1e-12)
+    assert salsa.objective(sp.csr_matrix(S), a, b.T) < 1e-10
+
+
+# --------------------------------------------------------------- P9 / P10: the objective
+def test_objective_routes_agree_and_bound_rmse():
+    """eq. SLloss (Z eliminated) equals eq. auxCost evaluated with the optimal Z, and by
+    Prop. 9 the objective is never below the RMSE (eq. RMSE)."""
+    rng = np.random.default_rng(8)
+    for _ in range(10):
+        m, n, r = rng.integers(3, 40, 3)
+        S = np.where(rng.random((m, n)) < 0.2, rng.uniform(0.1, 3.0, (m, n)), 0.0)
+        S[0, 0] = 1.0
+        L = rng.normal(size=(m, r)) @ rng.normal(size=(r, n))
+        f_aux = salsa.aux_objective_dense(S, L)
+        f_sl = math.sqrt(salsa.squared_loss_dense(S, L)) / np.linalg.norm(S)
+        assert abs(f_aux - f_sl) <= 1e-12 * max(1.0, f_aux)
+        assert f_aux >= salsa.rmse_dense(S, np.maximum(0, L)) - 1e-15
+        A = rng.normal(size=(m, r))
+        Bt = rng.normal(size=(r, n))
+        Ssp = sp.csr_matrix(S)
+        for chunk in (1, 7, 4096):
+            f_tiled = salsa.objective(Ssp, A, Bt, row_chunk=chunk)
+            assert abs(f_tiled - salsa.aux_objective_dense(S, A @ Bt)) <= 1e-12 * max(1, f_tiled)
+        assert salsa.objective(Ssp, A, Bt) >= salsa.rmse(Ssp, A, Bt) - 1e-15
+    # metrics are calibrated so that the all-zero approximation scores one (Sec. 3.1)
+    S = np.where(rng.random((9, 8)) < 0.3, 1.5, 0.0)
+    S[1, 1] = 2.0
+    assert abs(salsa.rmse_dense(S, np.zeros_like(S)) - 1.0) < 1e-15
+    assert abs(salsa.wjd_dense(S, np.zeros_like(S)) - 1.0) < 1e-15
+    assert salsa.wjd_dense(S, S) == 0.0
+
+
+# ------------------------------------------------------------------- P12: kernel algebra
+def test_clamped_contraction_identity():
+    """min(0, L) B_J = A (B_J^T B_J) - max(0, L) B_J, relating the clamped contraction to the
+    paper's fused product max(0, A B^T)(B^+)^T (eq. kernel)."""
+    rng = np.random.default_rng(4)
+    A = rng.normal(size=(50, 12))
+    BJ = rng.normal(size=(33, 12))
+    L = A @ BJ.T
+    lhs = salsa.clamped_contraction(A, BJ)
+    rhs = A @ (BJ.T @ BJ) - np.maximum(0, L) @ BJ
+    np.testing.assert_allclose(lhs, rhs, atol=1e-11)
+    # against a brute-force sum over j
+    brute = np.zeros_like(A)
+    for i in range(A.shape[0]):
+        for j in range(BJ.shape[0]):
+            brute[i] += min(0.0, float(A[i] @ BJ[j])) * BJ[j]
+    np.testing.assert_allclose(lhs, brute, atol=1e-11)
+
+
+def test_zb_product_brute_force():
+    """Z_{:,J} B_J by explicit loops over eq. updateZ."""
+    rng = np.random.default_rng(6)
+    m, n, r = 9, 11, 3
+    S = np.where(rng.random((m, n)) < 0.3, rng.uniform(0.2, 2.0, (m, n)), 0.0)
+    A = rng.normal(size=(m, r))
+    B = rng.normal(size=(n, r))
+    out = salsa.zb_product(sp.csr_matrix(S), A, B, 2, 9)
+    brute = np.zeros((m, r))
+    for i in range(m):
+        for j in range(2, 9):
+            l = float(A[i] @ B[j])
+            z = S[i, j] if S[i, j] > 0 else min(0.0, l)
+            brute[i] += z * B[j]
+    np.testing.assert_allclose(out, brute, atol=1e-12)
+
+
+# ----------------------------------------------------- P13: stochastic vs deterministic
+def test_one_block_stochastic_sweep_is_deterministic_sweep():
+    """With a single row block and a single column block, eta = 1 and no momentum, the
+    stochastic sweep performs exactly the two full least-squares half-steps; eta = 0 and no
+    momentum leaves the factors unchanged (eq. lsqA_sto)."""
+    m, n, r = 60, 45, 5
+    S, W, H = _rand_problem(m, n, r, 0.15, 21)
+    st_s = salsa.State(W, H)
+    salsa.sweep(S, S.T.tocsr(), st_s, m, n, seed=4, mode="stochastic", eta=1.0, gamma=0.0)
+    st_d = salsa.State(W, H)
+    salsa.sweep(S, S.T.tocsr(), st_d, 7, 3, seed=4, mode="deterministic")
+    np.testing.assert_allclose(st_s.A, st_d.A, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(st_s.B, st_d.B, rtol=1e-12, atol=1e-12)
+    st_0 = salsa.State(W, H)
+    salsa.sweep(S, S.T.tocsr(), st_0, 16, 16, seed=4, mode="stochastic", eta=0.0, gamma=0.0)
+    assert np.array_equal(st_0.A, W) and np.array_equal(st_0.B, H.T)
+
+
+def test_momentum_is_heavy_ball():
+    """Momentum adds a multiple gamma of the previously executed update (Sec. 4.1): two
+    consecutive steps on the same block with gamma give A2 - A1 = gamma (A1 - A0) + eta D1."""
+    m, n, r = 40, 30, 4
+    S, W, H = _rand_problem(m, n, r, 0.2, 2)
+    st = salsa.State(W, H)
+    A0 = st.A.copy()
+    salsa.w_step(S, st, 3, 20, 0.7, 0.9)
+    A1 = st.A.copy()
+    X1, _ = salsa.factor_step(S, A1, st.B, 3, 20, 1.0, 0.0, np.zeros_like(A1))
+    salsa.w_step(S, st, 3, 20, 0.7, 0.9)
+    np.testing.assert_allclose(st.A - A1, 0.9 * (A1 - A0) + 0.7 * (X1 - A1), atol=1e-12)
+
+
+# ------------------------------------------------------------------ P14: block invariance
+def test_row_tiling_and_blocks_do_not_change_results():
+    """The parallel (row-blockwise) update eq. lsqA_par gives the same factors for any row
+    tiling, and the deterministic sweep does not depend on the block sizes."""
+    m, n, r = 70, 50, 6
+    S, W, H = _rand_problem(m, n, r, 0.1, 13)
+    ref = None
+    for chunk, bm, bn in [(4096, 70, 50), (1, 7, 9), (13, 16, 50)]:
+        st = salsa.State(W, H)
+        salsa.sweep(S, S.T.tocsr(), st, bm, bn, seed=1, mode="deterministic", row_chunk=chunk)
+        if ref is None:
+            ref = st
+        else:
+            np.testing.assert_allclose(st.A, ref.A, rtol=1e-12, atol=1e-13)
+            np.testing.assert_allclose(st.B, ref.B, rtol=1e-12, atol=1e-13)
+
+
+def test_sampled_rows_match_full_step():
+    """Row-sampled evaluation of a stochastic step (used for full-size checks) reproduces the
+    full step on those rows."""
+    m, n, r = 80, 60, 5
+    S, W, H = _rand_problem(m, n, r, 0.1, 17)
+    A, B = W, H.T
+    V = np.random.default_rng(1).normal(size=A.shape) * 0.01
+    X, Vn = salsa.factor_step(S, A, B, 10, 41, 0.8, 0.9, V)
+    rows = np.array([0, 5, 79, 33])
+    Xs, Vs = salsa.factor_step(S, A, B, 10, 41, 0.8, 0.9, V, rows=rows)
+    np.testing.assert_allclose(Xs, X[rows], rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(Vs, Vn[rows], rtol=1e-13, atol=1e-14)
+
+
+def test_balanced_partition():
+    for size, block in [(1000, 256), (139255, 8192), (50000, 8192), (500000, 16384), (5, 7)]:
+        b = partition.bounds(size, block)
+        K = len(b) - 1
+        assert K == math.ceil(size / block)
+        sizes = np.diff(b)
+        assert b[0] == 0 and b[-1] == size
+        assert sizes.max() <= block and sizes.max() - sizes.min() <= 1
