@@ -1,0 +1,182 @@
+/*
+ * nmd.h - C ABI of an MI355X (gfx950) library for stochastic alternating least squares (SALSA)
+ * in subzero matrix completion: given a sparse nonnegative S (m x n), fit real factors W (m x r)
+ * and H (r x n) so that S ~ max(0, W H).
+ *
+ * The method (Saul et al., "Subzero matrix completion for sparse data analysis"):
+ *   L = W H (eq. ABt, with A = W and B = H^T), S-hat = max(0, L) (eq. rectify),
+ *   Z = S on the nonzeros of S and L - S-hat = min(0, L) elsewhere (eq. updateZ),
+ *   least-squares factor updates A <- Z B (B^T B)^-1, B <- Z^T A (A^T A)^-1 (eqs. lsqA, lsqB),
+ *   their stochastic form on a column mini-batch J, A <- A + eta Delta_{:J} B_J [B_J^T B_J]^-1
+ *   (eqs. Shat_sto, Delta_sto, lsqA_sto), the analogous update of B on a row mini-batch I, and a
+ *   momentum term that adds gamma times the previously executed update (Sec. 4.1).
+ *   Objective: ||Z - L||_F / ||S||_F (eq. auxCost) with Z eliminated as in eq. SLloss.
+ *
+ * Every entry point returns an int status (NMD_OK or a negative code); no C++ exception
+ * crosses this boundary.  Argument errors are detected before any device work is enqueued, so
+ * caller buffers are left untouched.  A context is not thread-safe; distinct contexts are
+ * independent.  All device pointers must be allocated on the device that is current when the
+ * context first touches the GPU (the device is remembered and made current on each call).
+ */
+#ifndef NMD_H
+#define NMD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct nmd_ctx nmd_ctx; /* opaque */
+
+enum {
+  NMD_OK = 0,
+  NMD_EINVAL = -1,     /* bad argument (sizes, pointers, CSR structure, values)            */
+  NMD_ENOMEM = -2,     /* host or device allocation failed                                 */
+  NMD_EDEVICE = -3,    /* a HIP runtime call failed or no usable gfx950 device             */
+  NMD_ENOTPD = -4,     /* a Gram matrix B_J^T B_J or A_I^T A_I was not positive definite    */
+  NMD_ESTATE = -5,     /* call out of order (e.g. a sweep before nmd_set_sparse_csr)         */
+  NMD_ENONFINITE = -6  /* an updated factor entry was NaN or infinite                       */
+};
+
+enum { NMD_DETERMINISTIC = 0, NMD_STOCHASTIC = 1 };
+
+enum {
+  NMD_FLAG_ASYNC = 1u, /* do not synchronise at the end of a sweep; device-detected errors
+                          are then reported by the next synchronising call               */
+  NMD_FLAG_TIMING = 2u /* record HIP events around every kernel class (see
+                          nmd_get_kernel_timing); adds a few microseconds per step        */
+};
+
+typedef struct {
+  uint32_t size;     /* sizeof(nmd_options), for forward compatibility                     */
+  int32_t mode;      /* NMD_DETERMINISTIC (full-batch least squares, eqs. lsqA/lsqB) or
+                        NMD_STOCHASTIC (mini-batch updates, eq. lsqA_sto)                 */
+  float eta;         /* step size eta > 0 of eq. lsqA_sto (1 = exact mini-batch solve)      */
+  float momentum;    /* gamma in [0, 1): V <- gamma V + eta (X - A), A <- A + V            */
+  uint32_t flags;    /* NMD_FLAG_* bits                                                     */
+} nmd_options;
+/* Defaults when opts == NULL: NMD_DETERMINISTIC, eta = 1, momentum = 0, flags = 0. */
+
+/*
+ * nmd_create - a context for an m x n problem fitted at rank r.
+ *   block_m, block_n: requested row- and column-block sizes.  The rows are split into
+ *     R = ceil(m / block_m) balanced blocks [floor(k m / R), floor((k+1) m / R)), the columns
+ *     likewise into C blocks (the paper's row sets I and column mini-batches J, Sec. 4.1).
+ *   seed: seed of the per-sweep block order (stochastic mode).
+ * Requires m, n >= 1; 1 <= r <= min(m, n) and r <= 512; block sizes >= 1; in stochastic mode
+ * r must not exceed the smallest row or column block (else a mini-batch Gram matrix is
+ * singular).  Returns NMD_EINVAL otherwise, NMD_ENOMEM if the context cannot be allocated.
+ * *out receives the context (NULL on failure).  No device memory is touched here.
+ */
+int nmd_create(nmd_ctx** out, int64_t m, int64_t n, int32_t r, int32_t block_m, int32_t block_n,
+               uint64_t seed, const nmd_options* opts);
+
+/*
+ * nmd_set_sparse_csr - copies S (host CSR arrays; the caller may free them afterwards).
+ *   row_ptr: int64[m+1], row_ptr[0] = 0, non-decreasing, row_ptr[m] = nnz.
+ *   col_idx: int32[nnz], 0 <= col < n, strictly increasing within each row.
+ *   values:  float[nnz], finite and >= 0.  Explicit zeros are dropped: the mask of eq. updateZ
+ *            is S_ij > 0.  At least one positive value is required (||S||_F normalises the
+ *            objective, eq. auxCost).
+ * Builds the per-column-block rows and per-row-block columns used by the updates.  Replaces
+ * any earlier S.  Returns NMD_EINVAL on a malformed matrix (S is then left unset).
+ */
+int nmd_set_sparse_csr(nmd_ctx* ctx, int64_t nnz, const int64_t* row_ptr, const int32_t* col_idx,
+                       const float* values);
+
+/*
+ * nmd_als_block_sweep - runs n_sweeps >= 1 sweeps (epochs) in place on W and H.
+ *   W: device float[m*r], row-major m x r.  H: device float[r*n], row-major r x n.
+ *   hip_stream: a hipStream_t (NULL = the null stream); all work is ordered on it.
+ * Stochastic mode: sweep t executes the seeded interleaved list of W-steps (one column block
+ * J each, eq. lsqA_sto) and H-steps (one row block I each); see nmd_get_schedule.
+ * Deterministic mode: the exact half-steps A <- A + Delta B (B^T B)^-1 over all columns, then
+ * B <- B + Delta^T A (A^T A)^-1 over all rows (eqs. spLsqA, spLsqB), with eta and gamma
+ * applied as in the stochastic update.  The sweep counter t and the momentum buffers persist
+ * across calls (nmd_reset clears them).  Returns NMD_ESTATE without S, NMD_EINVAL on NULL
+ * pointers or n_sweeps < 1, NMD_ENOTPD / NMD_ENONFINITE when the device flags a step (later
+ * steps are then skipped; nmd_last_error names the sweep and step), NMD_EDEVICE on a HIP
+ * failure.  Unless NMD_FLAG_ASYNC is set the call synchronises the stream before returning.
+ */
+int nmd_als_block_sweep(nmd_ctx* ctx, float* W, float* H, int32_t n_sweeps, void* hip_stream);
+
+/*
+ * nmd_objective - *out_obj = sqrt(sum_{S_ij = 0} max(0, L_ij)^2 + sum_{S_ij > 0} (S_ij - L_ij)^2)
+ * / ||S||_F with L = W H (eq. auxCost with Z eliminated, eq. SLloss).  W, H as in
+ * nmd_als_block_sweep (read only).  Products are formed in fp32 and summed in fp64.
+ * Synchronises the stream.  Errors as for nmd_als_block_sweep.
+ */
+int nmd_objective(nmd_ctx* ctx, const float* W, const float* H, double* out_obj, void* hip_stream);
+
+/* nmd_destroy - frees the context and its device memory; NULL-safe. */
+void nmd_destroy(nmd_ctx* ctx);
+
+/* ---------------------------------------------------------------- diagnostics ------------ */
+
+/* Last error message of the context ("" if none); valid until the next call on it.  With a
+ * NULL context, the message of the last failed nmd_create on this thread. */
+const char* nmd_last_error(const nmd_ctx* ctx);
+
+/*
+ * nmd_get_schedule - writes the step list of sweep `sweep` (0-based) into out[0..cap) and
+ * returns its length (R + C), or a negative code.  Encoding: +(k+1) is the W-step of column
+ * block k, -(k+1) the H-step of row block k.  Stochastic order: SplitMix64 stream seeded with
+ * seed XOR (sweep * 0x9E3779B97F4A7C15 mod 2^64), Lemire bounded integers, Fisher-Yates
+ * shuffles of the C column blocks then the R row blocks, merged so that a W-step comes next
+ * whenever (2w+1) R <= (2h+1) C (w, h = steps emitted so far).  Deterministic mode lists
+ * +1..+C then -1..-R (the W half accumulates over every column block before one solve).
+ * Host only; cap < R + C returns NMD_EINVAL.
+ */
+int nmd_get_schedule(const nmd_ctx* ctx, int64_t sweep, int32_t* out, int64_t cap);
+
+/* nmd_get_block_nnz - positive entries per column block (side 0, C values) or per row block
+ * (side 1, R values) into out[0..cap); returns the count or a negative code.  Host only. */
+int nmd_get_block_nnz(const nmd_ctx* ctx, int32_t side, int64_t* out, int64_t cap);
+
+/* nmd_get_block_bounds - the K+1 block offsets of the rows (side 1) or columns (side 0);
+ * returns K + 1 or a negative code.  Host only. */
+int nmd_get_block_bounds(const nmd_ctx* ctx, int32_t side, int64_t* out, int64_t cap);
+
+/* nmd_reset - zeroes the momentum buffers and the sweep counter. */
+int nmd_reset(nmd_ctx* ctx);
+
+/* nmd_get_sweep_count - *t = number of sweeps run since creation or the last reset. */
+int nmd_get_sweep_count(const nmd_ctx* ctx, int64_t* t);
+
+/*
+ * nmd_run_steps - runs the encoded steps steps[0..n_steps) (encoding of nmd_get_schedule)
+ * in order, each as a mini-batch update (eq. lsqA_sto on column block k for +(k+1), the
+ * analogous update of B on row block k for -(k+1)) with the context's eta and momentum,
+ * whatever its mode.  Does not advance the sweep counter.  Arguments and errors as for
+ * nmd_als_block_sweep.
+ */
+int nmd_run_steps(nmd_ctx* ctx, float* W, float* H, const int32_t* steps, int32_t n_steps,
+                  void* hip_stream);
+
+/*
+ * nmd_clamped_contraction - the dense product on its own: Y = min(0, A B^T) B for device
+ * row-major A (rows x r), B (blk x r) and Y (rows x r), i.e. Z B on the zeros of S (eq. updateZ
+ * contracted as in eq. lsqA); the L tile is never written to memory (the fused kernel of
+ * Sec. 4.2, in clamp-then-contract form).  r must be a multiple of 16 and <= 512; rows, blk
+ * >= 1.  One fp32 accumulation over all of B.  Asynchronous on hip_stream; allocates nothing.
+ */
+int nmd_clamped_contraction(const float* A, int64_t rows, const float* B, int64_t blk, int32_t r,
+                            float* Y, void* hip_stream);
+
+/*
+ * nmd_get_kernel_timing - with NMD_FLAG_TIMING set, the summed device time (HIP events on the
+ * stream the work ran on) and launch count of one kernel class since the last reset of the
+ * timers, plus the algorithmic work of those launches.  kernel: 0 = fused dense contraction
+ * (flops = 4 rows blk r per launch), 1 = sparse correction (bytes = algorithmic HBM bytes),
+ * 2 = Gram matrix and inverse, 3 = solve and update.  Synchronises the recorded events.
+ * reset != 0 clears the timers after reading.  Any output pointer may be NULL.
+ */
+int nmd_get_kernel_timing(nmd_ctx* ctx, int32_t kernel, double* total_ms, int64_t* launches,
+                          double* flops, double* bytes, int32_t reset);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NMD_H */

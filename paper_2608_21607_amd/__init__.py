@@ -1,0 +1,11 @@
+"""MI355X (gfx950) stochastic alternating least squares for subzero matrix completion.
+
+The method lives in libnmd.so (HIP kernels behind the C ABI of include/nmd.h); `nmd` is its
+ctypes binding and `build` compiles it in-tree.
+"""
+
+from .nmd import (  # noqa: F401
+    Context, NmdError, clamped_contraction, lib, header_functions,
+    DETERMINISTIC, STOCHASTIC, FLAG_ASYNC, FLAG_TIMING,
+    KERNEL_DENSE, KERNEL_SPARSE, KERNEL_FACTOR, KERNEL_APPLY,
+)

@@ -1,0 +1,883 @@
+// libnmd host side: the C ABI declared in include/nmd.h.
+//
+// Owns the context (problem sizes, block partition, copies of S arranged per block, device
+// workspaces, momentum buffers, sweep counter), validates every argument before any device
+// work, builds the per-sweep block order, and enqueues the kernels of each update on the
+// caller's stream.  Nothing here computes the method's arithmetic; the kernels do.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/nmd.h"
+#include "nmd_internal.h"
+
+using nmd::Item;
+using nmd::Split;
+
+namespace {
+
+thread_local std::string g_create_error;
+
+constexpr int kItemChunk = 128;    // entries per sparse work item
+constexpr int kMaxSplits = 16;     // partial outputs of the dense kernel
+constexpr int64_t kSplitRows = 1024;  // at most this many panel rows per fp32 accumulation
+constexpr int64_t kTargetWgs = 2048;  // dense workgroups wanted per launch (256 CUs)
+
+enum { K_DENSE = 0, K_SPARSE = 1, K_FACTOR = 2, K_APPLY = 3, K_COUNT = 4 };
+
+// ------------------------------------------------------------------------------ schedule --
+// SplitMix64 (Steele, Lea and Flood 2014), Lemire's bounded integers (2019), Fisher-Yates
+// (Durstenfeld order), and a proportional merge of column-block and row-block steps.
+struct SplitMix64 {
+  uint64_t s;
+  uint64_t next() {
+    s += 0x9E3779B97F4A7C15ULL;
+    uint64_t z = s;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+    return z ^ (z >> 31);
+  }
+};
+
+uint64_t bounded(SplitMix64& g, uint64_t k) {
+  unsigned __int128 prod = (unsigned __int128)g.next() * k;
+  uint64_t low = (uint64_t)prod;
+  if (low < k) {
+    const uint64_t thresh = (0 - k) % k;  // (2^64 - k) mod k
+    while (low < thresh) {
+      prod = (unsigned __int128)g.next() * k;
+      low = (uint64_t)prod;
+    }
+  }
+  return (uint64_t)(prod >> 64);
+}
+
+std::vector<int32_t> permutation(SplitMix64& g, int32_t k) {
+  std::vector<int32_t> a(k);
+  for (int32_t i = 0; i < k; ++i) a[i] = i;
+  for (int32_t i = k - 1; i > 0; --i) {
+    const int32_t j = (int32_t)bounded(g, (uint64_t)i + 1);
+    std::swap(a[i], a[j]);
+  }
+  return a;
+}
+
+std::vector<int32_t> make_schedule(uint64_t seed, int64_t t, int32_t R, int32_t C,
+                                   bool stochastic) {
+  std::vector<int32_t> out;
+  out.reserve((size_t)R + C);
+  if (!stochastic) {
+    for (int32_t k = 0; k < C; ++k) out.push_back(k + 1);
+    for (int32_t k = 0; k < R; ++k) out.push_back(-(k + 1));
+    return out;
+  }
+  SplitMix64 g{seed ^ ((uint64_t)t * 0x9E3779B97F4A7C15ULL)};
+  const std::vector<int32_t> sigma = permutation(g, C);
+  const std::vector<int32_t> pi = permutation(g, R);
+  int64_t w = 0, h = 0;
+  while (w < C || h < R) {
+    if (h == R || (w < C && (2 * w + 1) * (int64_t)R <= (2 * h + 1) * (int64_t)C)) {
+      out.push_back(sigma[w] + 1);
+      ++w;
+    } else {
+      out.push_back(-(pi[h] + 1));
+      ++h;
+    }
+  }
+  return out;
+}
+
+std::vector<int64_t> balanced_bounds(int64_t size, int64_t block) {
+  const int64_t K = (size + block - 1) / block;
+  std::vector<int64_t> b(K + 1);
+  for (int64_t k = 0; k <= K; ++k) b[k] = (int64_t)(((__int128)k * size) / K);
+  return b;
+}
+
+// ---------------------------------------------------------------------------- one side --
+// The entries of S arranged for the updates of one factor.  For the W side the "rows" are the
+// m rows of S and the blocks split the n columns; for the H side the rows are the n columns of S
+// and the blocks split its m rows (the transposed problem).
+struct Side {
+  int64_t rows = 0, other = 0;
+  std::vector<int64_t> bounds;           // block bounds over `other`
+  std::vector<int64_t> entry_off;        // entries of block b: [entry_off[b], entry_off[b+1])
+  std::vector<int32_t> idx;              // index into `other`
+  std::vector<float> val;
+  std::vector<int64_t> item_off;         // items of block b
+  std::vector<Item> items;
+  std::vector<int64_t> split_off;        // split rows of block b
+  std::vector<Split> splits;
+  int64_t max_slots = 0;
+  // device copies
+  int32_t* d_idx = nullptr;
+  float* d_val = nullptr;
+  Item* d_items = nullptr;
+  Split* d_splits = nullptr;
+
+  int32_t nblk() const { return (int32_t)bounds.size() - 1; }
+};
+
+// ptr/idx/val: the rows of this side in compressed form (entries sorted within a row).
+void build_side(Side& sd, int64_t rows, int64_t other, const std::vector<int64_t>& bounds,
+                const int64_t* ptr, const int32_t* idx, const float* val) {
+  sd.rows = rows;
+  sd.other = other;
+  sd.bounds = bounds;
+  const int32_t nb = sd.nblk();
+  std::vector<int32_t> blk_of(other);
+  for (int32_t b = 0; b < nb; ++b)
+    for (int64_t j = bounds[b]; j < bounds[b + 1]; ++j) blk_of[j] = b;
+  std::vector<int64_t> cnt(nb, 0);
+  const int64_t nnz = ptr[rows];
+  for (int64_t e = 0; e < nnz; ++e) ++cnt[blk_of[idx[e]]];
+  sd.entry_off.assign(nb + 1, 0);
+  for (int32_t b = 0; b < nb; ++b) sd.entry_off[b + 1] = sd.entry_off[b] + cnt[b];
+  sd.idx.resize(nnz);
+  sd.val.resize(nnz);
+  std::vector<int64_t> cur(sd.entry_off.begin(), sd.entry_off.end() - 1);
+  std::vector<std::vector<Item>> items(nb);
+  std::vector<std::vector<Split>> splits(nb);
+  std::vector<int32_t> slots(nb, 0);
+  for (int64_t i = 0; i < rows; ++i) {
+    int64_t e = ptr[i];
+    const int64_t e1 = ptr[i + 1];
+    while (e < e1) {
+      const int32_t b = blk_of[idx[e]];
+      int64_t f = e;
+      while (f < e1 && idx[f] < bounds[b + 1]) ++f;
+      const int64_t count = f - e;
+      const int64_t base = cur[b];
+      std::memcpy(&sd.idx[base], idx + e, count * sizeof(int32_t));
+      std::memcpy(&sd.val[base], val + e, count * sizeof(float));
+      cur[b] += count;
+      if (count <= kItemChunk) {
+        items[b].push_back(Item{base, (int32_t)count, (int32_t)i, -1, 0});
+      } else {
+        const int32_t pieces = (int32_t)((count + kItemChunk - 1) / kItemChunk);
+        splits[b].push_back(Split{(int32_t)i, slots[b], pieces, 0});
+        for (int32_t p = 0; p < pieces; ++p) {
+          const int64_t s0 = (int64_t)p * kItemChunk;
+          const int64_t c = std::min<int64_t>(kItemChunk, count - s0);
+          items[b].push_back(Item{base + s0, (int32_t)c, (int32_t)i, slots[b] + p, 0});
+        }
+        slots[b] += pieces;
+      }
+      e = f;
+    }
+  }
+  sd.item_off.assign(nb + 1, 0);
+  sd.split_off.assign(nb + 1, 0);
+  sd.items.clear();
+  sd.splits.clear();
+  sd.max_slots = 0;
+  for (int32_t b = 0; b < nb; ++b) {
+    sd.item_off[b + 1] = sd.item_off[b] + (int64_t)items[b].size();
+    sd.split_off[b + 1] = sd.split_off[b] + (int64_t)splits[b].size();
+    sd.items.insert(sd.items.end(), items[b].begin(), items[b].end());
+    sd.splits.insert(sd.splits.end(), splits[b].begin(), splits[b].end());
+    sd.max_slots = std::max<int64_t>(sd.max_slots, slots[b]);
+  }
+}
+
+struct TimerRec {
+  hipEvent_t a, b;
+  int kind;
+  double flops, bytes;
+};
+
+}  // namespace
+
+struct nmd_ctx {
+  int64_t m = 0, n = 0;
+  int32_t r = 0, rp = 0;
+  int32_t block_m = 0, block_n = 0;
+  uint64_t seed = 0;
+  nmd_options opt{};
+  std::vector<int64_t> rb, cb;  // row and column block bounds
+  int64_t t = 0;
+  std::string err;
+
+  bool has_S = false;
+  int64_t nnz = 0;
+  double s_norm = 0.0;
+  Side ws, hs;  // W side (column blocks), H side (row blocks)
+  std::vector<int64_t> nnz_col_blocks, nnz_row_blocks;
+
+  // device state
+  bool dev_ready = false;
+  bool sparse_uploaded = false;
+  int device = -1;
+  float *A = nullptr, *B = nullptr, *VA = nullptr, *VB = nullptr;
+  float* Ypart = nullptr;
+  int64_t ypart_floats = 0;
+  float* scratch = nullptr;
+  int64_t scratch_floats = 0;
+  double *G = nullptr, *Gtmp = nullptr, *Gpart = nullptr;
+  int gram_chunks_max = 64;
+  double* objpart = nullptr;
+  int64_t objpart_count = 0;
+  double* objout = nullptr;
+  int* status = nullptr;
+  int* h_status = nullptr;   // pinned
+  double* h_obj = nullptr;   // pinned
+
+  // timing
+  std::vector<TimerRec> pending;
+  std::vector<hipEvent_t> event_pool;
+  double t_ms[K_COUNT] = {0, 0, 0, 0};
+  int64_t t_launch[K_COUNT] = {0, 0, 0, 0};
+  double t_flops[K_COUNT] = {0, 0, 0, 0};
+  double t_bytes[K_COUNT] = {0, 0, 0, 0};
+};
+
+namespace {
+
+int fail(nmd_ctx* c, int code, const char* fmt, ...) __attribute__((format(printf, 3, 4)));
+int fail(nmd_ctx* c, int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c)
+    c->err = buf;
+  else
+    g_create_error = buf;
+  return code;
+}
+
+#define HIP_TRY(ctx, expr)                                                                  \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return fail(ctx, NMD_EDEVICE, "%s failed: %s", #expr, hipGetErrorString(e_));         \
+  } while (0)
+
+template <class T>
+hipError_t dalloc(T** p, int64_t count) {
+  *p = nullptr;
+  if (count <= 0) count = 1;
+  return hipMalloc((void**)p, (size_t)count * sizeof(T));
+}
+
+template <class T>
+void dfree(T*& p) {
+  if (p) (void)hipFree(p);
+  p = nullptr;
+}
+
+void free_sparse_device(nmd_ctx* c) {
+  for (Side* sd : {&c->ws, &c->hs}) {
+    dfree(sd->d_idx);
+    dfree(sd->d_val);
+    dfree(sd->d_items);
+    dfree(sd->d_splits);
+  }
+  dfree(c->scratch);
+  dfree(c->objpart);
+  c->sparse_uploaded = false;
+}
+
+void free_device(nmd_ctx* c) {
+  free_sparse_device(c);
+  dfree(c->A);
+  dfree(c->B);
+  dfree(c->VA);
+  dfree(c->VB);
+  dfree(c->Ypart);
+  dfree(c->G);
+  dfree(c->Gtmp);
+  dfree(c->Gpart);
+  dfree(c->objout);
+  dfree(c->status);
+  if (c->h_status) (void)hipHostFree(c->h_status);
+  if (c->h_obj) (void)hipHostFree(c->h_obj);
+  c->h_status = nullptr;
+  c->h_obj = nullptr;
+  for (auto& rec : c->pending) {
+    (void)hipEventDestroy(rec.a);
+    (void)hipEventDestroy(rec.b);
+  }
+  c->pending.clear();
+  for (hipEvent_t e : c->event_pool) (void)hipEventDestroy(e);
+  c->event_pool.clear();
+  c->dev_ready = false;
+}
+
+int64_t nsplit_for(int64_t rows, int64_t blk, int rp) {
+  const int64_t rw = nmd::dense_rows_per_wg(rp);
+  const int64_t tiles = (rows + rw - 1) / rw;
+  int64_t s = std::max<int64_t>((blk + kSplitRows - 1) / kSplitRows, (kTargetWgs + tiles - 1) / tiles);
+  s = std::min<int64_t>(s, kMaxSplits);
+  s = std::min<int64_t>(s, std::max<int64_t>(1, blk / 16));
+  return std::max<int64_t>(s, 1);
+}
+
+int gram_chunks(int64_t blk) {
+  return (int)std::min<int64_t>(64, std::max<int64_t>(1, blk / 256));
+}
+
+int ensure_device(nmd_ctx* c) {
+  if (!c->dev_ready) {
+    int dev = 0;
+    HIP_TRY(c, hipGetDevice(&dev));
+    hipDeviceProp_t prop;
+    HIP_TRY(c, hipGetDeviceProperties(&prop, dev));
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+      return fail(c, NMD_EDEVICE, "device %d is %s; this library is built for gfx950", dev,
+                  prop.gcnArchName);
+    c->device = dev;
+    const int64_t rp = c->rp;
+    const int64_t mpad = c->m + 256, npad = c->n + 256;
+    if (dalloc(&c->A, mpad * rp) != hipSuccess || dalloc(&c->B, npad * rp) != hipSuccess ||
+        dalloc(&c->VA, mpad * rp) != hipSuccess || dalloc(&c->VB, npad * rp) != hipSuccess ||
+        dalloc(&c->G, rp * rp) != hipSuccess || dalloc(&c->Gtmp, rp * rp + 64 * 64) != hipSuccess ||
+        dalloc(&c->Gpart, (int64_t)c->gram_chunks_max * rp * rp) != hipSuccess ||
+        dalloc(&c->objout, 4) != hipSuccess || dalloc(&c->status, 2) != hipSuccess) {
+      free_device(c);
+      return fail(c, NMD_ENOMEM, "device allocation of the factor workspaces failed");
+    }
+    // Partial outputs: the largest (splits x rows) over W-steps, H-steps and full half-sweeps.
+    int64_t need = 0;
+    for (size_t k = 0; k + 1 < c->cb.size(); ++k) {
+      const int64_t blk = c->cb[k + 1] - c->cb[k];
+      need = std::max(need, nsplit_for(c->m, blk, c->rp) * c->m);
+    }
+    for (size_t k = 0; k + 1 < c->rb.size(); ++k) {
+      const int64_t blk = c->rb[k + 1] - c->rb[k];
+      need = std::max(need, nsplit_for(c->n, blk, c->rp) * c->n);
+    }
+    need = std::max(need, nsplit_for(c->m, c->n, c->rp) * c->m);
+    need = std::max(need, nsplit_for(c->n, c->m, c->rp) * c->n);
+    c->ypart_floats = need * rp;
+    if (dalloc(&c->Ypart, c->ypart_floats) != hipSuccess) {
+      free_device(c);
+      return fail(c, NMD_ENOMEM, "device allocation of %lld partial-output floats failed",
+                  (long long)c->ypart_floats);
+    }
+    if (hipHostMalloc((void**)&c->h_status, 2 * sizeof(int)) != hipSuccess ||
+        hipHostMalloc((void**)&c->h_obj, 4 * sizeof(double)) != hipSuccess) {
+      free_device(c);
+      return fail(c, NMD_ENOMEM, "pinned host allocation failed");
+    }
+    HIP_TRY(c, hipMemset(c->VA, 0, (size_t)mpad * rp * sizeof(float)));
+    HIP_TRY(c, hipMemset(c->VB, 0, (size_t)npad * rp * sizeof(float)));
+    HIP_TRY(c, hipMemset(c->A, 0, (size_t)mpad * rp * sizeof(float)));
+    HIP_TRY(c, hipMemset(c->B, 0, (size_t)npad * rp * sizeof(float)));
+    HIP_TRY(c, hipMemset(c->status, 0, sizeof(int)));
+    HIP_TRY(c, hipMemset(c->status + 1, 0x7f, sizeof(int)));
+    HIP_TRY(c, hipDeviceSynchronize());
+    c->dev_ready = true;
+  } else {
+    HIP_TRY(c, hipSetDevice(c->device));
+  }
+  if (c->has_S && !c->sparse_uploaded) {
+    for (Side* sd : {&c->ws, &c->hs}) {
+      const int64_t nz = (int64_t)sd->idx.size();
+      if (dalloc(&sd->d_idx, nz) != hipSuccess || dalloc(&sd->d_val, nz) != hipSuccess ||
+          dalloc(&sd->d_items, (int64_t)sd->items.size()) != hipSuccess ||
+          dalloc(&sd->d_splits, (int64_t)sd->splits.size()) != hipSuccess) {
+        free_sparse_device(c);
+        return fail(c, NMD_ENOMEM, "device allocation of the sparse structures failed");
+      }
+      HIP_TRY(c, hipMemcpy(sd->d_idx, sd->idx.data(), nz * sizeof(int32_t), hipMemcpyHostToDevice));
+      HIP_TRY(c, hipMemcpy(sd->d_val, sd->val.data(), nz * sizeof(float), hipMemcpyHostToDevice));
+      if (!sd->items.empty())
+        HIP_TRY(c, hipMemcpy(sd->d_items, sd->items.data(), sd->items.size() * sizeof(Item),
+                             hipMemcpyHostToDevice));
+      if (!sd->splits.empty())
+        HIP_TRY(c, hipMemcpy(sd->d_splits, sd->splits.data(), sd->splits.size() * sizeof(Split),
+                             hipMemcpyHostToDevice));
+    }
+    c->scratch_floats = std::max<int64_t>(1, std::max(c->ws.max_slots, c->hs.max_slots)) * c->rp;
+    // objective partials: dense workgroups or W-side items, whichever is larger
+    const int64_t dense_parts = (int64_t)nmd::dense_max_wgs(c->m, c->rp, 64);
+    c->objpart_count = std::max<int64_t>(dense_parts, (int64_t)c->ws.items.size()) + 1;
+    if (dalloc(&c->scratch, c->scratch_floats) != hipSuccess ||
+        dalloc(&c->objpart, c->objpart_count) != hipSuccess) {
+      free_sparse_device(c);
+      return fail(c, NMD_ENOMEM, "device allocation of the sparse scratch failed");
+    }
+    c->sparse_uploaded = true;
+  }
+  return NMD_OK;
+}
+
+// ---------------------------------------------------------------------------- timing --
+hipEvent_t take_event(nmd_ctx* c) {
+  if (!c->event_pool.empty()) {
+    hipEvent_t e = c->event_pool.back();
+    c->event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+struct Scope {
+  nmd_ctx* c;
+  hipStream_t st;
+  TimerRec rec{};
+  bool on;
+  Scope(nmd_ctx* c_, hipStream_t st_, int kind, double flops, double bytes)
+      : c(c_), st(st_), on((c_->opt.flags & NMD_FLAG_TIMING) != 0) {
+    if (!on) return;
+    rec.a = take_event(c);
+    rec.b = take_event(c);
+    rec.kind = kind;
+    rec.flops = flops;
+    rec.bytes = bytes;
+    if (!rec.a || !rec.b) {
+      on = false;
+      return;
+    }
+    (void)hipEventRecord(rec.a, st);
+  }
+  ~Scope() {
+    if (!on) return;
+    (void)hipEventRecord(rec.b, st);
+    c->pending.push_back(rec);
+  }
+};
+
+int collect_timing(nmd_ctx* c) {
+  for (auto& rec : c->pending) {
+    HIP_TRY(c, hipEventSynchronize(rec.b));
+    float ms = 0.f;
+    HIP_TRY(c, hipEventElapsedTime(&ms, rec.a, rec.b));
+    c->t_ms[rec.kind] += ms;
+    c->t_launch[rec.kind] += 1;
+    c->t_flops[rec.kind] += rec.flops;
+    c->t_bytes[rec.kind] += rec.bytes;
+    c->event_pool.push_back(rec.a);
+    c->event_pool.push_back(rec.b);
+  }
+  c->pending.clear();
+  return NMD_OK;
+}
+
+// ---------------------------------------------------------------------- one update step --
+// wstep: update A = W from column block `block` (all column blocks if block < 0); otherwise
+// update B = H^T from row block `block` (all row blocks if block < 0).
+int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, int step_id,
+                hipStream_t st) {
+  Side& sd = wstep ? c->ws : c->hs;
+  float* X = wstep ? c->A : c->B;
+  const float* P = wstep ? c->B : c->A;
+  float* V = wstep ? c->VA : c->VB;
+  const int64_t rows = wstep ? c->m : c->n;
+  const int64_t j0 = block >= 0 ? sd.bounds[block] : 0;
+  const int64_t j1 = block >= 0 ? sd.bounds[block + 1] : sd.other;
+  const int64_t blk = j1 - j0;
+  const int rp = c->rp;
+  const float* PJ = P + j0 * rp;
+
+  double* Gneg = nullptr;
+  {
+    Scope sc(c, st, K_FACTOR, 2.0 * blk * (double)c->r * c->r + 2.0 * (double)rp * rp * rp, 0.0);
+    HIP_TRY(c, nmd::launch_gram(PJ, blk, c->r, rp, c->Gpart, gram_chunks(blk), c->G, st));
+    HIP_TRY(c, nmd::launch_inverse(c->G, c->Gtmp, rp, c->status, step_id, &Gneg, st));
+  }
+  const int64_t ns = nsplit_for(rows, blk, rp);
+  const int64_t y_stride = rows * rp;
+  if (ns * y_stride > c->ypart_floats)
+    return fail(c, NMD_EDEVICE, "internal: partial-output buffer too small");
+  {
+    Scope sc(c, st, K_DENSE, 4.0 * rows * (double)blk * c->r, 4.0 * (2.0 * rows + blk) * c->r);
+    HIP_TRY(c, nmd::launch_dense(X, rows, PJ, blk, rp, c->Ypart, y_stride, (int)ns, st));
+  }
+  const int32_t b0 = block >= 0 ? block : 0;
+  const int32_t b1 = block >= 0 ? block + 1 : sd.nblk();
+  for (int32_t b = b0; b < b1; ++b) {
+    const int64_t ni = sd.item_off[b + 1] - sd.item_off[b];
+    const int64_t nsp = sd.split_off[b + 1] - sd.split_off[b];
+    const int64_t nz = sd.entry_off[b + 1] - sd.entry_off[b];
+    // algorithmic bytes: entries (index + value), each touched row of X and Y (read x, read
+    // and write y), each panel row of the block once
+    const double bytes = 8.0 * nz + 12.0 * (double)ni * c->r + 4.0 * blk * c->r;
+    Scope sc(c, st, K_SPARSE, 4.0 * nz * c->r, bytes);
+    HIP_TRY(c, nmd::launch_sparse(sd.d_items + sd.item_off[b], ni, sd.d_idx, sd.d_val, X, P, rp,
+                                  c->Ypart, c->scratch, st));
+    HIP_TRY(c, nmd::launch_fixup(sd.d_splits + sd.split_off[b], nsp, c->scratch, rp, c->Ypart, st));
+  }
+  {
+    Scope sc(c, st, K_APPLY, 2.0 * rows * (double)rp * rp, 4.0 * rows * rp * (ns + 4));
+    HIP_TRY(c, nmd::launch_apply(c->Ypart, y_stride, (int)ns, Gneg, X, V, rows, rp, eta, gamma,
+                                 c->status, step_id, st));
+  }
+  return NMD_OK;
+}
+
+int load_factors(nmd_ctx* c, const float* W, const float* H, hipStream_t st) {
+  HIP_TRY(c, nmd::launch_pad_rows(W, c->m, c->r, c->A, c->rp, st));
+  HIP_TRY(c, nmd::launch_transpose_in(H, c->r, c->n, c->B, c->rp, st));
+  return NMD_OK;
+}
+
+int store_factors(nmd_ctx* c, float* W, float* H, hipStream_t st) {
+  HIP_TRY(c, nmd::launch_unpad_rows(c->A, c->m, c->rp, W, c->r, st));
+  HIP_TRY(c, nmd::launch_transpose_out(c->B, c->rp, c->n, H, c->r, st));
+  return NMD_OK;
+}
+
+std::string describe_step(nmd_ctx* c, int step_id, int64_t first_sweep, int32_t steps_per) {
+  char buf[160];
+  if (steps_per <= 0) {
+    snprintf(buf, sizeof buf, "step %d", step_id);
+  } else {
+    snprintf(buf, sizeof buf, "sweep %lld, step %d", (long long)(first_sweep + step_id / steps_per),
+             step_id % steps_per);
+  }
+  (void)c;
+  return buf;
+}
+
+int finish(nmd_ctx* c, hipStream_t st, int64_t first_sweep, int32_t steps_per) {
+  if (c->opt.flags & NMD_FLAG_ASYNC) return NMD_OK;
+  HIP_TRY(c, hipMemcpyAsync(c->h_status, c->status, 2 * sizeof(int), hipMemcpyDeviceToHost, st));
+  HIP_TRY(c, hipStreamSynchronize(st));
+  const int flags = c->h_status[0];
+  if (flags == 0) return NMD_OK;
+  const int step = c->h_status[1];
+  HIP_TRY(c, hipMemsetAsync(c->status, 0, sizeof(int), st));
+  HIP_TRY(c, hipMemsetAsync(c->status + 1, 0x7f, sizeof(int), st));
+  HIP_TRY(c, hipStreamSynchronize(st));
+  const std::string where = describe_step(c, step, first_sweep, steps_per);
+  if (flags & 1)
+    return fail(c, NMD_ENOTPD, "Gram matrix not positive definite at %s; later steps skipped",
+                where.c_str());
+  return fail(c, NMD_ENONFINITE, "non-finite factor entry produced at %s; later steps skipped",
+              where.c_str());
+}
+
+int check_ready(nmd_ctx* c, const void* W, const void* H) {
+  if (!c) return NMD_EINVAL;
+  c->err.clear();
+  if (!W || !H) return fail(c, NMD_EINVAL, "W and H must be non-NULL device pointers");
+  if (!c->has_S) return fail(c, NMD_ESTATE, "nmd_set_sparse_csr has not been called");
+  return NMD_OK;
+}
+
+}  // namespace
+
+// =================================================================================== ABI ==
+extern "C" {
+
+int nmd_create(nmd_ctx** out, int64_t m, int64_t n, int32_t r, int32_t block_m, int32_t block_n,
+               uint64_t seed, const nmd_options* opts) {
+  g_create_error.clear();
+  if (!out) return fail(nullptr, NMD_EINVAL, "out must be non-NULL");
+  *out = nullptr;
+  if (m < 1 || n < 1 || m > INT32_MAX || n > INT32_MAX)
+    return fail(nullptr, NMD_EINVAL, "m and n must lie in [1, 2^31-1] (got %lld, %lld)",
+                (long long)m, (long long)n);
+  if (r < 1 || r > 512 || r > m || r > n)
+    return fail(nullptr, NMD_EINVAL, "rank r = %d must satisfy 1 <= r <= min(m, n, 512)", r);
+  if (block_m < 1 || block_n < 1)
+    return fail(nullptr, NMD_EINVAL, "block sizes must be >= 1");
+  nmd_options o{sizeof(nmd_options), NMD_DETERMINISTIC, 1.0f, 0.0f, 0u};
+  if (opts) {
+    if (opts->size < sizeof(nmd_options))
+      return fail(nullptr, NMD_EINVAL, "opts->size = %u is smaller than sizeof(nmd_options)",
+                  opts->size);
+    o = *opts;
+  }
+  if (o.mode != NMD_DETERMINISTIC && o.mode != NMD_STOCHASTIC)
+    return fail(nullptr, NMD_EINVAL, "unknown mode %d", o.mode);
+  if (!(o.eta >= 0.0f) || !std::isfinite(o.eta))
+    return fail(nullptr, NMD_EINVAL, "eta must be finite and >= 0");
+  if (!(o.momentum >= 0.0f && o.momentum < 1.0f))
+    return fail(nullptr, NMD_EINVAL, "momentum must lie in [0, 1)");
+  std::vector<int64_t> rb = balanced_bounds(m, block_m), cb = balanced_bounds(n, block_n);
+  int64_t min_rb = m, min_cb = n;
+  for (size_t k = 0; k + 1 < rb.size(); ++k) min_rb = std::min(min_rb, rb[k + 1] - rb[k]);
+  for (size_t k = 0; k + 1 < cb.size(); ++k) min_cb = std::min(min_cb, cb[k + 1] - cb[k]);
+  if (o.mode == NMD_STOCHASTIC && (r > min_rb || r > min_cb))
+    return fail(nullptr, NMD_EINVAL,
+                "rank %d exceeds the smallest block (%lld rows, %lld columns): singular Gram",
+                r, (long long)min_rb, (long long)min_cb);
+  nmd_ctx* c = new (std::nothrow) nmd_ctx();
+  if (!c) return fail(nullptr, NMD_ENOMEM, "context allocation failed");
+  c->m = m;
+  c->n = n;
+  c->r = r;
+  c->rp = nmd::padded_rank(r);
+  c->block_m = block_m;
+  c->block_n = block_n;
+  c->seed = seed;
+  c->opt = o;
+  c->rb = std::move(rb);
+  c->cb = std::move(cb);
+  *out = c;
+  return NMD_OK;
+}
+
+int nmd_set_sparse_csr(nmd_ctx* c, int64_t nnz, const int64_t* row_ptr, const int32_t* col_idx,
+                       const float* values) {
+  if (!c) return NMD_EINVAL;
+  c->err.clear();
+  if (nnz < 0) return fail(c, NMD_EINVAL, "nnz must be >= 0");
+  if (!row_ptr) return fail(c, NMD_EINVAL, "row_ptr must be non-NULL");
+  if (nnz > 0 && (!col_idx || !values))
+    return fail(c, NMD_EINVAL, "col_idx and values must be non-NULL when nnz > 0");
+  if (nnz >= INT32_MAX) return fail(c, NMD_EINVAL, "nnz must be < 2^31-1");
+  const int64_t m = c->m, n = c->n;
+  if (row_ptr[0] != 0) return fail(c, NMD_EINVAL, "row_ptr[0] = %lld, expected 0", (long long)row_ptr[0]);
+  for (int64_t i = 0; i < m; ++i)
+    if (row_ptr[i + 1] < row_ptr[i])
+      return fail(c, NMD_EINVAL, "row_ptr decreases at row %lld", (long long)i);
+  if (row_ptr[m] != nnz)
+    return fail(c, NMD_EINVAL, "row_ptr[m] = %lld differs from nnz = %lld", (long long)row_ptr[m],
+                (long long)nnz);
+  for (int64_t i = 0; i < m; ++i) {
+    for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+      const int32_t j = col_idx[e];
+      if (j < 0 || j >= n)
+        return fail(c, NMD_EINVAL, "column index %d out of range in row %lld", j, (long long)i);
+      if (e > row_ptr[i] && j <= col_idx[e - 1])
+        return fail(c, NMD_EINVAL, "column indices not strictly increasing in row %lld",
+                    (long long)i);
+      const float v = values[e];
+      if (!std::isfinite(v) || v < 0.0f)
+        return fail(c, NMD_EINVAL, "value at row %lld, column %d is negative or not finite",
+                    (long long)i, j);
+    }
+  }
+  // keep the positive entries only (the mask of the Z-update is S_ij > 0)
+  std::vector<int64_t> ptr(m + 1, 0);
+  std::vector<int32_t> col;
+  std::vector<float> val;
+  col.reserve(nnz);
+  val.reserve(nnz);
+  double s2 = 0.0;
+  for (int64_t i = 0; i < m; ++i) {
+    for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+      if (values[e] > 0.0f) {
+        col.push_back(col_idx[e]);
+        val.push_back(values[e]);
+        s2 += (double)values[e] * values[e];
+      }
+    }
+    ptr[i + 1] = (int64_t)col.size();
+  }
+  const int64_t nz = (int64_t)col.size();
+  if (nz == 0) return fail(c, NMD_EINVAL, "S has no positive entry");
+  // column-compressed copy for the H side (rows ascending inside each column)
+  std::vector<int64_t> cptr(n + 1, 0);
+  for (int64_t e = 0; e < nz; ++e) ++cptr[col[e] + 1];
+  for (int64_t j = 0; j < n; ++j) cptr[j + 1] += cptr[j];
+  std::vector<int32_t> crow(nz);
+  std::vector<float> cval(nz);
+  {
+    std::vector<int64_t> cur(cptr.begin(), cptr.end() - 1);
+    for (int64_t i = 0; i < m; ++i)
+      for (int64_t e = ptr[i]; e < ptr[i + 1]; ++e) {
+        const int64_t d = cur[col[e]]++;
+        crow[d] = (int32_t)i;
+        cval[d] = val[e];
+      }
+  }
+  free_sparse_device(c);
+  c->has_S = false;
+  try {
+    build_side(c->ws, m, n, c->cb, ptr.data(), col.data(), val.data());
+    build_side(c->hs, n, m, c->rb, cptr.data(), crow.data(), cval.data());
+  } catch (const std::bad_alloc&) {
+    return fail(c, NMD_ENOMEM, "host allocation failed while arranging S");
+  }
+  c->nnz_col_blocks.assign(c->ws.nblk(), 0);
+  c->nnz_row_blocks.assign(c->hs.nblk(), 0);
+  for (int32_t b = 0; b < c->ws.nblk(); ++b)
+    c->nnz_col_blocks[b] = c->ws.entry_off[b + 1] - c->ws.entry_off[b];
+  for (int32_t b = 0; b < c->hs.nblk(); ++b)
+    c->nnz_row_blocks[b] = c->hs.entry_off[b + 1] - c->hs.entry_off[b];
+  c->nnz = nz;
+  c->s_norm = std::sqrt(s2);
+  c->has_S = true;
+  return NMD_OK;
+}
+
+static int run(nmd_ctx* c, float* W, float* H, const std::vector<std::vector<int32_t>>& lists,
+               bool full_halves, hipStream_t st) {
+  int rc = ensure_device(c);
+  if (rc) return rc;
+  if ((rc = load_factors(c, W, H, st))) return rc;
+  int step_id = 0;
+  for (const auto& list : lists) {
+    if (full_halves) {
+      if ((rc = factor_step(c, true, -1, c->opt.eta, c->opt.momentum, step_id, st))) return rc;
+      step_id += (int)c->ws.nblk();
+      if ((rc = factor_step(c, false, -1, c->opt.eta, c->opt.momentum, step_id, st))) return rc;
+      step_id += (int)c->hs.nblk();
+      continue;
+    }
+    for (int32_t code : list) {
+      const bool w = code > 0;
+      const int32_t b = (w ? code : -code) - 1;
+      if ((rc = factor_step(c, w, b, c->opt.eta, c->opt.momentum, step_id, st))) return rc;
+      ++step_id;
+    }
+  }
+  return store_factors(c, W, H, st);
+}
+
+int nmd_als_block_sweep(nmd_ctx* c, float* W, float* H, int32_t n_sweeps, void* hip_stream) {
+  int rc = check_ready(c, W, H);
+  if (rc) return rc;
+  if (n_sweeps < 1) return fail(c, NMD_EINVAL, "n_sweeps must be >= 1");
+  hipStream_t st = (hipStream_t)hip_stream;
+  const bool sto = c->opt.mode == NMD_STOCHASTIC;
+  std::vector<std::vector<int32_t>> lists;
+  for (int32_t s = 0; s < n_sweeps; ++s)
+    lists.push_back(make_schedule(c->seed, c->t + s, c->hs.nblk(), c->ws.nblk(), sto));
+  const int64_t first = c->t;
+  rc = run(c, W, H, lists, !sto, st);
+  if (rc) return rc;
+  c->t += n_sweeps;
+  return finish(c, st, first, c->hs.nblk() + c->ws.nblk());
+}
+
+int nmd_run_steps(nmd_ctx* c, float* W, float* H, const int32_t* steps, int32_t n_steps,
+                  void* hip_stream) {
+  int rc = check_ready(c, W, H);
+  if (rc) return rc;
+  if (n_steps < 0 || (n_steps > 0 && !steps)) return fail(c, NMD_EINVAL, "bad step list");
+  for (int32_t k = 0; k < n_steps; ++k) {
+    const int32_t code = steps[k];
+    if (code == 0 || (code > 0 && code > c->ws.nblk()) || (code < 0 && -code > c->hs.nblk()))
+      return fail(c, NMD_EINVAL, "step code %d out of range", code);
+  }
+  std::vector<std::vector<int32_t>> lists(1, std::vector<int32_t>(steps, steps + n_steps));
+  rc = run(c, W, H, lists, false, (hipStream_t)hip_stream);
+  if (rc) return rc;
+  return finish(c, (hipStream_t)hip_stream, 0, 0);
+}
+
+int nmd_objective(nmd_ctx* c, const float* W, const float* H, double* out_obj, void* hip_stream) {
+  int rc = check_ready(c, W, H);
+  if (rc) return rc;
+  if (!out_obj) return fail(c, NMD_EINVAL, "out_obj must be non-NULL");
+  hipStream_t st = (hipStream_t)hip_stream;
+  if ((rc = ensure_device(c))) return rc;
+  if ((rc = load_factors(c, W, H, st))) return rc;
+  int ndense = 0;
+  HIP_TRY(c, nmd::launch_obj_dense(c->A, c->m, c->B, c->n, c->rp, c->objpart, &ndense, st));
+  if (ndense + 1 > c->objpart_count) return fail(c, NMD_EDEVICE, "internal: objective buffer");
+  HIP_TRY(c, nmd::launch_sum(c->objpart, ndense, c->objout, st));
+  // sparse part over every column block, one partial per item
+  const Side& sd = c->ws;
+  const int64_t ni = (int64_t)sd.items.size();
+  HIP_TRY(c, nmd::launch_obj_sparse(sd.d_items, ni, sd.d_idx, sd.d_val, c->A, c->B, c->rp,
+                                    c->objpart, st));
+  HIP_TRY(c, nmd::launch_sum(c->objpart, ni, c->objout + 1, st));
+  HIP_TRY(c, hipMemcpyAsync(c->h_obj, c->objout, 2 * sizeof(double), hipMemcpyDeviceToHost, st));
+  HIP_TRY(c, hipStreamSynchronize(st));
+  double tot = c->h_obj[0] + c->h_obj[1];
+  if (tot < 0.0) tot = 0.0;
+  *out_obj = std::sqrt(tot) / c->s_norm;
+  return NMD_OK;
+}
+
+void nmd_destroy(nmd_ctx* c) {
+  if (!c) return;
+  if (c->dev_ready) (void)hipSetDevice(c->device);
+  free_device(c);
+  delete c;
+}
+
+const char* nmd_last_error(const nmd_ctx* c) {
+  return c ? c->err.c_str() : g_create_error.c_str();
+}
+
+int nmd_get_schedule(const nmd_ctx* c, int64_t sweep, int32_t* out, int64_t cap) {
+  if (!c || !out || sweep < 0) return NMD_EINVAL;
+  const int32_t R = (int32_t)c->rb.size() - 1, C = (int32_t)c->cb.size() - 1;
+  if (cap < (int64_t)R + C) return NMD_EINVAL;
+  const std::vector<int32_t> s = make_schedule(c->seed, sweep, R, C, c->opt.mode == NMD_STOCHASTIC);
+  std::copy(s.begin(), s.end(), out);
+  return (int)s.size();
+}
+
+int nmd_get_block_nnz(const nmd_ctx* c, int32_t side, int64_t* out, int64_t cap) {
+  if (!c || !out || (side != 0 && side != 1)) return NMD_EINVAL;
+  if (!c->has_S) return NMD_ESTATE;
+  const std::vector<int64_t>& v = side == 0 ? c->nnz_col_blocks : c->nnz_row_blocks;
+  if (cap < (int64_t)v.size()) return NMD_EINVAL;
+  std::copy(v.begin(), v.end(), out);
+  return (int)v.size();
+}
+
+int nmd_get_block_bounds(const nmd_ctx* c, int32_t side, int64_t* out, int64_t cap) {
+  if (!c || !out || (side != 0 && side != 1)) return NMD_EINVAL;
+  const std::vector<int64_t>& v = side == 0 ? c->cb : c->rb;
+  if (cap < (int64_t)v.size()) return NMD_EINVAL;
+  std::copy(v.begin(), v.end(), out);
+  return (int)v.size();
+}
+
+int nmd_reset(nmd_ctx* c) {
+  if (!c) return NMD_EINVAL;
+  c->err.clear();
+  c->t = 0;
+  if (c->dev_ready) {
+    HIP_TRY(c, hipSetDevice(c->device));
+    HIP_TRY(c, hipDeviceSynchronize());
+    HIP_TRY(c, hipMemset(c->VA, 0, (size_t)(c->m + 256) * c->rp * sizeof(float)));
+    HIP_TRY(c, hipMemset(c->VB, 0, (size_t)(c->n + 256) * c->rp * sizeof(float)));
+    HIP_TRY(c, hipDeviceSynchronize());
+  }
+  return NMD_OK;
+}
+
+int nmd_get_sweep_count(const nmd_ctx* c, int64_t* t) {
+  if (!c || !t) return NMD_EINVAL;
+  *t = c->t;
+  return NMD_OK;
+}
+
+int nmd_clamped_contraction(const float* A, int64_t rows, const float* B, int64_t blk, int32_t r,
+                            float* Y, void* hip_stream) {
+  g_create_error.clear();
+  if (!A || !B || !Y) return fail(nullptr, NMD_EINVAL, "A, B and Y must be non-NULL");
+  if (rows < 1 || blk < 1 || rows > INT32_MAX)
+    return fail(nullptr, NMD_EINVAL, "rows and blk must be >= 1");
+  if (r < 16 || r > 512 || nmd::padded_rank(r) != r)
+    return fail(nullptr, NMD_EINVAL,
+                "r = %d unsupported: use 16, 32, 48, 64 or a multiple of 64 up to 512", r);
+  hipError_t e = nmd::launch_dense(A, rows, B, blk, r, Y, 0, 1, (hipStream_t)hip_stream);
+  if (e != hipSuccess) return fail(nullptr, NMD_EDEVICE, "launch failed: %s", hipGetErrorString(e));
+  return NMD_OK;
+}
+
+int nmd_get_kernel_timing(nmd_ctx* c, int32_t kernel, double* total_ms, int64_t* launches,
+                          double* flops, double* bytes, int32_t reset) {
+  if (!c || kernel < 0 || kernel >= K_COUNT) return NMD_EINVAL;
+  int rc = collect_timing(c);
+  if (rc) return rc;
+  if (total_ms) *total_ms = c->t_ms[kernel];
+  if (launches) *launches = c->t_launch[kernel];
+  if (flops) *flops = c->t_flops[kernel];
+  if (bytes) *bytes = c->t_bytes[kernel];
+  if (reset) {
+    for (int k = 0; k < K_COUNT; ++k) {
+      c->t_ms[k] = 0;
+      c->t_launch[k] = 0;
+      c->t_flops[k] = 0;
+      c->t_bytes[k] = 0;
+    }
+  }
+  return NMD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,78 @@
+// Internal declarations shared by the host driver and the HIP kernels of libnmd.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace nmd {
+
+// One unit of sparse work: `count` consecutive entries (begin .. begin+count) of one row of a
+// block.  slot < 0: the row has a single item and its result is added to Y directly; else the
+// partial result goes to scratch row `slot` and a fix-up pass adds the row's slots in order.
+struct Item {
+  int64_t begin;
+  int32_t count;
+  int32_t row;
+  int32_t slot;
+  int32_t pad;
+};
+
+// A row whose entries were split over several items: slots first .. first+nslots-1.
+struct Split {
+  int32_t row;
+  int32_t first;
+  int32_t nslots;
+  int32_t pad;
+};
+
+// Padded rank: the kernels work on r_p columns (zeros beyond r).
+int padded_rank(int r);
+// Rows per workgroup of the dense kernel for padded rank rp.
+int dense_rows_per_wg(int rp);
+
+// Y_s = min(0, X P^T) P over the split s of the rows of P (rows of X: `rows`).  Ypart holds
+// nsplit buffers of y_stride floats each (row-major rows x rp).
+hipError_t launch_dense(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
+                        float* Ypart, int64_t y_stride, int nsplit, hipStream_t st);
+
+// Sparse correction: for every item, y_row += sum over its entries of (s - min(0, x_row . p_j)) p_j.
+hipError_t launch_sparse(const Item* items, int64_t nitems, const int32_t* idx, const float* val,
+                         const float* X, const float* P, int rp, float* Y, float* scratch,
+                         hipStream_t st);
+hipError_t launch_fixup(const Split* splits, int64_t nsplits, const float* scratch, int rp,
+                        float* Y, hipStream_t st);
+
+// Gram matrix G = P^T P (fp64, rp x rp, identity on the padded diagonal) of `blk` rows.
+hipError_t launch_gram(const float* P, int64_t blk, int r, int rp, double* Gpart, int nchunks,
+                       double* G, hipStream_t st);
+// Gsw <- -G^-1 by block sweeps; flags status on a non-positive pivot.  Gtmp: scratch rp x rp.
+hipError_t launch_inverse(double* G, double* Gtmp, int rp, int* status, int step_id,
+                          double** result, hipStream_t st);
+// X <- X + V, V <- gamma V + eta (Ysum (-Gneg) - X), Ysum = sum of the nsplit partial outputs.
+hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const double* Gneg,
+                        float* X, float* V, int64_t rows, int rp, float eta, float gamma,
+                        int* status, int step_id, hipStream_t st);
+
+// Layout helpers between the caller's W (m x r), H (r x n) and the padded panels.
+hipError_t launch_pad_rows(const float* src, int64_t rows, int r, float* dst, int rp,
+                           hipStream_t st);
+hipError_t launch_unpad_rows(const float* src, int64_t rows, int rp, float* dst, int r,
+                             hipStream_t st);
+hipError_t launch_transpose_in(const float* H, int r, int64_t n, float* B, int rp,
+                               hipStream_t st);
+hipError_t launch_transpose_out(const float* B, int rp, int64_t n, float* H, int r,
+                                hipStream_t st);
+hipError_t launch_zero(float* p, int64_t count, hipStream_t st);
+
+// Objective pieces.  Dense: per-workgroup fp64 sums of max(0, L)^2 over all (i, j) of X P^T.
+hipError_t launch_obj_dense(const float* X, int64_t rows, const float* P, int64_t cols, int rp,
+                            double* partial, int* npartial, hipStream_t st);
+// Sparse: per-item fp64 sums of (s - l)^2 - max(0, l)^2, l = x_row . p_j.
+hipError_t launch_obj_sparse(const Item* items, int64_t nitems, const int32_t* idx,
+                             const float* val, const float* X, const float* P, int rp,
+                             double* partial, hipStream_t st);
+hipError_t launch_sum(const double* partial, int64_t count, double* out, hipStream_t st);
+
+int dense_max_wgs(int64_t rows, int rp, int nsplit);
+
+}  // namespace nmd

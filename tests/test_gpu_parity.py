@@ -1,0 +1,279 @@
+"""GPU parity: libnmd (HIP, gfx950) against the fp64 oracle on the same seeded fp32 inputs.
+
+Bars:
+  * the block schedule and the per-block nonzero counts: bit-exact (checked on the host side
+    in test_abi_host.py, repeated here for the GPU workloads);
+  * W, H after one sweep and the objective: relative Frobenius error <= 1e-4;
+  * the standalone clamped contraction (one fp32 accumulation, no solve): <= 2e-5.
+Every test prints the case it runs before touching the GPU.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import partition, salsa, schedule
+from workloads import gen
+
+import paper_2608_21607_amd as nmd
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def rel(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
+
+
+def make_ctx(p, mode=None, eta=None, mom=None, seed=None, flags=0):
+    ctx = nmd.Context(p.m, p.n, p.r, p.block_m, p.block_n, seed=p.seed if seed is None else seed,
+                      mode=p.mode if mode is None else mode, eta=p.eta if eta is None else eta,
+                      momentum=p.momentum if mom is None else mom, flags=flags)
+    ctx.set_sparse_csr(p.row_ptr, p.col, p.val)
+    return ctx
+
+
+def gpu_run(p, sweeps, W0=None, H0=None, **kw):
+    ctx = make_ctx(p, **kw)
+    W = dev(p.W0 if W0 is None else W0)
+    H = dev(p.H0 if H0 is None else H0)
+    ctx.sweep(W, H, sweeps)
+    torch.cuda.synchronize()
+    return W.cpu().numpy(), H.cpu().numpy(), ctx
+
+
+def oracle_run(p, sweeps, W0=None, H0=None, mode=None, eta=None, mom=None, seed=None):
+    S = salsa.csr_matrix(p.m, p.n, p.row_ptr, p.col, p.val)
+    st = salsa.State(p.W0 if W0 is None else W0, p.H0 if H0 is None else H0)
+    ST = S.T.tocsr()
+    for _ in range(sweeps):
+        salsa.sweep(S, ST, st, p.block_m, p.block_n, p.seed if seed is None else seed,
+                    mode=p.mode if mode is None else mode, eta=p.eta if eta is None else eta,
+                    gamma=p.momentum if mom is None else mom)
+    return st.W, st.H, S
+
+
+def test_gpu_is_gfx950():
+    assert torch.cuda.is_available()
+    name = torch.cuda.get_device_properties(0).gcnArchName
+    assert name.startswith("gfx950"), name
+
+
+# ------------------------------------------------------------------ the dense kernel alone
+@pytest.mark.parametrize("r", [16, 32, 48, 64, 128, 192, 256, 320, 384, 448, 512])
+def test_clamped_contraction_kernel(r):
+    rows, blk = 333 + r % 7, 517
+    _say("clamped_contraction", rows, blk, r)
+    g = np.random.default_rng(r)
+    A = g.standard_normal((rows, r)).astype(np.float32)
+    B = g.standard_normal((blk, r)).astype(np.float32)
+    Y = nmd.clamped_contraction(dev(A), dev(B))
+    torch.cuda.synchronize()
+    want = salsa.clamped_contraction(A, B)
+    assert rel(Y.cpu().numpy(), want) < 2e-5
+
+
+@pytest.mark.parametrize("r", [16, 32, 64, 128])
+def test_clamped_contraction_paper_shape_sampled(r):
+    """The kernel at the shape of the paper's throughput table (A: 250000 x r, B: 2500 x r);
+    64 sampled output rows against the oracle."""
+    rows, blk = 250_000, 2500
+    _say("clamped_contraction paper shape", rows, blk, r)
+    g = torch.Generator(device="cuda").manual_seed(r)
+    A = torch.randn((rows, r), generator=g, device="cuda")
+    B = torch.randn((blk, r), generator=g, device="cuda")
+    Y = nmd.clamped_contraction(A, B)
+    torch.cuda.synchronize()
+    idx = np.random.default_rng(r).choice(rows, 64, replace=False)
+    want = salsa.clamped_contraction(A[idx].cpu().numpy(), B.cpu().numpy())
+    assert rel(Y[idx].cpu().numpy(), want) < 2e-5
+
+
+# -------------------------------------------------------------- whole sweeps, small problems
+def test_config1_deterministic_three_sweeps():
+    p = gen.config(1)
+    _say("config 1 deterministic, 3 sweeps")
+    Wg, Hg, ctx = gpu_run(p, 1)
+    Wo, Ho, S = oracle_run(p, 1)
+    assert rel(Wg, Wo) < TOL and rel(Hg, Ho) < TOL
+    Wg3, Hg3, ctx3 = gpu_run(p, 3)
+    Wo3, Ho3, _ = oracle_run(p, 3)
+    assert rel(Wg3, Wo3) < 3 * TOL and rel(Hg3, Ho3) < 3 * TOL
+    f_gpu = ctx3.objective(dev(Wg3), dev(Hg3))
+    f_orc = salsa.objective(S, Wg3, Hg3)
+    assert abs(f_gpu - f_orc) <= TOL * f_orc
+    f0 = ctx3.objective(dev(p.W0), dev(p.H0))
+    assert abs(f0 - salsa.objective(S, p.W0, p.H0)) <= TOL * f0
+    assert f_gpu < f0
+    assert ctx3.sweep_count == 3
+
+
+def test_deterministic_objective_monotone_on_gpu():
+    p = gen.config(1)
+    _say("config 1 monotone over 6 sweeps")
+    ctx = make_ctx(p)
+    W, H = dev(p.W0), dev(p.H0)
+    f = ctx.objective(W, H)
+    for _ in range(6):
+        ctx.sweep(W, H, 1)
+        f1 = ctx.objective(W, H)
+        assert f1 <= f * (1 + 1e-5)
+        f = f1
+
+
+@pytest.mark.parametrize("n", [256, 4096])
+def test_identity_exact_completion(n):
+    """Corollary 1: the rank-3 completion of I_n is an exact fixed point.  In fp32 its
+    objective is not zero (entries of size n^2/pi^2 cancel), so the GPU objective is compared
+    with the oracle's objective at the same fp32-rounded factors."""
+    _say("identity exact factors", n)
+    W, H = gen.identity_exact_factors(n, np.float32)
+    row_ptr, col, val = gen.identity(n)
+    p = gen.Problem("identity", n, n, 3, row_ptr, col, val, W, H, min(1024, n), min(1024, n))
+    Wg, Hg, ctx = gpu_run(p, 1)
+    Wo, Ho, S = oracle_run(p, 1)
+    assert rel(Wg, Wo) < TOL and rel(Hg, Ho) < TOL
+    assert rel(Wg, W) < 1e-3 and rel(Hg, H) < 1e-3  # stays at the fixed point
+    f_gpu = ctx.objective(dev(W), dev(H))
+    f_orc = salsa.objective(S, W, H)
+    assert f_orc < 0.1
+    assert f_gpu <= 2.0 * f_orc + 1e-6 and f_gpu >= 0.5 * f_orc - 1e-6
+
+
+def test_config2_identity_random_init():
+    p = gen.config(2)
+    _say("config 2 identity, random init, 1 sweep")
+    Wg, Hg, ctx = gpu_run(p, 1)
+    Wo, Ho, S = oracle_run(p, 1)
+    assert rel(Wg, Wo) < TOL and rel(Hg, Ho) < TOL
+    f_gpu = ctx.objective(dev(Wg), dev(Hg))
+    assert abs(f_gpu - salsa.objective(S, Wg, Hg)) <= TOL * f_gpu
+
+
+@pytest.mark.parametrize("eta,mom", [(1.0, 0.0), (1.0, 0.9), (0.5, 0.0), (0.5, 0.9)])
+def test_stochastic_planted_reduced(eta, mom):
+    p = gen.config(3, scale=0.125)  # 4096 x 4096, r = 64
+    p.block_m = p.block_n = 512
+    _say("config 3 reduced, stochastic", eta, mom)
+    Wg, Hg, ctx = gpu_run(p, 1, eta=eta, mom=mom)
+    Wo, Ho, S = oracle_run(p, 1, eta=eta, mom=mom)
+    assert rel(Wg, Wo) < TOL and rel(Hg, Ho) < TOL
+    R, C = partition.num_blocks(p.m, 512), partition.num_blocks(p.n, 512)
+    assert ctx.schedule(0) == schedule.sweep_schedule(p.seed, 0, R, C, True)
+
+
+def test_stochastic_three_sweeps_and_persistent_state():
+    """Sweeps run in one call equal the same sweeps run one call at a time (the sweep counter
+    and the momentum persist); after reset the first sweep repeats bit for bit."""
+    p = gen.config(3, scale=0.0625)
+    p.block_m = p.block_n = 512
+    _say("persistent state", p.m, p.n)
+    W1, H1, _ = gpu_run(p, 3)
+    ctx = make_ctx(p)
+    W, H = dev(p.W0), dev(p.H0)
+    for _ in range(3):
+        ctx.sweep(W, H, 1)
+    assert np.array_equal(W.cpu().numpy(), W1) and np.array_equal(H.cpu().numpy(), H1)
+    Wo, Ho, _ = oracle_run(p, 3)
+    assert rel(W1, Wo) < 3 * TOL and rel(H1, Ho) < 3 * TOL
+    ctx.reset()
+    W, H = dev(p.W0), dev(p.H0)
+    ctx.sweep(W, H, 1)
+    Wa, Ha, _ = gpu_run(p, 1)
+    assert np.array_equal(W.cpu().numpy(), Wa) and np.array_equal(H.cpu().numpy(), Ha)
+
+
+ODD = [
+    # m, n, r, block_m, block_n, mode, eta, mom, extras
+    (37, 53, 1, 10, 13, "stochastic", 1.0, 0.0, {}),
+    (100, 77, 3, 33, 20, "stochastic", 0.5, 0.9, {"empty_rows": 3, "empty_cols": 2}),
+    (129, 300, 8, 64, 100, "deterministic", 1.0, 0.0, {"heavy_row_frac": 0.5}),
+    (257, 65, 17, 100, 33, "stochastic", 1.0, 0.9, {}),
+    (300, 410, 64, 150, 205, "stochastic", 1.0, 0.9, {"heavy_row_frac": 0.5}),
+    (333, 290, 100, 333, 290, "deterministic", 1.0, 0.0, {"empty_rows": 5}),
+    (700, 600, 256, 350, 300, "stochastic", 1.0, 0.9, {}),
+    (1100, 900, 512, 550, 900, "stochastic", 1.0, 0.0, {"heavy_row_frac": 0.3}),
+]
+
+
+@pytest.mark.parametrize("case", ODD, ids=[f"{c[0]}x{c[1]}r{c[2]}" for c in ODD])
+def test_odd_shapes(case):
+    m, n, r, bm, bn, mode, eta, mom, extras = case
+    _say("odd shape", case)
+    row_ptr, col, val = gen.random_sparse(m, n, 0.05, m + n + r, **extras)
+    W0, H0 = gen.sign_constrained_init(m, n, r, float(val.mean()), r)
+    p = gen.Problem("odd", m, n, r, row_ptr, col, val, W0, H0, bm, bn, mode, eta, mom, 7)
+    Wg, Hg, ctx = gpu_run(p, 1)
+    Wo, Ho, S = oracle_run(p, 1)
+    assert rel(Wg, Wo) < TOL and rel(Hg, Ho) < TOL
+    f = ctx.objective(dev(Wg), dev(Hg))
+    assert abs(f - salsa.objective(S, Wg, Hg)) <= TOL * f
+
+
+def test_bitwise_determinism():
+    p = gen.config(3, scale=0.0625)
+    p.block_m = p.block_n = 256
+    _say("determinism")
+    W1, H1, _ = gpu_run(p, 2)
+    W2, H2, _ = gpu_run(p, 2)
+    assert np.array_equal(W1, W2) and np.array_equal(H1, H2)
+
+
+# ------------------------------------------------------------------------------ error paths
+def test_nonfinite_input_is_reported():
+    p = gen.config(1)
+    p.mode = "stochastic"
+    _say("NaN in W")
+    W0 = p.W0.copy()
+    W0[5, 2] = np.nan
+    ctx = make_ctx(p)
+    W, H = dev(W0), dev(p.H0)
+    with pytest.raises(nmd.NmdError) as e:
+        ctx.sweep(W, H, 1)
+    assert e.value.code == -6 and "sweep 0" in e.value.message
+
+
+def test_singular_gram_is_reported_and_later_steps_skipped():
+    p = gen.config(1)
+    p.mode = "stochastic"
+    _say("zero column block of H")
+    H0 = p.H0.copy()
+    first = gen_first_w_block(p)
+    H0[:, first[0]:first[1]] = 0.0  # the first W-step's Gram matrix is zero
+    ctx = make_ctx(p)
+    W, H = dev(p.W0), dev(H0)
+    with pytest.raises(nmd.NmdError) as e:
+        ctx.sweep(W, H, 1)
+    assert e.value.code == -4 and "step 0" in e.value.message
+    assert np.array_equal(W.cpu().numpy(), p.W0)
+    assert np.array_equal(H.cpu().numpy(), H0)
+
+
+def gen_first_w_block(p):
+    R, C = partition.num_blocks(p.m, p.block_m), partition.num_blocks(p.n, p.block_n)
+    code = schedule.sweep_schedule(p.seed, 0, R, C, True)[0]
+    assert code > 0
+    b = partition.bounds(p.n, p.block_n)
+    return b[code - 1], b[code]
+
+
+def test_bad_tensor_arguments():
+    p = gen.config(1)
+    ctx = make_ctx(p)
+    with pytest.raises(ValueError):
+        ctx.sweep(dev(p.W0.T), dev(p.H0), 1)
+    with pytest.raises(TypeError):
+        ctx.sweep(torch.from_numpy(p.W0), dev(p.H0), 1)
