@@ -18,7 +18,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnmd.so")
-SOURCES = ["host.cpp", "dense.hip", "sparse.hip", "solve.hip", "layout.hip"]
+SOURCES = ["host.cpp", "dense.hip", "objective.hip", "sparse.hip", "solve.hip", "layout.hip"]
 ARCH = "gfx950"
 
 # Packed-fp32 instructions are kept out of the generated code on purpose.

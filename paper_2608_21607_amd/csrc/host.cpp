@@ -31,6 +31,7 @@ constexpr int kItemChunk = 128;    // entries per sparse work item
 constexpr int kMaxSplits = 16;     // partial outputs of the dense kernel
 constexpr int64_t kSplitRows = 1024;  // at most this many panel rows per fp32 accumulation
 constexpr int64_t kTargetWgs = 2048;  // dense workgroups wanted per launch (256 CUs)
+constexpr int kObjSubMax = 16;        // sub-splits of a column block in the objective
 
 enum { K_DENSE = 0, K_SPARSE = 1, K_FACTOR = 2, K_APPLY = 3, K_COUNT = 4 };
 
@@ -117,12 +118,15 @@ struct Side {
   std::vector<Item> items;
   std::vector<int64_t> split_off;        // split rows of block b
   std::vector<Split> splits;
+  std::vector<int64_t> rowptr;           // block b, row i: entries [rowptr[b(rows+1)+i], ..+1])
   int64_t max_slots = 0;
   // device copies
   int32_t* d_idx = nullptr;
   float* d_val = nullptr;
   Item* d_items = nullptr;
   Split* d_splits = nullptr;
+  int64_t* d_rowptr = nullptr;
+  int64_t* d_bounds = nullptr;
 
   int32_t nblk() const { return (int32_t)bounds.size() - 1; }
 };
@@ -148,6 +152,8 @@ void build_side(Side& sd, int64_t rows, int64_t other, const std::vector<int64_t
   std::vector<std::vector<Item>> items(nb);
   std::vector<std::vector<Split>> splits(nb);
   std::vector<int32_t> slots(nb, 0);
+  sd.rowptr.assign((size_t)nb * (rows + 1), 0);
+  for (int32_t b = 0; b < nb; ++b) sd.rowptr[(size_t)b * (rows + 1)] = sd.entry_off[b];
   for (int64_t i = 0; i < rows; ++i) {
     int64_t e = ptr[i];
     const int64_t e1 = ptr[i + 1];
@@ -174,6 +180,7 @@ void build_side(Side& sd, int64_t rows, int64_t other, const std::vector<int64_t
       }
       e = f;
     }
+    for (int32_t b = 0; b < nb; ++b) sd.rowptr[(size_t)b * (rows + 1) + i + 1] = cur[b];
   }
   sd.item_off.assign(nb + 1, 0);
   sd.split_off.assign(nb + 1, 0);
@@ -282,6 +289,8 @@ void free_sparse_device(nmd_ctx* c) {
     dfree(sd->d_val);
     dfree(sd->d_items);
     dfree(sd->d_splits);
+    dfree(sd->d_rowptr);
+    dfree(sd->d_bounds);
   }
   dfree(c->scratch);
   dfree(c->objpart);
@@ -386,7 +395,9 @@ int ensure_device(nmd_ctx* c) {
       const int64_t nz = (int64_t)sd->idx.size();
       if (dalloc(&sd->d_idx, nz) != hipSuccess || dalloc(&sd->d_val, nz) != hipSuccess ||
           dalloc(&sd->d_items, (int64_t)sd->items.size()) != hipSuccess ||
-          dalloc(&sd->d_splits, (int64_t)sd->splits.size()) != hipSuccess) {
+          dalloc(&sd->d_splits, (int64_t)sd->splits.size()) != hipSuccess ||
+          dalloc(&sd->d_rowptr, (int64_t)sd->rowptr.size()) != hipSuccess ||
+          dalloc(&sd->d_bounds, (int64_t)sd->bounds.size()) != hipSuccess) {
         free_sparse_device(c);
         return fail(c, NMD_ENOMEM, "device allocation of the sparse structures failed");
       }
@@ -398,11 +409,14 @@ int ensure_device(nmd_ctx* c) {
       if (!sd->splits.empty())
         HIP_TRY(c, hipMemcpy(sd->d_splits, sd->splits.data(), sd->splits.size() * sizeof(Split),
                              hipMemcpyHostToDevice));
+      HIP_TRY(c, hipMemcpy(sd->d_rowptr, sd->rowptr.data(), sd->rowptr.size() * sizeof(int64_t),
+                           hipMemcpyHostToDevice));
+      HIP_TRY(c, hipMemcpy(sd->d_bounds, sd->bounds.data(), sd->bounds.size() * sizeof(int64_t),
+                           hipMemcpyHostToDevice));
     }
     c->scratch_floats = std::max<int64_t>(1, std::max(c->ws.max_slots, c->hs.max_slots)) * c->rp;
-    // objective partials: dense workgroups or W-side items, whichever is larger
-    const int64_t dense_parts = (int64_t)nmd::dense_max_wgs(c->m, c->rp, 64);
-    c->objpart_count = std::max<int64_t>(dense_parts, (int64_t)c->ws.items.size()) + 1;
+    // objective partials: one per (row tile, column block, sub-split)
+    c->objpart_count = (int64_t)nmd::dense_max_wgs(c->m, c->rp, 1) * c->ws.nblk() * kObjSubMax + 1;
     if (dalloc(&c->scratch, c->scratch_floats) != hipSuccess ||
         dalloc(&c->objpart, c->objpart_count) != hipSuccess) {
       free_sparse_device(c);
@@ -771,19 +785,21 @@ int nmd_objective(nmd_ctx* c, const float* W, const float* H, double* out_obj, v
   hipStream_t st = (hipStream_t)hip_stream;
   if ((rc = ensure_device(c))) return rc;
   if ((rc = load_factors(c, W, H, st))) return rc;
-  int ndense = 0;
-  HIP_TRY(c, nmd::launch_obj_dense(c->A, c->m, c->B, c->n, c->rp, c->objpart, &ndense, st));
-  if (ndense + 1 > c->objpart_count) return fail(c, NMD_EDEVICE, "internal: objective buffer");
-  HIP_TRY(c, nmd::launch_sum(c->objpart, ndense, c->objout, st));
-  // sparse part over every column block, one partial per item
   const Side& sd = c->ws;
-  const int64_t ni = (int64_t)sd.items.size();
-  HIP_TRY(c, nmd::launch_obj_sparse(sd.d_items, ni, sd.d_idx, sd.d_val, c->A, c->B, c->rp,
-                                    c->objpart, st));
-  HIP_TRY(c, nmd::launch_sum(c->objpart, ni, c->objout + 1, st));
-  HIP_TRY(c, hipMemcpyAsync(c->h_obj, c->objout, 2 * sizeof(double), hipMemcpyDeviceToHost, st));
+  const int64_t rw = nmd::dense_rows_per_wg(c->rp);
+  const int64_t units = ((c->m + rw - 1) / rw) * sd.nblk();
+  int64_t min_len = c->n;
+  for (int32_t b = 0; b < sd.nblk(); ++b) min_len = std::min(min_len, sd.bounds[b + 1] - sd.bounds[b]);
+  int nsub = (int)std::min<int64_t>(kObjSubMax, std::max<int64_t>(1, (kTargetWgs + units - 1) / units));
+  nsub = (int)std::max<int64_t>(1, std::min<int64_t>(nsub, min_len / 16));
+  int64_t npart = 0;
+  HIP_TRY(c, nmd::launch_objective(c->A, c->m, c->B, sd.d_bounds, sd.nblk(), nsub, sd.d_rowptr,
+                                   sd.d_idx, sd.d_val, c->rp, c->objpart, &npart, st));
+  if (npart + 1 > c->objpart_count) return fail(c, NMD_EDEVICE, "internal: objective buffer");
+  HIP_TRY(c, nmd::launch_sum(c->objpart, npart, c->objout, st));
+  HIP_TRY(c, hipMemcpyAsync(c->h_obj, c->objout, sizeof(double), hipMemcpyDeviceToHost, st));
   HIP_TRY(c, hipStreamSynchronize(st));
-  double tot = c->h_obj[0] + c->h_obj[1];
+  double tot = c->h_obj[0];
   if (tot < 0.0) tot = 0.0;
   *out_obj = std::sqrt(tot) / c->s_norm;
   return NMD_OK;

@@ -64,13 +64,12 @@ hipError_t launch_transpose_out(const float* B, int rp, int64_t n, float* H, int
                                 hipStream_t st);
 hipError_t launch_zero(float* p, int64_t count, hipStream_t st);
 
-// Objective pieces.  Dense: per-workgroup fp64 sums of max(0, L)^2 over all (i, j) of X P^T.
-hipError_t launch_obj_dense(const float* X, int64_t rows, const float* P, int64_t cols, int rp,
-                            double* partial, int* npartial, hipStream_t st);
-// Sparse: per-item fp64 sums of (s - l)^2 - max(0, l)^2, l = x_row . p_j.
-hipError_t launch_obj_sparse(const Item* items, int64_t nitems, const int32_t* idx,
-                             const float* val, const float* X, const float* P, int rp,
-                             double* partial, hipStream_t st);
+// Objective: per-workgroup fp64 sums of the eq. SLloss terms over (row tile, column block,
+// sub-split); rowptr holds, per column block, the row pointers of the W-side entries.
+hipError_t launch_objective(const float* X, int64_t rows, const float* P, const int64_t* cbounds,
+                            int nblk, int nsub, const int64_t* rowptr, const int32_t* idx,
+                            const float* val, int rp, double* partial, int64_t* npartial,
+                            hipStream_t st);
 hipError_t launch_sum(const double* partial, int64_t count, double* out, hipStream_t st);
 
 int dense_max_wgs(int64_t rows, int rp, int nsplit);

@@ -1,0 +1,147 @@
+// Objective of eq. auxCost with Z eliminated (eq. SLloss):
+//   f^2 ||S||_F^2 = sum_{S_ij = 0} max(0, L_ij)^2 + sum_{S_ij > 0} (S_ij - L_ij)^2,  L = X P^T.
+//
+// Every entry of L is formed once, on MFMA, exactly as in the fused contraction (same tiles,
+// same transposed layout).  Each lane owns one row i and four columns 4q..4q+3 of every
+// 16-column block, and walks row i's nonzeros of the current column block (sorted by column) in
+// step with the tile loop; an entry that falls on one of its four columns switches that term
+// from max(0, L)^2 to (S - L)^2.  So each term of eq. SLloss is taken once from the same L:
+// nothing is added over all entries and subtracted again at the nonzeros (which would cancel
+// large terms when L is large on the nonzeros).  Terms are summed in fp64.
+
+#include <climits>
+
+#include "tile.h"
+
+namespace nmd {
+
+template <int RP>
+__global__ __launch_bounds__(256) void objective_kernel(
+    const float* __restrict__ X, int64_t rows, const float* __restrict__ P,
+    const int64_t* __restrict__ cbounds, int nsub, const int64_t* __restrict__ rowptr,
+    const int32_t* __restrict__ idx, const float* __restrict__ val, int64_t row_tiles,
+    double* __restrict__ partial) {
+  constexpr int MI = DenseCfg<RP>::MI;
+  constexpr int NT = DenseCfg<RP>::NT;
+  __shared__ __attribute__((aligned(16))) float tile[NT * (RP + 4)];
+  __shared__ double red[256];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int q = lane >> 4, l16 = lane & 15;
+
+  const int64_t logical = xcd_logical(blockIdx.x, (int64_t)gridDim.x);
+  const int64_t unit = logical / row_tiles;
+  const int64_t rt = logical - unit * row_tiles;
+  const int b = (int)(unit / nsub), s = (int)(unit - (int64_t)b * nsub);
+  const int64_t lo = cbounds[b], len = cbounds[b + 1] - lo;
+  const int64_t jb0 = lo + (int64_t)s * len / nsub;
+  const int64_t jb1 = lo + (int64_t)(s + 1) * len / nsub;
+  const int64_t row0 = rt * (64 * MI) + (int64_t)wave * (16 * MI);
+
+  float a[MI][RP / 4];
+  load_x_frags<RP, MI>(a, X, rows, row0, q, l16);
+
+  // Row walks: first entry of row i in column block b at or after column jb0.
+  int64_t ptr[MI], end[MI];
+  int nextc[MI];
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi) {
+    const int64_t row = row0 + 16 * mi + l16;
+    ptr[mi] = end[mi] = 0;
+    nextc[mi] = INT_MAX;
+    if (row < rows) {
+      int64_t l = rowptr[(int64_t)b * (rows + 1) + row];
+      int64_t h = rowptr[(int64_t)b * (rows + 1) + row + 1];
+      end[mi] = h;
+      while (l < h) {
+        const int64_t mid = (l + h) >> 1;
+        if (idx[mid] < jb0) l = mid + 1; else h = mid;
+      }
+      ptr[mi] = l;
+      if (l < end[mi]) nextc[mi] = idx[l];
+    }
+  }
+
+  double acc = 0.0;
+  PanelTile<RP> pt;
+  if (jb0 < jb1) pt.fetch(P, jb0, jb1, tid);
+  for (int64_t j0 = jb0; j0 < jb1; j0 += NT) {
+    __syncthreads();
+    pt.stash(tile, tid);
+    __syncthreads();
+    if (j0 + NT < jb1) pt.fetch(P, j0 + NT, jb1, tid);
+    const int left = (int)((jb1 - j0 + 15) / 16);
+    const int njb = left < NT / 16 ? left : NT / 16;
+    for (int jb = 0; jb < njb; ++jb) {
+      floatx4 lt[MI];
+      l_tile<RP, MI>(lt, a, tile, jb, q, l16);
+      const int64_t c0 = j0 + 16 * jb + 4 * q;
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi) {
+        float sv[4] = {0.f, 0.f, 0.f, 0.f};
+        bool hit[4] = {false, false, false, false};
+        while (nextc[mi] < c0 + 4 && nextc[mi] < jb1) {
+          if (nextc[mi] >= c0) {
+            const int v = (int)(nextc[mi] - c0);
+            const float sval = val[ptr[mi]];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+              if (v == u) {
+                sv[u] = sval;
+                hit[u] = true;
+              }
+          }
+          ++ptr[mi];
+          nextc[mi] = ptr[mi] < end[mi] ? idx[ptr[mi]] : INT_MAX;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float l = lt[mi][u];
+          if (hit[u]) {
+            const double d = (double)sv[u] - (double)l;
+            acc += d * d;
+          } else {
+            const double p = (double)fmaxf(l, 0.f);
+            acc += p * p;
+          }
+        }
+      }
+    }
+  }
+
+  red[tid] = acc;
+  __syncthreads();
+  for (int k = 128; k > 0; k >>= 1) {
+    if (tid < k) red[tid] += red[tid + k];
+    __syncthreads();
+  }
+  if (tid == 0) partial[logical] = red[0];
+}
+
+template <int RP>
+static hipError_t launch_objective_t(const float* X, int64_t rows, const float* P,
+                                     const int64_t* cbounds, int nblk, int nsub,
+                                     const int64_t* rowptr, const int32_t* idx, const float* val,
+                                     double* partial, int64_t* npartial, hipStream_t st) {
+  const int64_t row_tiles = (rows + rows_per_wg<RP>() - 1) / rows_per_wg<RP>();
+  const int64_t total = row_tiles * nblk * nsub;
+  *npartial = total;
+  if (total <= 0) return hipSuccess;
+  if (total > 0x7fffffffLL) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((objective_kernel<RP>), dim3((unsigned)total), dim3(256), 0, st, X, rows, P,
+                     cbounds, nsub, rowptr, idx, val, row_tiles, partial);
+  return hipGetLastError();
+}
+
+hipError_t launch_objective(const float* X, int64_t rows, const float* P, const int64_t* cbounds,
+                            int nblk, int nsub, const int64_t* rowptr, const int32_t* idx,
+                            const float* val, int rp, double* partial, int64_t* npartial,
+                            hipStream_t st) {
+#define CALL(R) \
+  launch_objective_t<R>(X, rows, P, cbounds, nblk, nsub, rowptr, idx, val, partial, npartial, st)
+  NMD_RP_DISPATCH(rp, CALL)
+#undef CALL
+}
+
+}  // namespace nmd

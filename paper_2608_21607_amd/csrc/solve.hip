@@ -151,7 +151,8 @@ __global__ __launch_bounds__(256) void pivot_inverse_kernel(const double* __rest
     }
     __syncthreads();
   }
-  if (tid == 0 && bad) flag(status, STATUS_NOTPD, step_id);
+  // only the first failing step is recorded (a failure leaves later steps skipped)
+  if (tid == 0 && bad && *(volatile int*)status == 0) flag(status, STATUS_NOTPD, step_id);
   for (int e = tid; e < NB * NB; e += 256) {
     const int i = e / NB, j = e % NB;
     // symmetrise: the exact inverse of a symmetric block is symmetric

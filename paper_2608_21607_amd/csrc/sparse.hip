@@ -1,4 +1,4 @@
-// Sparse correction and the sparse part of the objective.
+// Sparse correction of the fused contraction at the nonzeros of S.
 //
 // The dense kernel contracts min(0, L) over every (i, j) of a block.  On the nonzeros of S the
 // auxiliary matrix is S itself (eq. updateZ), so each nonzero adds (s_ij - min(0, l_ij)) p_j to
@@ -116,40 +116,6 @@ __global__ __launch_bounds__(256) void fixup_kernel(const Split* __restrict__ sp
   for (int e = 0; e < E; ++e) yr[t + T * e] += acc[e];
 }
 
-// Objective over the nonzeros: (s - l)^2 - max(0, l)^2 per entry, summed per item in fp64.
-template <int T, int E>
-__global__ __launch_bounds__(256) void obj_sparse_kernel(const Item* __restrict__ items,
-                                                         int64_t nitems,
-                                                         const int32_t* __restrict__ idx,
-                                                         const float* __restrict__ val,
-                                                         const float* __restrict__ X,
-                                                         const float* __restrict__ P,
-                                                         double* __restrict__ partial) {
-  constexpr int RP = T * E;
-  const int64_t team = ((int64_t)blockIdx.x * 256 + threadIdx.x) / T;
-  const int t = threadIdx.x % T;
-  if (team >= nitems) return;
-  const Item it = items[team];
-  const float* xr = X + (int64_t)it.row * RP;
-  float x[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) x[e] = xr[t + T * e];
-  double sum = 0.0;
-  for (int p = 0; p < it.count; ++p) {
-    const int32_t j = idx[it.begin + p];
-    const float s = val[it.begin + p];
-    float dd = 0.f;
-#pragma unroll
-    for (int e = 0; e < E; ++e) dd = fmaf(x[e], P[(int64_t)j * RP + t + T * e], dd);
-#pragma unroll
-    for (int off = T / 2; off > 0; off >>= 1) dd += __shfl_xor(dd, off, T);
-    const double l = (double)dd;
-    const double pos = l > 0.0 ? l : 0.0;
-    sum += ((double)s - l) * ((double)s - l) - pos * pos;
-  }
-  if (t == 0) partial[team] = sum;
-}
-
 #define NMD_SPARSE_DISPATCH(rp, LAUNCH) \
   switch (rp) {                         \
     case 16: LAUNCH(16, 1); break;      \
@@ -188,17 +154,6 @@ hipError_t launch_fixup(const Split* splits, int64_t nsplits, const float* scrat
 #define LAUNCH(T, E)                                                                           \
   hipLaunchKernelGGL((fixup_kernel<T, E>), dim3(grid_for(nsplits, T)), dim3(256), 0, st, splits, \
                      nsplits, scratch, Y)
-  NMD_SPARSE_DISPATCH(rp, LAUNCH)
-#undef LAUNCH
-}
-
-hipError_t launch_obj_sparse(const Item* items, int64_t nitems, const int32_t* idx,
-                             const float* val, const float* X, const float* P, int rp,
-                             double* partial, hipStream_t st) {
-  if (nitems <= 0) return hipSuccess;
-#define LAUNCH(T, E)                                                                     \
-  hipLaunchKernelGGL((obj_sparse_kernel<T, E>), dim3(grid_for(nitems, T)), dim3(256), 0, st, \
-                     items, nitems, idx, val, X, P, partial)
   NMD_SPARSE_DISPATCH(rp, LAUNCH)
 #undef LAUNCH
 }

@@ -1,0 +1,128 @@
+// Device building blocks shared by the fused contraction and the objective kernels:
+// per-rank tiling constants, the XCD-aware workgroup order, the resident X fragments, the LDS
+// panel tile and the transposed L tile on v_mfma_f32_16x16x4f32.
+#pragma once
+
+#include "nmd_internal.h"
+
+namespace nmd {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+template <int RP>
+struct DenseCfg;
+// MI: 16-row blocks of X per wave (4 waves per workgroup).  NT: panel rows per LDS tile.
+template <> struct DenseCfg<16>  { static constexpr int MI = 4, NT = 512; };
+template <> struct DenseCfg<32>  { static constexpr int MI = 4, NT = 256; };
+template <> struct DenseCfg<48>  { static constexpr int MI = 4, NT = 160; };
+template <> struct DenseCfg<64>  { static constexpr int MI = 4, NT = 128; };
+template <> struct DenseCfg<128> { static constexpr int MI = 4, NT = 64; };
+template <> struct DenseCfg<192> { static constexpr int MI = 2, NT = 32; };
+template <> struct DenseCfg<256> { static constexpr int MI = 2, NT = 32; };
+template <> struct DenseCfg<320> { static constexpr int MI = 1, NT = 16; };
+template <> struct DenseCfg<384> { static constexpr int MI = 1, NT = 16; };
+template <> struct DenseCfg<448> { static constexpr int MI = 1, NT = 16; };
+template <> struct DenseCfg<512> { static constexpr int MI = 1, NT = 16; };
+
+template <int RP>
+constexpr int rows_per_wg() { return 64 * DenseCfg<RP>::MI; }
+
+// Workgroups are dispatched round-robin over the 8 XCDs; this maps the hardware index to a
+// logical one so that XCD x (= bid % 8) owns a contiguous range of logical indices.
+__device__ __forceinline__ int64_t xcd_logical(int64_t bid, int64_t total) {
+  const int64_t x = bid & 7, local = bid >> 3;
+  const int64_t per = total >> 3, rem = total & 7;
+  return x * per + (x < rem ? x : rem) + local;
+}
+
+// Resident X fragments: a[mi][4t + c] = X[row0 + 16 mi + l16][16t + 4q + c] (zero past rows).
+template <int RP, int MI>
+__device__ __forceinline__ void load_x_frags(float (&a)[MI][RP / 4], const float* __restrict__ X,
+                                             int64_t rows, int64_t row0, int q, int l16) {
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi) {
+    const int64_t row = row0 + 16 * mi + l16;
+#pragma unroll
+    for (int t = 0; t < RP / 16; ++t) {
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (row < rows) v = *reinterpret_cast<const float4*>(X + row * RP + 16 * t + 4 * q);
+      a[mi][4 * t + 0] = v.x;
+      a[mi][4 * t + 1] = v.y;
+      a[mi][4 * t + 2] = v.z;
+      a[mi][4 * t + 3] = v.w;
+    }
+  }
+}
+
+// Panel tile staging: NT rows of P (row stride RP) into LDS with row stride RP + 4; rows at or
+// past `jend` are zero.  fetch() issues the global loads into registers, stash() stores them.
+template <int RP>
+struct PanelTile {
+  static constexpr int NT = DenseCfg<RP>::NT;
+  static constexpr int LS = RP + 4;
+  static constexpr int NV4 = NT * RP / 4;
+  static constexpr int NLD = (NV4 + 255) / 256;
+  float4 pf[NLD];
+
+  __device__ __forceinline__ void fetch(const float* __restrict__ P, int64_t j0, int64_t jend,
+                                        int tid) {
+#pragma unroll
+    for (int u = 0; u < NLD; ++u) {
+      const int f = tid + 256 * u;
+      const int rr = f / (RP / 4), c4 = f - rr * (RP / 4);
+      const int64_t j = j0 + rr;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (f < NV4 && j < jend) v = *reinterpret_cast<const float4*>(P + j * RP + 4 * c4);
+      pf[u] = v;
+    }
+  }
+  __device__ __forceinline__ void stash(float* tile, int tid) const {
+#pragma unroll
+    for (int u = 0; u < NLD; ++u) {
+      const int f = tid + 256 * u;
+      const int rr = f / (RP / 4), c4 = f - rr * (RP / 4);
+      if (f < NV4) *reinterpret_cast<float4*>(&tile[rr * LS + 4 * c4]) = pf[u];
+    }
+  }
+};
+
+// Transposed L tile of one 16-row j-block: lt[mi] lane l, register v holds
+// L[i = row0 + 16 mi + l16][j = jb*16 + 4q + v] (srcA = panel rows, srcB = X rows, both over
+// the permuted k order 16t + 4q + c, one ds_read_b128 per four k-steps).
+template <int RP, int MI>
+__device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][RP / 4],
+                                       const float* tile, int jb, int q, int l16) {
+  constexpr int LS = RP + 4;
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi) lt[mi] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const float* brow = &tile[(jb * 16 + l16) * LS + 4 * q];
+#pragma unroll
+  for (int t = 0; t < RP / 16; ++t) {
+    const float4 bv = *reinterpret_cast<const float4*>(brow + 16 * t);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) {
+      lt[mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv.x, a[mi][4 * t + 0], lt[mi], 0, 0, 0);
+      lt[mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv.y, a[mi][4 * t + 1], lt[mi], 0, 0, 0);
+      lt[mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv.z, a[mi][4 * t + 2], lt[mi], 0, 0, 0);
+      lt[mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv.w, a[mi][4 * t + 3], lt[mi], 0, 0, 0);
+    }
+  }
+}
+
+#define NMD_RP_DISPATCH(rp, CALL) \
+  switch (rp) {                   \
+    case 16: return CALL(16);     \
+    case 32: return CALL(32);     \
+    case 48: return CALL(48);     \
+    case 64: return CALL(64);     \
+    case 128: return CALL(128);   \
+    case 192: return CALL(192);   \
+    case 256: return CALL(256);   \
+    case 320: return CALL(320);   \
+    case 384: return CALL(384);   \
+    case 448: return CALL(448);   \
+    case 512: return CALL(512);   \
+  }                               \
+  return hipErrorInvalidValue;
+
+}  // namespace nmd

@@ -1,0 +1,136 @@
+"""GPU parity at the full workload sizes, in the launch configuration the benchmark times.
+
+The 32768 x 32768 planted problem is small enough for the oracle to run a whole sweep.  For
+the 139,255 x 139,255 graph workload the oracle instead checks every step of a full stochastic
+sweep on a sample of rows: before each step the GPU state is copied to the host, and the
+oracle recomputes the step for the sampled rows from that state (a row of the update depends
+only on its own row, the block of the other factor, the block of S and the momentum of that
+row).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import partition, salsa, schedule
+from workloads import gen
+
+import paper_2608_21607_amd as nmd
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def rel(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
+
+
+def test_config3_full_one_sweep():
+    p = gen.config(3)
+    _say("config 3 full size, 1 stochastic sweep", p.m, p.n, p.nnz)
+    ctx = nmd.Context(p.m, p.n, p.r, p.block_m, p.block_n, seed=p.seed, mode=p.mode, eta=p.eta,
+                      momentum=p.momentum)
+    ctx.set_sparse_csr(p.row_ptr, p.col, p.val)
+    W, H = dev(p.W0), dev(p.H0)
+    ctx.sweep(W, H, 1)
+    f_gpu = ctx.objective(W, H)
+    Wg, Hg = W.cpu().numpy(), H.cpu().numpy()
+    S = salsa.csr_matrix(p.m, p.n, p.row_ptr, p.col, p.val)
+    st = salsa.State(p.W0, p.H0)
+    salsa.sweep(S, S.T.tocsr(), st, p.block_m, p.block_n, p.seed, mode=p.mode, eta=p.eta,
+                gamma=p.momentum)
+    ew, eh = rel(Wg, st.W), rel(Hg, st.H)
+    print(f"config 3: rel err W {ew:.2e} H {eh:.2e}")
+    assert ew < TOL and eh < TOL
+    f_orc = salsa.objective(S, Wg, Hg)
+    assert abs(f_gpu - f_orc) <= TOL * f_orc
+
+
+@pytest.fixture(scope="module")
+def config4():
+    p = gen.config(4)
+    S = salsa.csr_matrix(p.m, p.n, p.row_ptr, p.col, p.val)
+    return p, S, S.T.tocsr()
+
+
+def test_config4_block_structure_and_initial_objective(config4):
+    p, S, ST = config4
+    _say("config 4 structure and objective at the start")
+    ctx = nmd.Context(p.m, p.n, p.r, p.block_m, p.block_n, seed=p.seed, mode=p.mode, eta=p.eta,
+                      momentum=p.momentum)
+    ctx.set_sparse_csr(p.row_ptr, p.col, p.val)
+    cb = np.array(partition.bounds(p.n, p.block_n))
+    rb = np.array(partition.bounds(p.m, p.block_m))
+    rows, cols, _ = p.coo()
+    assert ctx.block_nnz(0).tolist() == np.bincount(np.searchsorted(cb, cols, "right") - 1).tolist()
+    assert ctx.block_nnz(1).tolist() == np.bincount(np.searchsorted(rb, rows, "right") - 1).tolist()
+    R, C = len(rb) - 1, len(cb) - 1
+    assert ctx.schedule(0) == schedule.sweep_schedule(p.seed, 0, R, C, True)
+    f_gpu = ctx.objective(dev(p.W0), dev(p.H0))
+    # at the sign-constrained start every L_ij < 0, so only the nonzeros contribute
+    A = p.W0.astype(np.float64)
+    Bt = p.H0.astype(np.float64)
+    tot = 0.0
+    for s in range(0, rows.size, 2_000_000):
+        i, j = rows[s:s + 2_000_000], cols[s:s + 2_000_000]
+        l = np.einsum("ij,ji->i", A[i], Bt[:, j])
+        tot += float(np.sum((p.val[s:s + 2_000_000] - l) ** 2))
+    f_orc = np.sqrt(tot) / np.linalg.norm(p.val.astype(np.float64))
+    print(f"config 4 initial objective: gpu {f_gpu:.6f} oracle {f_orc:.6f}")
+    assert abs(f_gpu - f_orc) <= TOL * f_orc
+
+
+def test_config4_full_sweep_stepwise_sampled(config4):
+    p, S, ST = config4
+    _say("config 4 full sweep, every step checked on sampled rows")
+    ctx = nmd.Context(p.m, p.n, p.r, p.block_m, p.block_n, seed=p.seed, mode=p.mode, eta=p.eta,
+                      momentum=p.momentum)
+    ctx.set_sparse_csr(p.row_ptr, p.col, p.val)
+    rb = partition.bounds(p.m, p.block_m)
+    cb = partition.bounds(p.n, p.block_n)
+    steps = ctx.schedule(0)
+    g = np.random.default_rng(0)
+    rs = np.sort(g.choice(p.m, 96, replace=False))
+    cs = np.sort(g.choice(p.n, 96, replace=False))
+    W, H = dev(p.W0), dev(p.H0)
+    A_prevW = None  # A before the last W-step, for the momentum of the sampled rows
+    B_prevH = None
+    worst = 0.0
+    for k, code in enumerate(steps):
+        A = W.cpu().numpy().astype(np.float64)
+        B = H.cpu().numpy().T.astype(np.float64)
+        ctx.run_steps(W, H, [code])
+        if code > 0:
+            b = code - 1
+            V = np.zeros_like(A)
+            if A_prevW is not None:
+                V[rs] = A[rs] - A_prevW[rs]
+            want, _ = salsa.factor_step(S, A, B, cb[b], cb[b + 1], p.eta, p.momentum, V, rows=rs)
+            got = W[torch.from_numpy(rs).cuda()].cpu().numpy()
+            A_prevW = A
+        else:
+            b = -code - 1
+            V = np.zeros_like(B)
+            if B_prevH is not None:
+                V[cs] = B[cs] - B_prevH[cs]
+            want, _ = salsa.factor_step(ST, B, A, rb[b], rb[b + 1], p.eta, p.momentum, V, rows=cs)
+            got = H[:, torch.from_numpy(cs).cuda()].cpu().numpy().T
+            B_prevH = B
+        e = rel(got, want)
+        worst = max(worst, e)
+        print(f"step {k} code {code}: rel err {e:.2e}", flush=True)
+        assert e < TOL
+    print(f"worst step error {worst:.2e}")
+    f = ctx.objective(W, H)
+    assert np.isfinite(f)
