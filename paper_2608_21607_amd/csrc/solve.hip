@@ -23,19 +23,22 @@ __device__ __forceinline__ void flag(int* status, int bit, int step_id) {
   atomicMin(&status[1], step_id);
 }
 
+typedef double doublex4 __attribute__((ext_vector_type(4)));
+
 // ---------------------------------------------------------------------------------- Gram --
-// grid (npairs, nchunks); tile T = min(64, rp); thread (tx, ty) in 16 x 16 owns the entries
-// (ty + 16a, tx + 16b) of the T x T tile.
+// grid (npairs, nchunks); tile T = min(64, rp).  A workgroup accumulates the T x T tile
+// (ti, tj), ti <= tj, of P^T P over one chunk of panel rows on fp64 MFMA: wave w owns the
+// 16-row block w of the tile; srcA lane l = P[k + l/16][ti T + 16 w + l%16], srcB lane l =
+// P[k + l/16][tj T + 16 cb + l%16] (fp32 inputs widened exactly to fp64).
 template <int T>
 __global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ P, int64_t blk, int rp,
                                                    double* __restrict__ Gpart, int nchunks) {
-  constexpr int NA = T / 16;
-  constexpr int KB = 32;
+  constexpr int NCB = T / 16;
+  constexpr int KB = 64;
   __shared__ float si[KB][T + 1];
   __shared__ float sj[KB][T + 1];
   const int nt = rp / T;
-  // pair index -> (ti <= tj)
-  int pidx = blockIdx.x, ti = 0;
+  int pidx = blockIdx.x, ti = 0;  // pair index -> (ti <= tj)
   while (pidx >= nt - ti) {
     pidx -= nt - ti;
     ++ti;
@@ -43,15 +46,15 @@ __global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ P, 
   const int tj = ti + pidx;
   const int c = blockIdx.y;
   const int64_t k0 = (int64_t)c * blk / nchunks, k1 = (int64_t)(c + 1) * blk / nchunks;
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  double acc[NA][NA];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int q = lane >> 4, l16 = lane & 15;
+  const bool active = wave < NCB;
+  doublex4 acc[NCB];
 #pragma unroll
-  for (int a = 0; a < NA; ++a)
-#pragma unroll
-    for (int b = 0; b < NA; ++b) acc[a][b] = 0.0;
+  for (int cb = 0; cb < NCB; ++cb) acc[cb] = doublex4{0.0, 0.0, 0.0, 0.0};
   for (int64_t kb = k0; kb < k1; kb += KB) {
     __syncthreads();
-    for (int e = threadIdx.x; e < KB * T; e += 256) {
+    for (int e = tid; e < KB * T; e += 256) {
       const int kk = e / T, col = e - kk * T;
       const int64_t k = kb + kk;
       float vi = 0.f, vj = 0.f;
@@ -63,25 +66,24 @@ __global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ P, 
       sj[kk][col] = vj;
     }
     __syncthreads();
-#pragma unroll 4
-    for (int kk = 0; kk < KB; ++kk) {
-      double xi[NA], xj[NA];
+    if (active) {
+      for (int kk = 0; kk < KB; kk += 4) {
+        const double av = (double)si[kk + q][16 * wave + l16];
 #pragma unroll
-      for (int a = 0; a < NA; ++a) xi[a] = (double)si[kk][ty + 16 * a];
-#pragma unroll
-      for (int b = 0; b < NA; ++b) xj[b] = (double)sj[kk][tx + 16 * b];
-#pragma unroll
-      for (int a = 0; a < NA; ++a)
-#pragma unroll
-        for (int b = 0; b < NA; ++b) acc[a][b] = fma(xi[a], xj[b], acc[a][b]);
+        for (int cb = 0; cb < NCB; ++cb) {
+          const double bv = (double)sj[kk + q][16 * cb + l16];
+          acc[cb] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[cb], 0, 0, 0);
+        }
+      }
     }
   }
+  if (!active) return;
   double* out = Gpart + (int64_t)c * rp * rp;
 #pragma unroll
-  for (int a = 0; a < NA; ++a)
+  for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-    for (int b = 0; b < NA; ++b)
-      out[(int64_t)(ti * T + ty + 16 * a) * rp + tj * T + tx + 16 * b] = acc[a][b];
+    for (int v = 0; v < 4; ++v)
+      out[(int64_t)(ti * T + 16 * wave + 4 * v + q) * rp + tj * T + 16 * cb + l16] = acc[cb][v];
 }
 
 // G[i][j] = sum over chunks of the upper-tile partial (mirrored), identity on padded diagonal.
@@ -120,126 +122,165 @@ hipError_t launch_gram(const float* P, int64_t blk, int r, int rp, double* Gpart
 }
 
 // -------------------------------------------------------------------------- block sweeps --
-// Inverse of one NB x NB pivot block by Gauss-Jordan elimination without pivoting (1 WG).
+// Inverse of one NB x NB pivot block by Gauss-Jordan elimination without pivoting.  Thread
+// (i = tid % 64, jq = tid / 64) keeps row i, columns jq*CPT .. jq*CPT+CPT-1 in registers; the
+// pivot row and the pivot column are broadcast through double-buffered LDS, so each pivot
+// costs one barrier.  For an s.p.d. block every pivot is positive; a non-positive or
+// non-finite pivot flags the step as not positive definite.
 template <int NB>
 __global__ __launch_bounds__(256) void pivot_inverse_kernel(const double* __restrict__ G, int rp,
                                                             int k, double* __restrict__ D,
                                                             int* status, int step_id) {
-  __shared__ double a[NB][NB + 1];
-  __shared__ double colp[NB];
-  __shared__ int bad;
+  constexpr int CPT = NB / 4;
+  __shared__ double prow[2][NB];
+  __shared__ double colp[2][64];
   const int tid = threadIdx.x;
-  if (tid == 0) bad = 0;
-  for (int e = tid; e < NB * NB; e += 256) {
-    const int i = e / NB, j = e % NB;
-    a[i][j] = G[(int64_t)(k * NB + i) * rp + k * NB + j];
-  }
-  __syncthreads();
+  const int i = tid & 63, jq = tid >> 6;
+  const bool live = i < NB;
+  double a[CPT];
+#pragma unroll
+  for (int c = 0; c < CPT; ++c)
+    a[c] = live ? G[(int64_t)(k * NB + i) * rp + k * NB + jq * CPT + c] : 0.0;
+  bool bad = false;
+#pragma unroll
   for (int p = 0; p < NB; ++p) {
-    double piv = a[p][p];
-    const bool ok = piv > 0.0 && isfinite(piv);
-    if (!ok) piv = 1.0;
-    __syncthreads();
-    if (tid == 0 && !ok) bad = 1;
-    for (int i = tid; i < NB; i += 256) colp[i] = a[i][p];
-    __syncthreads();
-    for (int j = tid; j < NB; j += 256) a[p][j] = (j == p ? 1.0 : a[p][j]) / piv;
-    __syncthreads();
-    for (int e = tid; e < NB * NB; e += 256) {
-      const int i = e / NB, j = e % NB;
-      if (i != p) a[i][j] = (j == p ? 0.0 : a[i][j]) - colp[i] * a[p][j];
+    const int buf = p & 1;
+    if (jq == p / CPT) {
+      if (i == p) {
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) prow[buf][jq * CPT + c] = a[c];
+      }
+      colp[buf][i] = a[p % CPT];
+    }
+    // the row owners of the other column quarters publish their part of the pivot row
+    if (i == p && jq != p / CPT) {
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) prow[buf][jq * CPT + c] = a[c];
     }
     __syncthreads();
+    double piv = prow[buf][p];
+    if (!(piv > 0.0) || !isfinite(piv)) {
+      bad = true;
+      piv = 1.0;
+    }
+    const double inv = 1.0 / piv;
+    const double f = colp[buf][i];
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) {
+      const int j = jq * CPT + c;
+      const double r = prow[buf][j] * inv;
+      if (i == p)
+        a[c] = (j == p) ? inv : r;
+      else
+        a[c] = (j == p) ? -f * inv : fma(-f, r, a[c]);
+    }
   }
   // only the first failing step is recorded (a failure leaves later steps skipped)
   if (tid == 0 && bad && *(volatile int*)status == 0) flag(status, STATUS_NOTPD, step_id);
-  for (int e = tid; e < NB * NB; e += 256) {
-    const int i = e / NB, j = e % NB;
-    // symmetrise: the exact inverse of a symmetric block is symmetric
-    D[(int64_t)i * NB + j] = 0.5 * (a[i][j] + a[j][i]);
+  if (live) {
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) D[(int64_t)i * NB + jq * CPT + c] = a[c];
   }
 }
 
-// One block sweep over pivot block k; grid (nblk, nblk), one NB x NB output tile per WG.
+// One block sweep over pivot block k; grid (nblk, nblk), one NB x NB output tile per WG, on
+// fp64 MFMA.  Wave w owns the 16-row block w of the tile (NB = 64) and its four 16 x 16 output
+// blocks.  Tiles live in LDS with row stride NB + 1.
+template <int NB>
+__device__ __forceinline__ void tile_mm(doublex4 (&acc)[NB / 16], const double* L,
+                                        const double* R, int rb, int q, int l16) {
+  constexpr int LS = NB + 1;
+  for (int k0 = 0; k0 < NB; k0 += 4) {
+    const double av = L[(16 * rb + l16) * LS + k0 + q];
+#pragma unroll
+    for (int cb = 0; cb < NB / 16; ++cb) {
+      const double bv = R[(k0 + q) * LS + 16 * cb + l16];
+      acc[cb] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[cb], 0, 0, 0);
+    }
+  }
+}
+
 template <int NB>
 __global__ __launch_bounds__(256) void sweep_kernel(const double* __restrict__ Gin,
                                                     double* __restrict__ Gout, int rp, int k,
                                                     const double* __restrict__ D) {
-  constexpr int NA = NB / 16;
-  __shared__ double s1[NB][NB];
-  __shared__ double s2[NB][NB];
+  constexpr int LS = NB + 1;
+  constexpr int NCB = NB / 16;
+  __shared__ double s1[NB * LS];
+  __shared__ double s2[NB * LS];
   const int tj = blockIdx.x, ti = blockIdx.y;
-  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
-  auto load = [&](double (*dst)[NB], int bi, int bj) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int q = lane >> 4, l16 = lane & 15;
+  auto load = [&](double* dst, int bi, int bj) {
     for (int e = tid; e < NB * NB; e += 256) {
-      const int i = e / NB, j = e % NB;
-      dst[i][j] = Gin[(int64_t)(bi * NB + i) * rp + bj * NB + j];
+      const int r = e / NB, c = e - r * NB;
+      dst[r * LS + c] = Gin[(int64_t)(bi * NB + r) * rp + bj * NB + c];
     }
   };
-  auto loadD = [&](double (*dst)[NB]) {
-    for (int e = tid; e < NB * NB; e += 256) dst[e / NB][e % NB] = D[e];
-  };
-  double acc[NA][NA];
-  auto matmul = [&](double (*L)[NB], double (*R)[NB]) {
-#pragma unroll
-    for (int a = 0; a < NA; ++a)
-#pragma unroll
-      for (int b = 0; b < NA; ++b) acc[a][b] = 0.0;
-    for (int kk = 0; kk < NB; ++kk) {
-      double l[NA], r[NA];
-#pragma unroll
-      for (int a = 0; a < NA; ++a) l[a] = L[ty + 16 * a][kk];
-#pragma unroll
-      for (int b = 0; b < NA; ++b) r[b] = R[kk][tx + 16 * b];
-#pragma unroll
-      for (int a = 0; a < NA; ++a)
-#pragma unroll
-        for (int b = 0; b < NA; ++b) acc[a][b] = fma(l[a], r[b], acc[a][b]);
+  auto loadD = [&](double* dst) {
+    for (int e = tid; e < NB * NB; e += 256) {
+      const int r = e / NB, c = e - r * NB;
+      dst[r * LS + c] = D[e];
     }
   };
-  auto store = [&](double sign, bool sub) {
-#pragma unroll
-    for (int a = 0; a < NA; ++a)
-#pragma unroll
-      for (int b = 0; b < NA; ++b) {
-        const int64_t o = (int64_t)(ti * NB + ty + 16 * a) * rp + tj * NB + tx + 16 * b;
-        Gout[o] = sub ? Gin[o] - acc[a][b] : sign * acc[a][b];
-      }
+  // output element of accumulator (cb, v): row 16 wave + 4v + q, column 16 cb + l16
+  auto out_index = [&](int cb, int v) {
+    return (int64_t)(ti * NB + 16 * wave + 4 * v + q) * rp + tj * NB + 16 * cb + l16;
   };
+  const bool active = wave < NB / 16;
+  doublex4 acc[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) acc[cb] = doublex4{0.0, 0.0, 0.0, 0.0};
   if (ti == k && tj == k) {
-    loadD(s1);
-    __syncthreads();
-#pragma unroll
-    for (int a = 0; a < NA; ++a)
-#pragma unroll
-      for (int b = 0; b < NA; ++b) acc[a][b] = s1[ty + 16 * a][tx + 16 * b];
-    store(-1.0, false);
-  } else if (ti == k) {
+    for (int e = tid; e < NB * NB; e += 256) {
+      const int r = e / NB, c = e - r * NB;
+      Gout[(int64_t)(k * NB + r) * rp + k * NB + c] = -D[e];
+    }
+    return;
+  }
+  if (ti == k) {  // D G_kj
     loadD(s1);
     load(s2, k, tj);
     __syncthreads();
-    matmul(s1, s2);
-    store(1.0, false);
-  } else if (tj == k) {
+    if (active) tile_mm<NB>(acc, s1, s2, wave, q, l16);
+  } else if (tj == k) {  // G_ik D
     load(s1, ti, k);
     loadD(s2);
     __syncthreads();
-    matmul(s1, s2);
-    store(1.0, false);
-  } else {
+    if (active) tile_mm<NB>(acc, s1, s2, wave, q, l16);
+  } else {  // G_ij - (G_ik D) G_kj
     load(s1, ti, k);
     loadD(s2);
     __syncthreads();
-    matmul(s1, s2);  // T1 = G_ik D
+    if (active) tile_mm<NB>(acc, s1, s2, wave, q, l16);
     __syncthreads();
+    if (active) {
 #pragma unroll
-    for (int a = 0; a < NA; ++a)
+      for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-      for (int b = 0; b < NA; ++b) s1[ty + 16 * a][tx + 16 * b] = acc[a][b];
+        for (int v = 0; v < 4; ++v) s1[(16 * wave + 4 * v + q) * LS + 16 * cb + l16] = acc[cb][v];
+    }
     load(s2, k, tj);
     __syncthreads();
-    matmul(s1, s2);  // T1 G_kj
-    store(1.0, true);
+    if (active) {
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) acc[cb] = doublex4{0.0, 0.0, 0.0, 0.0};
+      tile_mm<NB>(acc, s1, s2, wave, q, l16);
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int64_t o = out_index(cb, v);
+          Gout[o] = Gin[o] - acc[cb][v];
+        }
+    }
+    return;
+  }
+  if (active) {
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) Gout[out_index(cb, v)] = acc[cb][v];
   }
 }
 
@@ -275,55 +316,77 @@ hipError_t launch_inverse(double* G, double* Gtmp, int rp, int* status, int step
 }
 
 // --------------------------------------------------------------------------------- apply --
-// One workgroup per RW = 256 / TX rows.  The fp64 row sums of the partial Y go to LDS; thread
-// (tx, ty) computes row ty, columns tx + TX b of X = Ysum (-Gneg), then the momentum update.
-template <int RP, int TX>
+// X = Ysum (-Gneg) on fp64 MFMA (v_mfma_f64_16x16x4f64), then the momentum update.
+// A workgroup owns RW rows: their fp64 sums over the nsplit partial outputs are staged in LDS,
+// and the (RW/16) x (RP/16) output blocks of 16 x 16 are dealt round-robin to the 4 waves.
+// srcA lane l = Ysum[16 rb + l%16][k + l/16], srcB lane l = Gneg[k + l/16][16 cb + l%16];
+// accumulator lane l, register v = X[16 rb + 4 v + l/16][16 cb + l%16] (the fp64 MFMA
+// interleaves accumulator rows, unlike the fp32 16x16x4 form).
+
+template <int RP>
+struct ApplyCfg {
+  static constexpr int RW = RP <= 64 ? 64 : (RP <= 256 ? 32 : 16);
+};
+
+template <int RP>
 __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Ypart,
                                                     int64_t y_stride, int nsplit,
                                                     const double* __restrict__ Gneg,
                                                     float* __restrict__ X, float* __restrict__ V,
                                                     int64_t rows, float eta, float gamma,
-                                                    const int* status_in, int* status,
-                                                    int step_id) {
-  constexpr int RW = 256 / TX;
-  constexpr int NC = RP / TX;
-  __shared__ double ys[RW][RP + 1];
-  const int tid = threadIdx.x, tx = tid % TX, ty = tid / TX;
-  const bool skip = *(volatile const int*)status_in != 0;
-  if (skip) return;  // an earlier step failed: leave the factors as they are
+                                                    int* status, int step_id) {
+  constexpr int RW = ApplyCfg<RP>::RW;
+  constexpr int CBN = RP / 16;
+  constexpr int NBW = (RW / 16) * CBN / 4;  // output blocks per wave
+  constexpr int LS = RP + 1;
+  __shared__ double ys[RW * LS];
+  if (*(volatile const int*)status != 0) return;  // an earlier step failed: factors stay
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int q = lane >> 4, l16 = lane & 15;
   const int64_t r0 = (int64_t)blockIdx.x * RW;
   for (int e = tid; e < RW * RP; e += 256) {
-    const int i = e / RP, c = e % RP;
+    const int i = e / RP, c = e - i * RP;
     const int64_t row = r0 + i;
     double s = 0.0;
     if (row < rows)
       for (int sp = 0; sp < nsplit; ++sp) s += (double)Ypart[(int64_t)sp * y_stride + row * RP + c];
-    ys[i][c] = s;
+    ys[i * LS + c] = s;
   }
   __syncthreads();
-  double acc[NC];
+  doublex4 acc[NBW];
 #pragma unroll
-  for (int b = 0; b < NC; ++b) acc[b] = 0.0;
-  for (int k = 0; k < RP; ++k) {
-    const double yv = ys[ty][k];
-    const double* g = Gneg + (int64_t)k * RP + tx;
+  for (int u = 0; u < NBW; ++u) acc[u] = doublex4{0.0, 0.0, 0.0, 0.0};
+  for (int k0 = 0; k0 < RP; k0 += 4) {
 #pragma unroll
-    for (int b = 0; b < NC; ++b) acc[b] = fma(yv, g[TX * b], acc[b]);
+    for (int u = 0; u < NBW; ++u) {
+      const int b = wave + 4 * u;
+      const int rb = b / CBN, cb = b - rb * CBN;
+      const double av = ys[(16 * rb + l16) * LS + k0 + q];
+      const double bv = Gneg[(int64_t)(k0 + q) * RP + 16 * cb + l16];
+      acc[u] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[u], 0, 0, 0);
+    }
   }
-  const int64_t row = r0 + ty;
-  if (row >= rows) return;
   bool bad = false;
 #pragma unroll
-  for (int b = 0; b < NC; ++b) {
-    const int64_t o = row * RP + tx + TX * b;
-    const double xnew = -acc[b];
-    const double xa = (double)X[o];
-    const double v = (double)gamma * (double)V[o] + (double)eta * (xnew - xa);
-    const float xf = (float)(xa + v);
-    const float vf = (float)v;
-    bad |= !isfinite(xf) || !isfinite(vf);
-    X[o] = xf;
-    V[o] = vf;
+  for (int u = 0; u < NBW; ++u) {
+    const int b = wave + 4 * u;
+    const int rb = b / CBN, cb = b - rb * CBN;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t row = r0 + 16 * rb + 4 * v + q;
+      if (row < rows) {
+        const int64_t o = row * RP + 16 * cb + l16;
+        const double xnew = -acc[u][v];
+        const double xa = (double)X[o];
+        const double vn = (double)gamma * (double)V[o] + (double)eta * (xnew - xa);
+        const float xf = (float)(xa + vn);
+        const float vf = (float)vn;
+        bad |= !isfinite(xf) || !isfinite(vf);
+        X[o] = xf;
+        V[o] = vf;
+      }
+    }
   }
   if (bad) flag(status, STATUS_NONFINITE, step_id);
 }
@@ -332,16 +395,17 @@ hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const 
                         float* X, float* V, int64_t rows, int rp, float eta, float gamma,
                         int* status, int step_id, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-#define CASE(R, TXV)                                                                         \
+#define CASE(R)                                                                              \
   case R: {                                                                                  \
-    const dim3 grid((unsigned)((rows + (256 / TXV) - 1) / (256 / TXV)));                     \
-    hipLaunchKernelGGL((apply_kernel<R, TXV>), grid, dim3(256), 0, st, Ypart, y_stride, nsplit, \
-                       Gneg, X, V, rows, eta, gamma, status, status, step_id);              \
+    constexpr int RW = ApplyCfg<R>::RW;                                                      \
+    hipLaunchKernelGGL((apply_kernel<R>), dim3((unsigned)((rows + RW - 1) / RW)), dim3(256), 0, \
+                       st, Ypart, y_stride, nsplit, Gneg, X, V, rows, eta, gamma, status,    \
+                       step_id);                                                             \
     break;                                                                                   \
   }
   switch (rp) {
-    CASE(16, 16) CASE(32, 16) CASE(48, 16) CASE(64, 16) CASE(128, 16) CASE(192, 16)
-    CASE(256, 16) CASE(320, 32) CASE(384, 32) CASE(448, 32) CASE(512, 32)
+    CASE(16) CASE(32) CASE(48) CASE(64) CASE(128) CASE(192) CASE(256) CASE(320) CASE(384)
+    CASE(448) CASE(512)
     default: return hipErrorInvalidValue;
   }
 #undef CASE
