@@ -63,6 +63,7 @@ __global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X,
   constexpr int NT = DenseCfg<RP>::NT;
   constexpr int CB = RP / 16;
   constexpr int LS = RP + 4;
+  (void)LS;
   __shared__ __attribute__((aligned(16))) float tile[NT * LS];
 
   const int tid = threadIdx.x;
@@ -100,18 +101,8 @@ __global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X,
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) lt[mi][v] = fminf(lt[mi][v], 0.f);
-      const float* b2 = &tile[(jb * 16 + 4 * q) * LS + l16];
-#pragma unroll
-      for (int cb = 0; cb < CB; ++cb) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const float bb = b2[v * LS + 16 * cb];
-#pragma unroll
-          for (int mi = 0; mi < MI; ++mi)
-            y[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(lt[mi][v], bb, y[mi][cb], 0, 0, 0);
-        }
-      }
+        for (int v = 0; v < 4; ++v) lt[mi][v] = lt[mi][v] < 0.f ? lt[mi][v] : 0.f;
+      zb_tile<RP, MI>(y, lt, tile, jb, q, l16);
     }
   }
 

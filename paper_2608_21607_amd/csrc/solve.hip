@@ -317,15 +317,19 @@ hipError_t launch_inverse(double* G, double* Gtmp, int rp, int* status, int step
 
 // --------------------------------------------------------------------------------- apply --
 // X = Ysum (-Gneg) on fp64 MFMA (v_mfma_f64_16x16x4f64), then the momentum update.
-// A workgroup owns RW rows: their fp64 sums over the nsplit partial outputs are staged in LDS,
-// and the (RW/16) x (RP/16) output blocks of 16 x 16 are dealt round-robin to the 4 waves.
+// A workgroup owns RW rows: their fp64 sums over the nsplit partial outputs are staged in LDS.
+// For RP >= 64 wave w owns the output column blocks w, w+4, ... over all RW/16 row blocks, so
+// each Gneg operand feeds RW/16 MFMAs; for RP < 64 wave w owns row block w and every column
+// block.  Gneg operands (L2-resident) are prefetched two k-steps ahead in registers.
 // srcA lane l = Ysum[16 rb + l%16][k + l/16], srcB lane l = Gneg[k + l/16][16 cb + l%16];
 // accumulator lane l, register v = X[16 rb + 4 v + l/16][16 cb + l%16] (the fp64 MFMA
 // interleaves accumulator rows, unlike the fp32 16x16x4 form).
-
 template <int RP>
 struct ApplyCfg {
   static constexpr int RW = RP <= 64 ? 64 : (RP <= 256 ? 32 : 16);
+  static constexpr bool COLS = RP >= 64;                 // waves split columns
+  static constexpr int NRB = COLS ? RW / 16 : 1;         // row blocks per wave
+  static constexpr int NCB = COLS ? RP / 64 : RP / 16;   // column blocks per wave
 };
 
 template <int RP>
@@ -335,59 +339,91 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Yp
                                                     float* __restrict__ X, float* __restrict__ V,
                                                     int64_t rows, float eta, float gamma,
                                                     int* status, int step_id) {
-  constexpr int RW = ApplyCfg<RP>::RW;
-  constexpr int CBN = RP / 16;
-  constexpr int NBW = (RW / 16) * CBN / 4;  // output blocks per wave
+  using C = ApplyCfg<RP>;
+  constexpr int RW = C::RW, NRB = C::NRB, NCB = C::NCB;
   constexpr int LS = RP + 1;
+  constexpr int PD = 2;  // prefetch distance in k-steps
   __shared__ double ys[RW * LS];
   if (*(volatile const int*)status != 0) return;  // an earlier step failed: factors stay
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int q = lane >> 4, l16 = lane & 15;
   const int64_t r0 = (int64_t)blockIdx.x * RW;
-  for (int e = tid; e < RW * RP; e += 256) {
-    const int i = e / RP, c = e - i * RP;
+  for (int e = tid; e < RW * RP / 4; e += 256) {
+    const int i = e / (RP / 4), c4 = e - i * (RP / 4);
     const int64_t row = r0 + i;
-    double s = 0.0;
-    if (row < rows)
-      for (int sp = 0; sp < nsplit; ++sp) s += (double)Ypart[(int64_t)sp * y_stride + row * RP + c];
-    ys[i * LS + c] = s;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    if (row < rows) {
+      const float* src = Ypart + row * RP + 4 * c4;
+      for (int sp = 0; sp < nsplit; ++sp) {
+        const float4 v = *reinterpret_cast<const float4*>(src + (int64_t)sp * y_stride);
+        s0 += (double)v.x;
+        s1 += (double)v.y;
+        s2 += (double)v.z;
+        s3 += (double)v.w;
+      }
+    }
+    double* d = &ys[i * LS + 4 * c4];
+    d[0] = s0;
+    d[1] = s1;
+    d[2] = s2;
+    d[3] = s3;
   }
   __syncthreads();
-  doublex4 acc[NBW];
+  auto rblock = [&](int a) { return C::COLS ? a : wave; };
+  auto cblock = [&](int b) { return C::COLS ? wave + 4 * b : b; };
+  doublex4 acc[NRB][NCB];
 #pragma unroll
-  for (int u = 0; u < NBW; ++u) acc[u] = doublex4{0.0, 0.0, 0.0, 0.0};
-  for (int k0 = 0; k0 < RP; k0 += 4) {
+  for (int a = 0; a < NRB; ++a)
 #pragma unroll
-    for (int u = 0; u < NBW; ++u) {
-      const int b = wave + 4 * u;
-      const int rb = b / CBN, cb = b - rb * CBN;
-      const double av = ys[(16 * rb + l16) * LS + k0 + q];
-      const double bv = Gneg[(int64_t)(k0 + q) * RP + 16 * cb + l16];
-      acc[u] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[u], 0, 0, 0);
+    for (int b = 0; b < NCB; ++b) acc[a][b] = doublex4{0.0, 0.0, 0.0, 0.0};
+  double pre[PD][NCB];
+#pragma unroll
+  for (int d = 0; d < PD; ++d)
+#pragma unroll
+    for (int b = 0; b < NCB; ++b)
+      pre[d][b] = Gneg[(int64_t)(4 * d + q) * RP + 16 * cblock(b) + l16];
+  for (int k0 = 0; k0 < RP; k0 += 4 * PD) {
+#pragma unroll
+    for (int d = 0; d < PD; ++d) {
+      const int k = k0 + 4 * d;
+      double bv[NCB];
+#pragma unroll
+      for (int b = 0; b < NCB; ++b) bv[b] = pre[d][b];
+      const int kn = k + 4 * PD;
+      if (kn < RP) {
+#pragma unroll
+        for (int b = 0; b < NCB; ++b) pre[d][b] = Gneg[(int64_t)(kn + q) * RP + 16 * cblock(b) + l16];
+      }
+#pragma unroll
+      for (int a = 0; a < NRB; ++a) {
+        const double av = ys[(16 * rblock(a) + l16) * LS + k + q];
+#pragma unroll
+        for (int b = 0; b < NCB; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv[b], acc[a][b], 0, 0, 0);
+      }
     }
   }
   bool bad = false;
 #pragma unroll
-  for (int u = 0; u < NBW; ++u) {
-    const int b = wave + 4 * u;
-    const int rb = b / CBN, cb = b - rb * CBN;
+  for (int a = 0; a < NRB; ++a)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t row = r0 + 16 * rb + 4 * v + q;
-      if (row < rows) {
-        const int64_t o = row * RP + 16 * cb + l16;
-        const double xnew = -acc[u][v];
-        const double xa = (double)X[o];
-        const double vn = (double)gamma * (double)V[o] + (double)eta * (xnew - xa);
-        const float xf = (float)(xa + vn);
-        const float vf = (float)vn;
-        bad |= !isfinite(xf) || !isfinite(vf);
-        X[o] = xf;
-        V[o] = vf;
+    for (int b = 0; b < NCB; ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t row = r0 + 16 * rblock(a) + 4 * v + q;
+        if (row < rows) {
+          const int64_t o = row * RP + 16 * cblock(b) + l16;
+          const double xnew = -acc[a][b][v];
+          const double xa = (double)X[o];
+          const double vn = (double)gamma * (double)V[o] + (double)eta * (xnew - xa);
+          const float xf = (float)(xa + vn);
+          const float vf = (float)vn;
+          bad |= !isfinite(xf) || !isfinite(vf);
+          X[o] = xf;
+          V[o] = vf;
+        }
       }
-    }
-  }
   if (bad) flag(status, STATUS_NONFINITE, step_id);
 }
 

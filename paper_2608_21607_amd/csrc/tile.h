@@ -88,23 +88,79 @@ struct PanelTile {
 
 // Transposed L tile of one 16-row j-block: lt[mi] lane l, register v holds
 // L[i = row0 + 16 mi + l16][j = jb*16 + 4q + v] (srcA = panel rows, srcB = X rows, both over
-// the permuted k order 16t + 4q + c, one ds_read_b128 per four k-steps).
+// the permuted k order 16t + 4q + c, one ds_read_b128 per four k-steps).  The panel fragments
+// of group t+2 are read while the MFMAs of group t run, so LDS latency stays off the MFMA pipe.
 template <int RP, int MI>
 __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][RP / 4],
                                        const float* tile, int jb, int q, int l16) {
   constexpr int LS = RP + 4;
+  constexpr int KG = RP / 16;
+  constexpr int LA = 3;  // fragment groups in flight
+  // NA accumulators per row block (k-groups taken round-robin) so that consecutive MFMAs of
+  // a wave never wait on each other's results
+  constexpr int NA = MI >= 4 ? 1 : 4 / MI;
+  floatx4 acc[NA][MI];
 #pragma unroll
-  for (int mi = 0; mi < MI; ++mi) lt[mi] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int h = 0; h < NA; ++h)
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) acc[h][mi] = floatx4{0.f, 0.f, 0.f, 0.f};
   const float* brow = &tile[(jb * 16 + l16) * LS + 4 * q];
+  float4 bf[KG];
 #pragma unroll
-  for (int t = 0; t < RP / 16; ++t) {
-    const float4 bv = *reinterpret_cast<const float4*>(brow + 16 * t);
+  for (int t = 0; t < LA && t < KG; ++t) bf[t] = *reinterpret_cast<const float4*>(brow + 16 * t);
+  __builtin_amdgcn_sched_group_barrier(0x100, LA < KG ? LA : KG, 0);
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi) {
-      lt[mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv.x, a[mi][4 * t + 0], lt[mi], 0, 0, 0);
-      lt[mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv.y, a[mi][4 * t + 1], lt[mi], 0, 0, 0);
-      lt[mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv.z, a[mi][4 * t + 2], lt[mi], 0, 0, 0);
-      lt[mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv.w, a[mi][4 * t + 3], lt[mi], 0, 0, 0);
+  for (int t = 0; t < KG; ++t) {
+    if (t + LA < KG) bf[t + LA] = *reinterpret_cast<const float4*>(brow + 16 * (t + LA));
+    const int h = t % NA;
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+      acc[h][mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[t].x, a[mi][4 * t + 0], acc[h][mi], 0, 0, 0);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+      acc[h][mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[t].y, a[mi][4 * t + 1], acc[h][mi], 0, 0, 0);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+      acc[h][mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[t].z, a[mi][4 * t + 2], acc[h][mi], 0, 0, 0);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+      acc[h][mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[t].w, a[mi][4 * t + 3], acc[h][mi], 0, 0, 0);
+    if (t + LA < KG) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // read of group t+LA
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * MI, 0);               // MFMAs of group t
+  }
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi) {
+    lt[mi] = acc[0][mi];
+#pragma unroll
+    for (int h = 1; h < NA; ++h)
+      if (h < KG) lt[mi] += acc[h][mi];
+  }
+}
+
+// Y[i][c] += sum_j z[i][j] P[j][c] for one 16-row j-block: srcA = z (the clamped L^T
+// accumulator, register v <-> k-slice 4q + v), srcB = P[jb*16 + 4q + v][16 cb + l16] from LDS.
+// The k-slices v run in the outer loop so that consecutive MFMAs update different column
+// blocks; operands are read one k-slice ahead.
+template <int RP, int MI>
+__device__ __forceinline__ void zb_tile(floatx4 (&y)[MI][RP / 16], const floatx4 (&z)[MI],
+                                        const float* tile, int jb, int q, int l16) {
+  constexpr int LS = RP + 4;
+  constexpr int CB = RP / 16;
+  const float* b2 = &tile[(jb * 16 + 4 * q) * LS + l16];
+  float bb[4][CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) bb[0][cb] = b2[16 * cb];
+  __builtin_amdgcn_sched_group_barrier(0x100, CB, 0);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      if (v + 1 < 4) bb[v + 1][cb] = b2[(v + 1) * LS + 16 * cb];
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+        y[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(z[mi][v], bb[v][cb], y[mi][cb], 0, 0, 0);
+      if (v + 1 < 4) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, MI, 0);
     }
   }
 }
