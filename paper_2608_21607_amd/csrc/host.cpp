@@ -229,12 +229,15 @@ struct nmd_ctx {
   int64_t ypart_floats = 0;
   float* scratch = nullptr;
   int64_t scratch_floats = 0;
+
   double *G = nullptr, *Gtmp = nullptr, *Gpart = nullptr;
   int gram_chunks_max = 64;
   double* objpart = nullptr;
   int64_t objpart_count = 0;
   double* objout = nullptr;
   int* status = nullptr;
+  hipStream_t side = nullptr;     // Gram and inverse run here, beside the contraction
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   int* h_status = nullptr;   // pinned
   double* h_obj = nullptr;   // pinned
 
@@ -309,6 +312,11 @@ void free_device(nmd_ctx* c) {
   dfree(c->Gpart);
   dfree(c->objout);
   dfree(c->status);
+  if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
+  if (c->ev_join) (void)hipEventDestroy(c->ev_join);
+  if (c->side) (void)hipStreamDestroy(c->side);
+  c->ev_fork = c->ev_join = nullptr;
+  c->side = nullptr;
   if (c->h_status) (void)hipHostFree(c->h_status);
   if (c->h_obj) (void)hipHostFree(c->h_obj);
   c->h_status = nullptr;
@@ -383,6 +391,13 @@ int ensure_device(nmd_ctx* c) {
     HIP_TRY(c, hipMemset(c->VB, 0, (size_t)npad * rp * sizeof(float)));
     HIP_TRY(c, hipMemset(c->A, 0, (size_t)mpad * rp * sizeof(float)));
     HIP_TRY(c, hipMemset(c->B, 0, (size_t)npad * rp * sizeof(float)));
+    // default priority on purpose: every stream of the library runs at the same priority
+    if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess) {
+      free_device(c);
+      return fail(c, NMD_EDEVICE, "creating the side stream or its events failed");
+    }
     HIP_TRY(c, hipMemset(c->status, 0, sizeof(int)));
     HIP_TRY(c, hipMemset(c->status + 1, 0x7f, sizeof(int)));
     HIP_TRY(c, hipDeviceSynchronize());
@@ -497,12 +512,17 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
   const int rp = c->rp;
   const float* PJ = P + j0 * rp;
 
+  // Gram matrix and its inverse depend only on the panel rows of the block: they run on the
+  // side stream while the contraction runs on the caller's stream, and the solve joins both.
   double* Gneg = nullptr;
+  HIP_TRY(c, hipEventRecord(c->ev_fork, st));
+  HIP_TRY(c, hipStreamWaitEvent(c->side, c->ev_fork, 0));
   {
-    Scope sc(c, st, K_FACTOR, 2.0 * blk * (double)c->r * c->r + 2.0 * (double)rp * rp * rp, 0.0);
-    HIP_TRY(c, nmd::launch_gram(PJ, blk, c->r, rp, c->Gpart, gram_chunks(blk), c->G, st));
-    HIP_TRY(c, nmd::launch_inverse(c->G, c->Gtmp, rp, c->status, step_id, &Gneg, st));
+    Scope sc(c, c->side, K_FACTOR, 2.0 * blk * (double)c->r * c->r + 2.0 * (double)rp * rp * rp, 0.0);
+    HIP_TRY(c, nmd::launch_gram(PJ, blk, c->r, rp, c->Gpart, gram_chunks(blk), c->G, c->side));
+    HIP_TRY(c, nmd::launch_inverse(c->G, c->Gtmp, rp, c->status, step_id, &Gneg, c->side));
   }
+  HIP_TRY(c, hipEventRecord(c->ev_join, c->side));
   const int64_t ns = nsplit_for(rows, blk, rp);
   const int64_t y_stride = rows * rp;
   if (ns * y_stride > c->ypart_floats)
@@ -511,24 +531,29 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
     Scope sc(c, st, K_DENSE, 4.0 * rows * (double)blk * c->r, 4.0 * (2.0 * rows + blk) * c->r);
     HIP_TRY(c, nmd::launch_dense(X, rows, PJ, blk, rp, c->Ypart, y_stride, (int)ns, st));
   }
+  // Sparse correction at the nonzeros, added in place to the first partial output.  It runs
+  // after the contraction on the same stream: beside it, its gathers would take issue slots
+  // from the single MFMA wave per SIMD of the contraction.
   const int32_t b0 = block >= 0 ? block : 0;
   const int32_t b1 = block >= 0 ? block + 1 : sd.nblk();
   for (int32_t b = b0; b < b1; ++b) {
     const int64_t ni = sd.item_off[b + 1] - sd.item_off[b];
     const int64_t nsp = sd.split_off[b + 1] - sd.split_off[b];
     const int64_t nz = sd.entry_off[b + 1] - sd.entry_off[b];
-    // algorithmic bytes: entries (index + value), each touched row of X and Y (read x, read
-    // and write y), each panel row of the block once
+    // algorithmic bytes: entries (index + value), each touched row of X and of Y (read x,
+    // read and write y), each panel row of the block once
     const double bytes = 8.0 * nz + 12.0 * (double)ni * c->r + 4.0 * blk * c->r;
     Scope sc(c, st, K_SPARSE, 4.0 * nz * c->r, bytes);
     HIP_TRY(c, nmd::launch_sparse(sd.d_items + sd.item_off[b], ni, sd.d_idx, sd.d_val, X, P, rp,
-                                  c->Ypart, c->scratch, st));
-    HIP_TRY(c, nmd::launch_fixup(sd.d_splits + sd.split_off[b], nsp, c->scratch, rp, c->Ypart, st));
+                                  c->Ypart, c->scratch, 1, st));
+    HIP_TRY(c, nmd::launch_fixup(sd.d_splits + sd.split_off[b], nsp, c->scratch, rp, c->Ypart, 1,
+                                 st));
   }
+  HIP_TRY(c, hipStreamWaitEvent(st, c->ev_join, 0));
   {
     Scope sc(c, st, K_APPLY, 2.0 * rows * (double)rp * rp, 4.0 * rows * rp * (ns + 4));
-    HIP_TRY(c, nmd::launch_apply(c->Ypart, y_stride, (int)ns, Gneg, X, V, rows, rp, eta, gamma,
-                                 c->status, step_id, st));
+    HIP_TRY(c, nmd::launch_apply(c->Ypart, y_stride, (int)ns, nullptr, Gneg, X, V, rows, rp, eta,
+                                 gamma, c->status, step_id, st));
   }
   return NMD_OK;
 }

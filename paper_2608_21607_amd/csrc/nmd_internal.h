@@ -35,12 +35,15 @@ int dense_rows_per_wg(int rp);
 hipError_t launch_dense(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
                         float* Ypart, int64_t y_stride, int nsplit, hipStream_t st);
 
-// Sparse correction: for every item, y_row += sum over its entries of (s - min(0, x_row . p_j)) p_j.
+// Sparse correction: for every item, c = sum over its entries of (s - min(0, x_row . p_j)) p_j;
+// a row with a single item gets Y[row] = c (accumulate = 0) or Y[row] += c (accumulate = 1);
+// a row split over several items has its slots summed in order by the fix-up, which writes or
+// adds the same way.
 hipError_t launch_sparse(const Item* items, int64_t nitems, const int32_t* idx, const float* val,
                          const float* X, const float* P, int rp, float* Y, float* scratch,
-                         hipStream_t st);
+                         int accumulate, hipStream_t st);
 hipError_t launch_fixup(const Split* splits, int64_t nsplits, const float* scratch, int rp,
-                        float* Y, hipStream_t st);
+                        float* Y, int accumulate, hipStream_t st);
 
 // Gram matrix G = P^T P (fp64, rp x rp, identity on the padded diagonal) of `blk` rows.
 hipError_t launch_gram(const float* P, int64_t blk, int r, int rp, double* Gpart, int nchunks,
@@ -48,8 +51,10 @@ hipError_t launch_gram(const float* P, int64_t blk, int r, int rp, double* Gpart
 // Gsw <- -G^-1 by block sweeps; flags status on a non-positive pivot.  Gtmp: scratch rp x rp.
 hipError_t launch_inverse(double* G, double* Gtmp, int rp, int* status, int step_id,
                           double** result, hipStream_t st);
-// X <- X + V, V <- gamma V + eta (Ysum (-Gneg) - X), Ysum = sum of the nsplit partial outputs.
-hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const double* Gneg,
+// X <- X + V, V <- gamma V + eta (Ysum (-Gneg) - X), Ysum = the nsplit partial outputs plus,
+// when Ysp is not NULL, a separate correction buffer (rows x rp), summed in fp64.
+hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const float* Ysp,
+                        const double* Gneg,
                         float* X, float* V, int64_t rows, int rp, float eta, float gamma,
                         int* status, int step_id, hipStream_t st);
 

@@ -326,7 +326,7 @@ hipError_t launch_inverse(double* G, double* Gtmp, int rp, int* status, int step
 // interleaves accumulator rows, unlike the fp32 16x16x4 form).
 template <int RP>
 struct ApplyCfg {
-  static constexpr int RW = RP <= 64 ? 64 : (RP <= 256 ? 32 : 16);
+  static constexpr int RW = RP <= 64 ? 64 : (RP <= 128 ? 32 : 16);
   static constexpr bool COLS = RP >= 64;                 // waves split columns
   static constexpr int NRB = COLS ? RW / 16 : 1;         // row blocks per wave
   static constexpr int NCB = COLS ? RP / 64 : RP / 16;   // column blocks per wave
@@ -335,6 +335,7 @@ struct ApplyCfg {
 template <int RP>
 __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Ypart,
                                                     int64_t y_stride, int nsplit,
+                                                    const float* __restrict__ Ysp,
                                                     const double* __restrict__ Gneg,
                                                     float* __restrict__ X, float* __restrict__ V,
                                                     int64_t rows, float eta, float gamma,
@@ -361,6 +362,13 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Yp
         s1 += (double)v.y;
         s2 += (double)v.z;
         s3 += (double)v.w;
+      }
+      if (Ysp) {
+        const float4 w = *reinterpret_cast<const float4*>(Ysp + row * RP + 4 * c4);
+        s0 += (double)w.x;
+        s1 += (double)w.y;
+        s2 += (double)w.z;
+        s3 += (double)w.w;
       }
     }
     double* d = &ys[i * LS + 4 * c4];
@@ -427,7 +435,8 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Yp
   if (bad) flag(status, STATUS_NONFINITE, step_id);
 }
 
-hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const double* Gneg,
+hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const float* Ysp,
+                        const double* Gneg,
                         float* X, float* V, int64_t rows, int rp, float eta, float gamma,
                         int* status, int step_id, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
@@ -435,7 +444,7 @@ hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const 
   case R: {                                                                                  \
     constexpr int RW = ApplyCfg<R>::RW;                                                      \
     hipLaunchKernelGGL((apply_kernel<R>), dim3((unsigned)((rows + RW - 1) / RW)), dim3(256), 0, \
-                       st, Ypart, y_stride, nsplit, Gneg, X, V, rows, eta, gamma, status,    \
+                       st, Ypart, y_stride, nsplit, Ysp, Gneg, X, V, rows, eta, gamma, status,    \
                        step_id);                                                             \
     break;                                                                                   \
   }

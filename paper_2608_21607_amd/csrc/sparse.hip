@@ -21,7 +21,8 @@ __global__ __launch_bounds__(256) void sparse_kernel(const Item* __restrict__ it
                                                      const float* __restrict__ X,
                                                      const float* __restrict__ P,
                                                      float* __restrict__ Y,
-                                                     float* __restrict__ scratch) {
+                                                     float* __restrict__ scratch,
+                                                     int accumulate) {
   constexpr int RP = T * E;
   const int64_t team = ((int64_t)blockIdx.x * 256 + threadIdx.x) / T;
   const int t = threadIdx.x % T;
@@ -86,7 +87,7 @@ __global__ __launch_bounds__(256) void sparse_kernel(const Item* __restrict__ it
   if (it.slot < 0) {
     float* yr = Y + (int64_t)it.row * RP;
 #pragma unroll
-    for (int e = 0; e < E; ++e) yr[t + T * e] += acc[e];
+    for (int e = 0; e < E; ++e) yr[t + T * e] = accumulate ? yr[t + T * e] + acc[e] : acc[e];
   } else {
     float* sr = scratch + (int64_t)it.slot * RP;
 #pragma unroll
@@ -97,7 +98,7 @@ __global__ __launch_bounds__(256) void sparse_kernel(const Item* __restrict__ it
 template <int T, int E>
 __global__ __launch_bounds__(256) void fixup_kernel(const Split* __restrict__ splits, int64_t n,
                                                     const float* __restrict__ scratch,
-                                                    float* __restrict__ Y) {
+                                                    float* __restrict__ Y, int accumulate) {
   constexpr int RP = T * E;
   const int64_t team = ((int64_t)blockIdx.x * 256 + threadIdx.x) / T;
   const int t = threadIdx.x % T;
@@ -113,7 +114,7 @@ __global__ __launch_bounds__(256) void fixup_kernel(const Split* __restrict__ sp
   }
   float* yr = Y + (int64_t)sp.row * RP;
 #pragma unroll
-  for (int e = 0; e < E; ++e) yr[t + T * e] += acc[e];
+  for (int e = 0; e < E; ++e) yr[t + T * e] = accumulate ? yr[t + T * e] + acc[e] : acc[e];
 }
 
 #define NMD_SPARSE_DISPATCH(rp, LAUNCH) \
@@ -139,21 +140,21 @@ static inline unsigned grid_for(int64_t teams, int T) {
 
 hipError_t launch_sparse(const Item* items, int64_t nitems, const int32_t* idx, const float* val,
                          const float* X, const float* P, int rp, float* Y, float* scratch,
-                         hipStream_t st) {
+                         int accumulate, hipStream_t st) {
   if (nitems <= 0) return hipSuccess;
 #define LAUNCH(T, E)                                                                          \
   hipLaunchKernelGGL((sparse_kernel<T, E>), dim3(grid_for(nitems, T)), dim3(256), 0, st, items, \
-                     nitems, idx, val, X, P, Y, scratch)
+                     nitems, idx, val, X, P, Y, scratch, accumulate)
   NMD_SPARSE_DISPATCH(rp, LAUNCH)
 #undef LAUNCH
 }
 
 hipError_t launch_fixup(const Split* splits, int64_t nsplits, const float* scratch, int rp,
-                        float* Y, hipStream_t st) {
+                        float* Y, int accumulate, hipStream_t st) {
   if (nsplits <= 0) return hipSuccess;
 #define LAUNCH(T, E)                                                                           \
   hipLaunchKernelGGL((fixup_kernel<T, E>), dim3(grid_for(nsplits, T)), dim3(256), 0, st, splits, \
-                     nsplits, scratch, Y)
+                     nsplits, scratch, Y, accumulate)
   NMD_SPARSE_DISPATCH(rp, LAUNCH)
 #undef LAUNCH
 }
