@@ -29,6 +29,34 @@ PEAK_HBM = 8.0e3         # GB/s, MI355X HBM3E
 
 METRIC = "ALS sweeps/sec and dense-equiv TFLOP/s (4mnr/sweep), % of fp32 MFMA peak"
 
+# HBM traffic of the fused dense kernel, from two rocprofv3 --pmc passes (FETCH_SIZE, then
+# WRITE_SIZE) scaled by the same counters on a plain copy of known size; valid only for the
+# kernel sources it was taken on.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dense_r256_graph139255_traffic.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f) for f in ("tile.h", "dense.hip")]
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(config):
+    """Bytes per dense-kernel launch from the committed counter summary, or None when the
+    summary is missing, was taken on another workload, or the kernel has changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_source_hash() or t.get("config") != config:
+        return None
+    return t.get("traffic_bytes_per_launch")
+
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
@@ -82,6 +110,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="first run one plain 1 GiB copy kernel (calibrates rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -95,6 +125,13 @@ def main():
     from workloads import gen
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_probe:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)  # reads 1 GiB, writes 1 GiB
+        torch.cuda.synchronize()
+        log("copy probe: 1 GiB read + 1 GiB written by one elementwise kernel")
+        del src, dst
     t0 = time.perf_counter()
     p = gen.config(args.config)
     log(f"workload {p.name}: m={p.m} n={p.n} r={p.r} nnz={p.nnz} "
@@ -175,7 +212,7 @@ def main():
             "peak": PEAK_FP32_MFMA,
             "unit": "TFLOP/s",
             "frac": dense_tflops / PEAK_FP32_MFMA,
-            "traffic": None,
+            "traffic": measured_traffic(args.config),
             "kernel": "dense_kernel<256>",
             "launches": dense["launches"],
             "avg_launch_ms": dense["ms"] / max(1, dense["launches"]),

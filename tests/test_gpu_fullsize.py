@@ -91,18 +91,20 @@ def test_config4_block_structure_and_initial_objective(config4):
     assert abs(f_gpu - f_orc) <= TOL * f_orc
 
 
-def test_config4_full_sweep_stepwise_sampled(config4):
-    p, S, ST = config4
-    _say("config 4 full sweep, every step checked on sampled rows")
+def stepwise_sampled(p, S, ST, n_steps=None, nsample=96):
+    """Run sweep 0 step by step on the GPU; before each step copy the state to the host and
+    let the oracle recompute that step for sampled rows (with their momentum)."""
     ctx = nmd.Context(p.m, p.n, p.r, p.block_m, p.block_n, seed=p.seed, mode=p.mode, eta=p.eta,
                       momentum=p.momentum)
     ctx.set_sparse_csr(p.row_ptr, p.col, p.val)
     rb = partition.bounds(p.m, p.block_m)
     cb = partition.bounds(p.n, p.block_n)
     steps = ctx.schedule(0)
+    if n_steps is not None:
+        steps = steps[:n_steps]
     g = np.random.default_rng(0)
-    rs = np.sort(g.choice(p.m, 96, replace=False))
-    cs = np.sort(g.choice(p.n, 96, replace=False))
+    rs = np.sort(g.choice(p.m, nsample, replace=False))
+    cs = np.sort(g.choice(p.n, nsample, replace=False))
     W, H = dev(p.W0), dev(p.H0)
     A_prevW = None  # A before the last W-step, for the momentum of the sampled rows
     B_prevH = None
@@ -134,3 +136,21 @@ def test_config4_full_sweep_stepwise_sampled(config4):
     print(f"worst step error {worst:.2e}")
     f = ctx.objective(W, H)
     assert np.isfinite(f)
+    ctx.close()
+
+
+def test_config4_full_sweep_stepwise_sampled(config4):
+    p, S, ST = config4
+    _say("config 4 full sweep, every step checked on sampled rows")
+    stepwise_sampled(p, S, ST)
+
+
+def test_config5_first_steps_sampled():
+    """The 500000 x 50000 co-occurrence workload at rank 512 (about 100M nonzeros, Zipf rows
+    and columns, the heaviest rows fully dense): the first four steps of sweep 0, each checked
+    on sampled rows."""
+    p = gen.config(5)
+    _say("config 5 full size, first steps checked on sampled rows", p.m, p.n, p.nnz)
+    S = salsa.csr_matrix(p.m, p.n, p.row_ptr, p.col, p.val)
+    ST = S.T.tocsr()
+    stepwise_sampled(p, S, ST, n_steps=4, nsample=64)
