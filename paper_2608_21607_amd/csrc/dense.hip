@@ -54,20 +54,36 @@ int dense_max_wgs(int64_t rows, int rp, int nsplit) {
   return rw ? (int)(((rows + rw - 1) / rw) * nsplit) : 0;
 }
 
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void glb_void;
+
+// Panel staging per padded rank: direct global->LDS loads into double-buffered tiles for the
+// long rows of RP >= 320 (register staging there pushes the VGPR budget into spills), register
+// staging through one LDS tile for shorter rows (a direct load moves 64 chunks of one row, so
+// short rows would leave most lanes idle).
+template <int RP>
+struct DenseStage {
+  static constexpr bool DIRECT = RP >= 320;
+  static constexpr int LS = RP + 4;
+  static constexpr int FLOATS = DIRECT ? 2 * DenseCfg<RP>::NTD * LS : DenseCfg<RP>::NT * LS;
+};
+
 template <int RP>
 __global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X, int64_t rows,
                                                     const float* __restrict__ P, int64_t blk,
                                                     float* __restrict__ Ypart, int64_t y_stride,
                                                     int nsplit, int64_t row_tiles) {
   constexpr int MI = DenseCfg<RP>::MI;
-  constexpr int NT = DenseCfg<RP>::NT;
   constexpr int CB = RP / 16;
-  constexpr int LS = RP + 4;
-  (void)LS;
-  __shared__ __attribute__((aligned(16))) float tile[NT * LS];
+  constexpr int LS = RP + 4;  // padded LDS row stride (floats)
+  constexpr bool DIRECT = DenseStage<RP>::DIRECT;
+  constexpr int NT = DIRECT ? DenseCfg<RP>::NTD : DenseCfg<RP>::NT;
+  static_assert(NT % 16 == 0, "tile shape");
+  __shared__ __attribute__((aligned(16))) float smem[DenseStage<RP>::FLOATS];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q = lane >> 4, l16 = lane & 15;
 
   const int64_t logical = xcd_logical(blockIdx.x, (int64_t)gridDim.x);
@@ -76,6 +92,29 @@ __global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X,
   const int64_t jb0 = (int64_t)split * blk / nsplit;
   const int64_t jb1 = (int64_t)(split + 1) * blk / nsplit;
   const int64_t row0 = rt * (64 * MI) + (int64_t)wave * (16 * MI);
+
+  // Direct staging: panel rows j0 .. j0+NT-1 from global memory straight into a padded LDS
+  // tile; wave w fills rows w, w+4, ...; a direct load writes 64 consecutive 16-byte chunks
+  // (lane l -> chunk l), so each instruction covers up to 64 chunks of one row.  Rows past the
+  // split end repeat its last row (finite data; their L values are zeroed below).
+  constexpr int CPR = RP / 4;
+  constexpr int IPR = (CPR + 63) / 64;
+  auto issue = [&](float* dst, int64_t j0) {
+#pragma unroll
+    for (int rr = 0; rr < NT / 4; ++rr) {
+      const int r = wave + 4 * rr;
+      int64_t jr = j0 + r;
+      if (jr > jb1 - 1) jr = jb1 - 1;
+      const float* src = P + jr * RP;
+#pragma unroll
+      for (int k = 0; k < IPR; ++k) {
+        const int c = 64 * k + lane;
+        if (CPR % 64 == 0 || c < CPR)
+          __builtin_amdgcn_global_load_lds((glb_void*)(src + 4 * c),
+                                           (lds_void*)(dst + r * LS + 256 * k), 16, 0, 0);
+      }
+    }
+  };
 
   float a[MI][RP / 4];
   load_x_frags<RP, MI>(a, X, rows, row0, q, l16);
@@ -86,23 +125,46 @@ __global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X,
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) y[mi][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  PanelTile<RP> pt;
-  if (jb0 < jb1) pt.fetch(P, jb0, jb1, tid);
-  for (int64_t j0 = jb0; j0 < jb1; j0 += NT) {
-    __syncthreads();  // previous tile fully consumed
-    pt.stash(tile, tid);
-    __syncthreads();
-    if (j0 + NT < jb1) pt.fetch(P, j0 + NT, jb1, tid);
+  auto consume = [&](const float* tile, int64_t j0) {
     const int left = (int)((jb1 - j0 + 15) / 16);
     const int njb = left < NT / 16 ? left : NT / 16;
+    const bool tail = j0 + NT > jb1;
     for (int jb = 0; jb < njb; ++jb) {
       floatx4 lt[MI];
       l_tile<RP, MI>(lt, a, tile, jb, q, l16);
+      const int64_t jrow = j0 + 16 * jb + 4 * q;  // panel row of register v = jrow + v
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) lt[mi][v] = lt[mi][v] < 0.f ? lt[mi][v] : 0.f;
+        for (int v = 0; v < 4; ++v) {
+          float z = lt[mi][v] < 0.f ? lt[mi][v] : 0.f;
+          if (DIRECT && tail && jrow + v >= jb1) z = 0.f;
+          lt[mi][v] = z;
+        }
       zb_tile<RP, MI>(y, lt, tile, jb, q, l16);
+    }
+  };
+
+  if constexpr (DIRECT) {
+    if (jb0 < jb1) issue(smem, jb0);
+    int cur = 0;
+    for (int64_t j0 = jb0; j0 < jb1; j0 += NT, cur ^= 1) {
+      __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the tile have landed
+      __syncthreads();                // every wave's have; the other buffer is free again
+      if (j0 + NT < jb1) issue(smem + (cur ^ 1) * (NT * LS), j0 + NT);
+      consume(smem + cur * (NT * LS), j0);
+    }
+  } else {
+    // register staging: the next tile's global loads are in flight while this one is consumed
+    // (rows past the split end are stored as zeros)
+    PanelTile<RP> pt;
+    if (jb0 < jb1) pt.fetch(P, jb0, jb1, tid);
+    for (int64_t j0 = jb0; j0 < jb1; j0 += NT) {
+      __syncthreads();  // previous tile fully consumed
+      pt.stash(smem, tid);
+      __syncthreads();
+      if (j0 + NT < jb1) pt.fetch(P, j0 + NT, jb1, tid);
+      consume(smem, j0);
     }
   }
 

@@ -12,17 +12,20 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 template <int RP>
 struct DenseCfg;
 // MI: 16-row blocks of X per wave (4 waves per workgroup).  NT: panel rows per LDS tile.
-template <> struct DenseCfg<16>  { static constexpr int MI = 4, NT = 512; };
-template <> struct DenseCfg<32>  { static constexpr int MI = 4, NT = 256; };
-template <> struct DenseCfg<48>  { static constexpr int MI = 4, NT = 160; };
-template <> struct DenseCfg<64>  { static constexpr int MI = 4, NT = 128; };
-template <> struct DenseCfg<128> { static constexpr int MI = 4, NT = 64; };
-template <> struct DenseCfg<192> { static constexpr int MI = 2, NT = 32; };
-template <> struct DenseCfg<256> { static constexpr int MI = 2, NT = 32; };
-template <> struct DenseCfg<320> { static constexpr int MI = 1, NT = 16; };
-template <> struct DenseCfg<384> { static constexpr int MI = 1, NT = 16; };
-template <> struct DenseCfg<448> { static constexpr int MI = 1, NT = 16; };
-template <> struct DenseCfg<512> { static constexpr int MI = 1, NT = 16; };
+// NT: panel rows per register-staged LDS tile (objective kernel).  NTD: panel rows per
+// directly loaded, double-buffered LDS tile of the contraction (a multiple of 16; both buffers
+// together within the 160 KB of LDS).
+template <> struct DenseCfg<16>  { static constexpr int MI = 4, NT = 512, NTD = 512; };
+template <> struct DenseCfg<32>  { static constexpr int MI = 4, NT = 256, NTD = 512; };
+template <> struct DenseCfg<48>  { static constexpr int MI = 4, NT = 160, NTD = 320; };
+template <> struct DenseCfg<64>  { static constexpr int MI = 4, NT = 128, NTD = 256; };
+template <> struct DenseCfg<128> { static constexpr int MI = 4, NT = 64, NTD = 128; };
+template <> struct DenseCfg<192> { static constexpr int MI = 2, NT = 32, NTD = 80; };
+template <> struct DenseCfg<256> { static constexpr int MI = 2, NT = 32, NTD = 64; };
+template <> struct DenseCfg<320> { static constexpr int MI = 1, NT = 16, NTD = 48; };
+template <> struct DenseCfg<384> { static constexpr int MI = 1, NT = 16, NTD = 32; };
+template <> struct DenseCfg<448> { static constexpr int MI = 1, NT = 16, NTD = 32; };
+template <> struct DenseCfg<512> { static constexpr int MI = 1, NT = 16, NTD = 32; };
 
 template <int RP>
 constexpr int rows_per_wg() { return 64 * DenseCfg<RP>::MI; }
@@ -111,7 +114,8 @@ __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][R
   __builtin_amdgcn_sched_group_barrier(0x100, LA < KG ? LA : KG, 0);
 #pragma unroll
   for (int t = 0; t < KG; ++t) {
-    if (t + LA < KG) bf[t + LA] = *reinterpret_cast<const float4*>(brow + 16 * (t + LA));
+    if (t + LA < KG)
+      bf[t + LA] = *reinterpret_cast<const float4*>(brow + 16 * (t + LA));
     const int h = t % NA;
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi)
@@ -139,29 +143,30 @@ __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][R
 
 // Y[i][c] += sum_j z[i][j] P[j][c] for one 16-row j-block: srcA = z (the clamped L^T
 // accumulator, register v <-> k-slice 4q + v), srcB = P[jb*16 + 4q + v][16 cb + l16] from LDS.
-// The k-slices v run in the outer loop so that consecutive MFMAs update different column
-// blocks; operands are read one k-slice ahead.
+// The (v, cb) pairs run v-major so that consecutive MFMAs update different column blocks; the
+// LDS operand is read LA pairs ahead of its MFMAs (a fixed window keeps register use flat).
 template <int RP, int MI>
 __device__ __forceinline__ void zb_tile(floatx4 (&y)[MI][RP / 16], const floatx4 (&z)[MI],
                                         const float* tile, int jb, int q, int l16) {
   constexpr int LS = RP + 4;
   constexpr int CB = RP / 16;
+  constexpr int N = 4 * CB;
+  constexpr int LA = N < 8 ? N : 8;
   const float* b2 = &tile[(jb * 16 + 4 * q) * LS + l16];
-  float bb[4][CB];
+  auto at = [&](int k) { return b2[(k / CB) * LS + 16 * (k % CB)]; };
+  float bb[N];
 #pragma unroll
-  for (int cb = 0; cb < CB; ++cb) bb[0][cb] = b2[16 * cb];
-  __builtin_amdgcn_sched_group_barrier(0x100, CB, 0);
+  for (int k = 0; k < LA; ++k) bb[k] = at(k);
+  __builtin_amdgcn_sched_group_barrier(0x100, LA, 0);
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
+  for (int k = 0; k < N; ++k) {
+    const int v = k / CB, cb = k % CB;
+    if (k + LA < N) bb[k + LA] = at(k + LA);
 #pragma unroll
-    for (int cb = 0; cb < CB; ++cb) {
-      if (v + 1 < 4) bb[v + 1][cb] = b2[(v + 1) * LS + 16 * cb];
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-        y[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(z[mi][v], bb[v][cb], y[mi][cb], 0, 0, 0);
-      if (v + 1 < 4) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, MI, 0);
-    }
+    for (int mi = 0; mi < MI; ++mi)
+      y[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(z[mi][v], bb[k], y[mi][cb], 0, 0, 0);
+    if (k + LA < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, MI, 0);
   }
 }
 
