@@ -153,6 +153,7 @@ def main():
     torch.cuda.synchronize()
     for kern in range(4):
         ctx.kernel_timing(kern, reset=True)
+    ctx.dense_blocks(reset=True)
 
     stream = torch.cuda.current_stream()
     start = torch.cuda.Event(enable_timing=True)
@@ -174,7 +175,14 @@ def main():
     sweeps_per_s = args.steps / (ms / 1e3)
     dense_equiv = 4.0 * p.m * p.n * p.r * sweeps_per_s / 1e12
     actual = 8.0 * p.m * p.n * p.r * sweeps_per_s / 1e12
-    dense_tflops = dense["flops"] / (dense["ms"] / 1e3) / 1e12 if dense["ms"] > 0 else 0.0
+    # The second product of the dense kernel runs only on the slices where max(0, L) has a
+    # positive entry; its algorithmic flops are the first product's times that fraction.
+    g2_run, g2_total = ctx.dense_blocks()
+    g2_frac = g2_run / g2_total if g2_total else 1.0
+    dense_alg_flops = dense["flops"] * (0.5 + 0.5 * g2_frac)
+    dense_s = dense["ms"] / 1e3
+    dense_tflops = dense_alg_flops / dense_s / 1e12 if dense_s > 0 else 0.0
+    dense_equiv_kernel = dense["flops"] / dense_s / 1e12 if dense_s > 0 else 0.0
     sparse_gbs = sparse["bytes"] / (sparse["ms"] / 1e3) / 1e9 if sparse["ms"] > 0 else 0.0
 
     out = {
@@ -217,6 +225,9 @@ def main():
             "kernel": f"dense_kernel<{rp}>",
             "launches": dense["launches"],
             "avg_launch_ms": dense["ms"] / max(1, dense["launches"]),
+            "flops_per_launch": dense_alg_flops / max(1, dense["launches"]),
+            "second_product_fraction_run": g2_frac,
+            "dense_equiv_kernel_tflops": dense_equiv_kernel,
         },
     }
     if not args.no_cpu_baseline:

@@ -155,14 +155,27 @@ int nmd_run_steps(nmd_ctx* ctx, float* W, float* H, const int32_t* steps, int32_
                   void* hip_stream);
 
 /*
- * nmd_clamped_contraction - the dense product on its own: Y = min(0, A B^T) B for device
- * row-major A (rows x r), B (blk x r) and Y (rows x r), i.e. Z B on the zeros of S (eq. updateZ
- * contracted as in eq. lsqA); the L tile is never written to memory (the fused kernel of
- * Sec. 4.2, in clamp-then-contract form).  r must be a multiple of 16 and <= 512; rows, blk
- * >= 1.  One fp32 accumulation over all of B.  Asynchronous on hip_stream; allocates nothing.
+ * nmd_rectified_contraction - the dense product of a step on its own: Y = max(0, A B^T) B, the
+ * rectified low-rank matrix S-hat of eq. rectify contracted with the panel (the dense term of
+ * Delta B in eqs. updateD and spLsqA), for device row-major A (rows x r), B (blk x r) and Y
+ * (rows x r, overwritten).  The L tile is never written to memory (the fused kernel of Sec.
+ * 4.2), and the second product is skipped on every slice of 16 rows x 4 panel rows where S-hat
+ * is zero (Sec. 4.3).  r must be 16, 32, 48, 64 or a multiple of 64 up to 512; rows >= 1 and
+ * <= 2^31 - 1, blk >= 1.  Padding columns of A and B must hold zeros.  One fp32 accumulation
+ * over all of B.  Asynchronous on hip_stream; allocates nothing.  NMD_EINVAL on bad arguments,
+ * NMD_EDEVICE if the launch fails.
  */
-int nmd_clamped_contraction(const float* A, int64_t rows, const float* B, int64_t blk, int32_t r,
-                            float* Y, void* hip_stream);
+int nmd_rectified_contraction(const float* A, int64_t rows, const float* B, int64_t blk,
+                              int32_t r, float* Y, void* hip_stream);
+
+/*
+ * nmd_get_dense_blocks - how much of the second product of the dense contraction the sweeps
+ * ran: *run = slices of 16 rows x 4 panel rows where max(0, L) had a positive entry and the
+ * product ran, *total = slices examined, both since the context was created or last reset
+ * here (the second product's flops are run/total of its dense count).  Synchronises the device.  reset != 0 clears both after
+ * reading.  Either output pointer may be NULL.
+ */
+int nmd_get_dense_blocks(nmd_ctx* ctx, int64_t* run, int64_t* total, int32_t reset);
 
 /*
  * nmd_get_kernel_timing - with NMD_FLAG_TIMING set, the summed device time (HIP events on the

@@ -230,6 +230,15 @@ def clamped_contraction(A, BJ):
     return np.minimum(0.0, A @ BJ.T) @ BJ
 
 
+def rectified_contraction(A, BJ):
+    """max(0, A B_J^T) B_J: the rectified low-rank matrix of eq. rectify times the panel, the
+    dense term of Delta_{:,J} B_J (eq. updateD off the nonzeros of S, contracted as in
+    eq. spLsqA)."""
+    A = np.asarray(A, dtype=np.float64)
+    BJ = np.asarray(BJ, dtype=np.float64)
+    return rectify(A @ BJ.T) @ BJ
+
+
 def zb_product(S_rows, X, P, j0, j1, rows=None):
     """Z_{I,J} P_J for the rows I of X (all rows by default): the right-hand side of the
     least-squares update in Z form (eq. lsqA restricted to the columns J)."""

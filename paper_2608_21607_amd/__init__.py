@@ -5,7 +5,7 @@ ctypes binding and `build` compiles it in-tree.
 """
 
 from .nmd import (  # noqa: F401
-    Context, NmdError, clamped_contraction, lib, header_functions,
+    Context, NmdError, rectified_contraction, lib, header_functions,
     DETERMINISTIC, STOCHASTIC, FLAG_ASYNC, FLAG_TIMING,
     KERNEL_DENSE, KERNEL_SPARSE, KERNEL_FACTOR, KERNEL_APPLY,
 )

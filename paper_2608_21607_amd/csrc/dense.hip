@@ -1,25 +1,27 @@
-// Fused dense contraction Y = min(0, X P^T) P on gfx950 fp32 MFMA.
+// Fused dense contraction Y = sgn * max(0, X P^T) P on gfx950 fp32 MFMA.
 //
-// This is the dense part of Z_{:,J} P_J (eq. updateZ contracted as in eqs. lsqA / lsqA_sto):
-// on the zeros of S the auxiliary matrix equals min(0, L); the sparse correction adds the
-// nonzeros afterwards.  The L tile is produced by MFMA, clamped in registers and consumed by
-// MFMA; neither L nor Z reaches memory (the IO-aware fusion of Sec. 4.2, with the clamp-then-
-// contract order and the raw panel P instead of a pseudo-inverse).
+// With L = X P_J^T and S-hat = max(0, L) (eq. rectify), the difference matrix of eq. updateD
+// gives Delta_{:J} P_J = sum over the nonzeros of S of (S - min(0, L)) p_j  -  S-hat P_J, and
+// the least-squares update is X <- X + Delta_{:J} P_J (P_J^T P_J)^-1 (eqs. spLsqA, lsqA_sto).
+// This kernel forms the dense term -S-hat P_J (sgn = -1); the sparse correction adds the first
+// term.  S-hat is mostly zero (the factors start with opposite signs and the fit keeps it sparse,
+// Sec. 4.3), so a wave skips the MFMAs of every 16 x 4 operand slice of S-hat that holds no
+// positive entry.  The L tile is produced by MFMA, rectified in registers and
+// consumed by MFMA; neither L nor S-hat reaches memory (the IO-aware fusion of Sec. 4.2, with
+// the raw panel P instead of a pseudo-inverse).
 //
 // Data flow (one workgroup = 4 waves, one per SIMD):
 //   * X: rows x RP row-major (RP = padded rank, zero columns beyond r).  Each wave keeps
 //     16*MI rows of X resident in VGPRs as MFMA operands for the whole launch.
-//   * P rows of the split's range stream through LDS in tiles of NT rows (row stride RP + 4
-//     floats, which keeps both read patterns below free of bank conflicts); the next tile's
-//     global loads are in flight while the current one is consumed.
+//   * P rows of the split's range stream through LDS (row stride RP + 4 floats, which keeps
+//     both read patterns free of bank conflicts); the next tile is in flight while the current
+//     one is consumed.
 //   * GEMM1 builds the transposed tile L^T (16 j x 16 i); the accumulator of lane l, register
 //     v holds L[i = l%16][j = 4(l/16) + v], which is exactly the srcA layout of GEMM2 for the
-//     k-slice {4(l/16) + v}: the clamped tile feeds GEMM2 with no data movement.
-//   * GEMM2: Y[i][c] += sum_j min(0, L[i][j]) P[j][c], srcB read from LDS as single floats.
-//   * Split-J: the workgroups of one row tile are spread over `nsplit` disjoint ranges of P
-//     rows, each writing its own partial Y; the solve kernel sums them in fp64.  Short fp32
-//     accumulation chains keep the rounding error of Y small, which matters because the Gram
-//     solve amplifies it by the condition number of P^T P.
+//     k-slice {4(l/16) + v}: the rectified tile feeds GEMM2 with no data movement.
+//   * GEMM2: Y[i][c] += sum_j max(0, L[i][j]) P[j][c], srcB read from LDS as single floats.
+//   * Split-J: the workgroups of one row tile may be spread over `nsplit` disjoint ranges of P
+//     rows, each writing its own partial Y; the solve kernel sums them in fp64.
 
 #include "tile.h"
 
@@ -72,7 +74,8 @@ template <int RP>
 __global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X, int64_t rows,
                                                     const float* __restrict__ P, int64_t blk,
                                                     float* __restrict__ Ypart, int64_t y_stride,
-                                                    int nsplit, int64_t row_tiles) {
+                                                    int nsplit, int64_t row_tiles, float sgn,
+                                                    unsigned long long* __restrict__ gemm2_blocks) {
   constexpr int MI = DenseCfg<RP>::MI;
   constexpr int CB = RP / 16;
   constexpr int LS = RP + 4;  // padded LDS row stride (floats)
@@ -125,23 +128,33 @@ __global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X,
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) y[mi][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+  unsigned int done = 0;  // 16 x 4 slices of max(0, L) that ran the second contraction (wave)
   auto consume = [&](const float* tile, int64_t j0) {
     const int left = (int)((jb1 - j0 + 15) / 16);
     const int njb = left < NT / 16 ? left : NT / 16;
     const bool tail = j0 + NT > jb1;
+    float4 pre[l_lookahead<RP>()];
+    l_prefetch<RP>(pre, tile, 0, q, l16);
     for (int jb = 0; jb < njb; ++jb) {
+      // operands of the block's second product, in flight during its first product
+      float ring[2][CB];
+      zb_read<RP>(ring[0], tile, jb, 0, q, l16);
+      zb_read<RP>(ring[1], tile, jb, 1, q, l16);
       floatx4 lt[MI];
-      l_tile<RP, MI>(lt, a, tile, jb, q, l16);
+      l_tile<RP, MI>(lt, a, pre, tile, jb, q, l16);
       const int64_t jrow = j0 + 16 * jb + 4 * q;  // panel row of register v = jrow + v
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          float z = lt[mi][v] < 0.f ? lt[mi][v] : 0.f;
+          float z = lt[mi][v] > 0.f ? lt[mi][v] : 0.f;
           if (DIRECT && tail && jrow + v >= jb1) z = 0.f;
           lt[mi][v] = z;
         }
-      zb_tile<RP, MI>(y, lt, tile, jb, q, l16);
+      const unsigned live = live_slices<MI>(lt);
+      // the next block's first panel fragments, in flight during this block's second product
+      if (jb + 1 < njb) l_prefetch<RP>(pre, tile, jb + 1, q, l16);
+      done += zb_tile<RP, MI>(y, lt, live, ring, tile, jb, q, l16);
     }
   };
 
@@ -177,26 +190,40 @@ __global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X,
       const int64_t row = row0 + 16 * mi + 4 * q + v;
       if (row < rows) {
 #pragma unroll
-        for (int cb = 0; cb < CB; ++cb) Y[row * RP + 16 * cb + l16] = y[mi][cb][v];
+        for (int cb = 0; cb < CB; ++cb) Y[row * RP + 16 * cb + l16] = sgn * y[mi][cb][v];
       }
     }
+  if (gemm2_blocks && lane == 0) atomicAdd(gemm2_blocks, (unsigned long long)done);
 }
 
 template <int RP>
 static hipError_t launch_dense_t(const float* X, int64_t rows, const float* P, int64_t blk,
-                                 float* Ypart, int64_t y_stride, int nsplit, hipStream_t st) {
+                                 float* Ypart, int64_t y_stride, int nsplit, float sgn,
+                                 unsigned long long* gemm2_blocks, hipStream_t st) {
   const int64_t row_tiles = (rows + rows_per_wg<RP>() - 1) / rows_per_wg<RP>();
   const int64_t total = row_tiles * nsplit;
   if (total <= 0) return hipSuccess;
   if (total > 0x7fffffffLL) return hipErrorInvalidValue;
   hipLaunchKernelGGL((dense_kernel<RP>), dim3((unsigned)total), dim3(256), 0, st, X, rows, P, blk,
-                     Ypart, y_stride, nsplit, row_tiles);
+                     Ypart, y_stride, nsplit, row_tiles, sgn, gemm2_blocks);
   return hipGetLastError();
 }
 
+template <int RP>
+static hipError_t wgs_per_cu_t(int* out) {
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(out, dense_kernel<RP>, 256, 0);
+}
+
+hipError_t dense_wgs_per_cu(int rp, int* out) {
+#define CALL(R) wgs_per_cu_t<R>(out)
+  NMD_RP_DISPATCH(rp, CALL)
+#undef CALL
+}
+
 hipError_t launch_dense(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
-                        float* Ypart, int64_t y_stride, int nsplit, hipStream_t st) {
-#define CALL(R) launch_dense_t<R>(X, rows, P, blk, Ypart, y_stride, nsplit, st)
+                        float* Ypart, int64_t y_stride, int nsplit, float sgn,
+                        unsigned long long* gemm2_blocks, hipStream_t st) {
+#define CALL(R) launch_dense_t<R>(X, rows, P, blk, Ypart, y_stride, nsplit, sgn, gemm2_blocks, st)
   NMD_RP_DISPATCH(rp, CALL)
 #undef CALL
 }

@@ -29,8 +29,9 @@ thread_local std::string g_create_error;
 
 constexpr int kItemChunk = 128;    // entries per sparse work item
 constexpr int kMaxSplits = 16;     // partial outputs of the dense kernel
-constexpr int64_t kSplitRows = 1024;  // at most this many panel rows per fp32 accumulation
+constexpr int64_t kSplitRows = 8192;  // at most this many panel rows per fp32 accumulation
 constexpr int64_t kTargetWgs = 2048;  // dense workgroups wanted per launch (256 CUs)
+constexpr int64_t kWgFixedRows = 32;  // per-workgroup set-up and write-back, in panel rows
 constexpr int kObjSubMax = 16;        // sub-splits of a column block in the objective
 
 enum { K_DENSE = 0, K_SPARSE = 1, K_FACTOR = 2, K_APPLY = 3, K_COUNT = 4 };
@@ -236,6 +237,9 @@ struct nmd_ctx {
   int64_t objpart_count = 0;
   double* objout = nullptr;
   int* status = nullptr;
+  unsigned long long* g2 = nullptr;  // S-hat slices that ran the second contraction
+  int64_t g2_total = 0;              // slices examined (host count)
+  int64_t dense_slots = 0;           // dense workgroups resident at once (CUs x per CU)
   hipStream_t side = nullptr;     // Gram and inverse run here, beside the contraction
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   int* h_status = nullptr;   // pinned
@@ -312,6 +316,7 @@ void free_device(nmd_ctx* c) {
   dfree(c->Gpart);
   dfree(c->objout);
   dfree(c->status);
+  dfree(c->g2);
   if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
   if (c->ev_join) (void)hipEventDestroy(c->ev_join);
   if (c->side) (void)hipStreamDestroy(c->side);
@@ -331,13 +336,29 @@ void free_device(nmd_ctx* c) {
   c->dev_ready = false;
 }
 
-int64_t nsplit_for(int64_t rows, int64_t blk, int rp) {
+// Number of disjoint panel ranges (partial outputs) of one dense launch.  At least enough for
+// kTargetWgs workgroups and for at most kSplitRows panel rows per fp32 accumulation; beyond that
+// the count that wastes the least of the last round of workgroups on `slots` concurrent
+// workgroups (CUs x workgroups per CU), each workgroup costing its panel rows plus a fixed
+// equivalent of kWgFixedRows for loading its rows of X and writing its output.
+int64_t nsplit_for(int64_t rows, int64_t blk, int rp, int64_t slots) {
   const int64_t rw = nmd::dense_rows_per_wg(rp);
   const int64_t tiles = (rows + rw - 1) / rw;
-  int64_t s = std::max<int64_t>((blk + kSplitRows - 1) / kSplitRows, (kTargetWgs + tiles - 1) / tiles);
-  s = std::min<int64_t>(s, kMaxSplits);
-  s = std::min<int64_t>(s, std::max<int64_t>(1, blk / 16));
-  return std::max<int64_t>(s, 1);
+  const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(kMaxSplits, blk / 16));
+  int64_t lo = std::max<int64_t>((blk + kSplitRows - 1) / kSplitRows, (kTargetWgs + tiles - 1) / tiles);
+  lo = std::max<int64_t>(1, std::min(lo, cap));
+  if (slots < 1) return lo;
+  int64_t best = lo;
+  double best_cost = 0.0;
+  for (int64_t s = lo; s <= cap; ++s) {
+    const int64_t rounds = (tiles * s + slots - 1) / slots;
+    const double cost = (double)rounds * ((double)blk / (double)s + (double)kWgFixedRows);
+    if (s == lo || cost < best_cost * 0.995) {  // a larger count must win by a margin
+      best = s;
+      best_cost = cost;
+    }
+  }
+  return best;
 }
 
 int gram_chunks(int64_t blk) {
@@ -355,12 +376,16 @@ int ensure_device(nmd_ctx* c) {
                   prop.gcnArchName);
     c->device = dev;
     const int64_t rp = c->rp;
+    int per_cu = 0;
+    HIP_TRY(c, nmd::dense_wgs_per_cu(c->rp, &per_cu));
+    c->dense_slots = (int64_t)prop.multiProcessorCount * std::max(per_cu, 1);
     const int64_t mpad = c->m + 256, npad = c->n + 256;
     if (dalloc(&c->A, mpad * rp) != hipSuccess || dalloc(&c->B, npad * rp) != hipSuccess ||
         dalloc(&c->VA, mpad * rp) != hipSuccess || dalloc(&c->VB, npad * rp) != hipSuccess ||
         dalloc(&c->G, rp * rp) != hipSuccess || dalloc(&c->Gtmp, rp * rp + 64 * 64) != hipSuccess ||
         dalloc(&c->Gpart, (int64_t)c->gram_chunks_max * rp * rp) != hipSuccess ||
-        dalloc(&c->objout, 4) != hipSuccess || dalloc(&c->status, 2) != hipSuccess) {
+        dalloc(&c->objout, 4) != hipSuccess || dalloc(&c->status, 2) != hipSuccess ||
+        dalloc(&c->g2, 1) != hipSuccess) {
       free_device(c);
       return fail(c, NMD_ENOMEM, "device allocation of the factor workspaces failed");
     }
@@ -368,14 +393,14 @@ int ensure_device(nmd_ctx* c) {
     int64_t need = 0;
     for (size_t k = 0; k + 1 < c->cb.size(); ++k) {
       const int64_t blk = c->cb[k + 1] - c->cb[k];
-      need = std::max(need, nsplit_for(c->m, blk, c->rp) * c->m);
+      need = std::max(need, nsplit_for(c->m, blk, c->rp, c->dense_slots) * c->m);
     }
     for (size_t k = 0; k + 1 < c->rb.size(); ++k) {
       const int64_t blk = c->rb[k + 1] - c->rb[k];
-      need = std::max(need, nsplit_for(c->n, blk, c->rp) * c->n);
+      need = std::max(need, nsplit_for(c->n, blk, c->rp, c->dense_slots) * c->n);
     }
-    need = std::max(need, nsplit_for(c->m, c->n, c->rp) * c->m);
-    need = std::max(need, nsplit_for(c->n, c->m, c->rp) * c->n);
+    need = std::max(need, nsplit_for(c->m, c->n, c->rp, c->dense_slots) * c->m);
+    need = std::max(need, nsplit_for(c->n, c->m, c->rp, c->dense_slots) * c->n);
     c->ypart_floats = need * rp;
     if (dalloc(&c->Ypart, c->ypart_floats) != hipSuccess) {
       free_device(c);
@@ -400,6 +425,7 @@ int ensure_device(nmd_ctx* c) {
     }
     HIP_TRY(c, hipMemset(c->status, 0, sizeof(int)));
     HIP_TRY(c, hipMemset(c->status + 1, 0x7f, sizeof(int)));
+    HIP_TRY(c, hipMemset(c->g2, 0, sizeof(unsigned long long)));
     HIP_TRY(c, hipDeviceSynchronize());
     c->dev_ready = true;
   } else {
@@ -523,15 +549,23 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
     HIP_TRY(c, nmd::launch_inverse(c->G, c->Gtmp, rp, c->status, step_id, &Gneg, c->side));
   }
   HIP_TRY(c, hipEventRecord(c->ev_join, c->side));
-  const int64_t ns = nsplit_for(rows, blk, rp);
+  const int64_t ns = nsplit_for(rows, blk, rp, c->dense_slots);
   const int64_t y_stride = rows * rp;
   if (ns * y_stride > c->ypart_floats)
     return fail(c, NMD_EDEVICE, "internal: partial-output buffer too small");
   {
+    // U = Delta_{:J} P_J starts as -max(0, X P_J^T) P_J (eq. updateD off the nonzeros); the
+    // second contraction is skipped on the 16 x 4 slices where that rectified tile is zero
     Scope sc(c, st, K_DENSE, 4.0 * rows * (double)blk * c->r, 4.0 * (2.0 * rows + blk) * c->r);
-    HIP_TRY(c, nmd::launch_dense(X, rows, PJ, blk, rp, c->Ypart, y_stride, (int)ns, st));
+    HIP_TRY(c, nmd::launch_dense(X, rows, PJ, blk, rp, c->Ypart, y_stride, (int)ns, -1.0f, c->g2,
+                                 st));
+    // slices of 16 rows x 4 panel rows examined (those entirely past the last row never run)
+    int64_t jblocks = 0;
+    for (int64_t s = 0; s < ns; ++s) jblocks += ((s + 1) * blk / ns - s * blk / ns + 15) / 16;
+    c->g2_total += (rows + 15) / 16 * jblocks * 4;
   }
-  // Sparse correction at the nonzeros, added in place to the first partial output.  It runs
+  // Sparse correction at the nonzeros (eq. updateD there: s - l = (s - min(0, l)) - max(0, l)),
+  // added in place to the first partial output.  It runs
   // after the contraction on the same stream: beside it, its gathers would take issue slots
   // from the single MFMA wave per SIMD of the contraction.
   const int32_t b0 = block >= 0 ? block : 0;
@@ -887,8 +921,8 @@ int nmd_get_sweep_count(const nmd_ctx* c, int64_t* t) {
   return NMD_OK;
 }
 
-int nmd_clamped_contraction(const float* A, int64_t rows, const float* B, int64_t blk, int32_t r,
-                            float* Y, void* hip_stream) {
+int nmd_rectified_contraction(const float* A, int64_t rows, const float* B, int64_t blk,
+                              int32_t r, float* Y, void* hip_stream) {
   g_create_error.clear();
   if (!A || !B || !Y) return fail(nullptr, NMD_EINVAL, "A, B and Y must be non-NULL");
   if (rows < 1 || blk < 1 || rows > INT32_MAX)
@@ -896,7 +930,8 @@ int nmd_clamped_contraction(const float* A, int64_t rows, const float* B, int64_
   if (r < 16 || r > 512 || nmd::padded_rank(r) != r)
     return fail(nullptr, NMD_EINVAL,
                 "r = %d unsupported: use 16, 32, 48, 64 or a multiple of 64 up to 512", r);
-  hipError_t e = nmd::launch_dense(A, rows, B, blk, r, Y, 0, 1, (hipStream_t)hip_stream);
+  hipError_t e =
+      nmd::launch_dense(A, rows, B, blk, r, Y, 0, 1, 1.0f, nullptr, (hipStream_t)hip_stream);
   if (e != hipSuccess) return fail(nullptr, NMD_EDEVICE, "launch failed: %s", hipGetErrorString(e));
   return NMD_OK;
 }
@@ -917,6 +952,26 @@ int nmd_get_kernel_timing(nmd_ctx* c, int32_t kernel, double* total_ms, int64_t*
       c->t_flops[k] = 0;
       c->t_bytes[k] = 0;
     }
+  }
+  return NMD_OK;
+}
+
+int nmd_get_dense_blocks(nmd_ctx* c, int64_t* run, int64_t* total, int32_t reset) {
+  if (!c) return NMD_EINVAL;
+  unsigned long long v = 0;
+  if (c->dev_ready) {
+    HIP_TRY(c, hipSetDevice(c->device));
+    HIP_TRY(c, hipDeviceSynchronize());
+    HIP_TRY(c, hipMemcpy(&v, c->g2, sizeof v, hipMemcpyDeviceToHost));
+  }
+  if (run) *run = (int64_t)v;
+  if (total) *total = c->g2_total;
+  if (reset) {
+    if (c->dev_ready) {
+      HIP_TRY(c, hipMemset(c->g2, 0, sizeof v));
+      HIP_TRY(c, hipDeviceSynchronize());
+    }
+    c->g2_total = 0;
   }
   return NMD_OK;
 }

@@ -30,10 +30,16 @@ int padded_rank(int r);
 // Rows per workgroup of the dense kernel for padded rank rp.
 int dense_rows_per_wg(int rp);
 
-// Y_s = min(0, X P^T) P over the split s of the rows of P (rows of X: `rows`).  Ypart holds
-// nsplit buffers of y_stride floats each (row-major rows x rp).
+// Workgroups of the dense kernel for padded rank rp that one CU holds at once.
+hipError_t dense_wgs_per_cu(int rp, int* out);
+
+// Y_s = sgn * max(0, X P^T) P over the split s of the rows of P (rows of X: `rows`).  Ypart
+// holds nsplit buffers of y_stride floats each (row-major rows x rp).  When gemm2_blocks is not
+// NULL it receives (atomically) the number of slices (16 rows x 4 panel rows) that ran the
+// second contraction; the others had no positive L entry and were skipped.
 hipError_t launch_dense(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
-                        float* Ypart, int64_t y_stride, int nsplit, hipStream_t st);
+                        float* Ypart, int64_t y_stride, int nsplit, float sgn,
+                        unsigned long long* gemm2_blocks, hipStream_t st);
 
 // Sparse correction: for every item, c = sum over its entries of (s - min(0, x_row . p_j)) p_j;
 // a row with a single item gets Y[row] = c (accumulate = 0) or Y[row] += c (accumulate = 1);
@@ -51,8 +57,9 @@ hipError_t launch_gram(const float* P, int64_t blk, int r, int rp, double* Gpart
 // Gsw <- -G^-1 by block sweeps; flags status on a non-positive pivot.  Gtmp: scratch rp x rp.
 hipError_t launch_inverse(double* G, double* Gtmp, int rp, int* status, int step_id,
                           double** result, hipStream_t st);
-// X <- X + V, V <- gamma V + eta (Ysum (-Gneg) - X), Ysum = the nsplit partial outputs plus,
-// when Ysp is not NULL, a separate correction buffer (rows x rp), summed in fp64.
+// V <- gamma V + eta U (-Gneg), X <- X + V, where U = Delta P_J is the sum (fp64) of the nsplit
+// partial outputs plus, when Ysp is not NULL, a separate correction buffer (rows x rp), and
+// -Gneg = (P_J^T P_J)^-1.
 hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const float* Ysp,
                         const double* Gneg,
                         float* X, float* V, int64_t rows, int rp, float eta, float gamma,

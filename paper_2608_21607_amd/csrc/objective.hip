@@ -75,7 +75,9 @@ __global__ __launch_bounds__(256) void objective_kernel(
     const int njb = left < NT / 16 ? left : NT / 16;
     for (int jb = 0; jb < njb; ++jb) {
       floatx4 lt[MI];
-      l_tile<RP, MI>(lt, a, tile, jb, q, l16);
+      float4 pre[l_lookahead<RP>()];
+      l_prefetch<RP>(pre, tile, jb, q, l16);
+      l_tile<RP, MI>(lt, a, pre, tile, jb, q, l16);
       const int64_t c0 = j0 + 16 * jb + 4 * q;
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi) {

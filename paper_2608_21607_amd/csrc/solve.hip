@@ -8,8 +8,9 @@
 //      after every block has been swept the matrix holds -G^-1.  For a symmetric positive
 //      definite G every pivot (a Schur complement) is positive definite, so no pivoting is
 //      needed; a non-positive pivot flags the step as not positive definite.
-//   3. Apply: X = (sum of the partial Y) G^-1, then V <- gamma V + eta (X - A), A <- A + V
-//      (heavy-ball momentum on eq. lsqA_sto; eta = 1, gamma = 0 gives A <- X).
+//   3. Apply: with U = Delta_{:J} P_J (the sum of the partial outputs), the step is U G^-1
+//      (eqs. spLsqA, lsqA_sto), then V <- gamma V + eta U G^-1, A <- A + V (heavy-ball
+//      momentum; eta = 1, gamma = 0 gives the exact least-squares update).
 
 #include "nmd_internal.h"
 
@@ -316,7 +317,7 @@ hipError_t launch_inverse(double* G, double* Gtmp, int rp, int* status, int step
 }
 
 // --------------------------------------------------------------------------------- apply --
-// X = Ysum (-Gneg) on fp64 MFMA (v_mfma_f64_16x16x4f64), then the momentum update.
+// step = U (-Gneg) = U G^-1 on fp64 MFMA (v_mfma_f64_16x16x4f64), then the momentum update.
 // A workgroup owns RW rows: their fp64 sums over the nsplit partial outputs are staged in LDS.
 // For RP >= 64 wave w owns the output column blocks w, w+4, ... over all RW/16 row blocks, so
 // each Gneg operand feeds RW/16 MFMAs; for RP < 64 wave w owns row block w and every column
@@ -422,9 +423,9 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Yp
         const int64_t row = r0 + 16 * rblock(a) + 4 * v + q;
         if (row < rows) {
           const int64_t o = row * RP + 16 * cblock(b) + l16;
-          const double xnew = -acc[a][b][v];
+          const double stepv = -acc[a][b][v];
           const double xa = (double)X[o];
-          const double vn = (double)gamma * (double)V[o] + (double)eta * (xnew - xa);
+          const double vn = (double)gamma * (double)V[o] + (double)eta * stepv;
           const float xf = (float)(xa + vn);
           const float vf = (float)vn;
           bad |= !isfinite(xf) || !isfinite(vf);

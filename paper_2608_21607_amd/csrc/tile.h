@@ -89,16 +89,32 @@ struct PanelTile {
   }
 };
 
+// Fragment groups of the panel read ahead of the first product's MFMAs.
+template <int RP>
+constexpr int l_lookahead() { return RP / 16 < 3 ? RP / 16 : 3; }
+
+// The first l_lookahead<RP>() fragment groups of j-block jb, read before the block's MFMAs
+// start (typically while the previous block's second product runs).
+template <int RP>
+__device__ __forceinline__ void l_prefetch(float4 (&pre)[l_lookahead<RP>()], const float* tile,
+                                           int jb, int q, int l16) {
+  const float* brow = &tile[(jb * 16 + l16) * (RP + 4) + 4 * q];
+#pragma unroll
+  for (int t = 0; t < l_lookahead<RP>(); ++t) pre[t] = *reinterpret_cast<const float4*>(brow + 16 * t);
+}
+
 // Transposed L tile of one 16-row j-block: lt[mi] lane l, register v holds
 // L[i = row0 + 16 mi + l16][j = jb*16 + 4q + v] (srcA = panel rows, srcB = X rows, both over
-// the permuted k order 16t + 4q + c, one ds_read_b128 per four k-steps).  The panel fragments
-// of group t+2 are read while the MFMAs of group t run, so LDS latency stays off the MFMA pipe.
+// the permuted k order 16t + 4q + c, one ds_read_b128 per four k-steps).  `pre` holds the first
+// fragment groups (l_prefetch); group t + LA is read while the MFMAs of group t run, so LDS
+// latency stays off the MFMA pipe.
 template <int RP, int MI>
 __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][RP / 4],
-                                       const float* tile, int jb, int q, int l16) {
+                                       const float4 (&pre)[l_lookahead<RP>()], const float* tile,
+                                       int jb, int q, int l16) {
   constexpr int LS = RP + 4;
   constexpr int KG = RP / 16;
-  constexpr int LA = 3;  // fragment groups in flight
+  constexpr int LA = l_lookahead<RP>();
   // NA accumulators per row block (k-groups taken round-robin) so that consecutive MFMAs of
   // a wave never wait on each other's results
   constexpr int NA = MI >= 4 ? 1 : 4 / MI;
@@ -110,8 +126,7 @@ __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][R
   const float* brow = &tile[(jb * 16 + l16) * LS + 4 * q];
   float4 bf[KG];
 #pragma unroll
-  for (int t = 0; t < LA && t < KG; ++t) bf[t] = *reinterpret_cast<const float4*>(brow + 16 * t);
-  __builtin_amdgcn_sched_group_barrier(0x100, LA < KG ? LA : KG, 0);
+  for (int t = 0; t < LA; ++t) bf[t] = pre[t];
 #pragma unroll
   for (int t = 0; t < KG; ++t) {
     if (t + LA < KG)
@@ -141,33 +156,71 @@ __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][R
   }
 }
 
-// Y[i][c] += sum_j z[i][j] P[j][c] for one 16-row j-block: srcA = z (the clamped L^T
-// accumulator, register v <-> k-slice 4q + v), srcB = P[jb*16 + 4q + v][16 cb + l16] from LDS.
-// The (v, cb) pairs run v-major so that consecutive MFMAs update different column blocks; the
-// LDS operand is read LA pairs ahead of its MFMAs (a fixed window keeps register use flat).
+// srcB operands of the second product for k-slice v of j-block jb: P[jb*16 + 4q + v][16 cb + l16].
+template <int RP>
+__device__ __forceinline__ void zb_read(float (&bb)[RP / 16], const float* tile, int jb, int v,
+                                        int q, int l16) {
+  const float* b2 = &tile[(jb * 16 + 4 * q + v) * (RP + 4) + l16];
+#pragma unroll
+  for (int cb = 0; cb < RP / 16; ++cb) bb[cb] = b2[16 * cb];
+}
+
+// Which 16 x 4 slices (mi, v) of the rectified tile z = max(0, L) hold a positive entry: bit
+// 4 mi + v of the wave-uniform result.
+template <int MI>
+__device__ __forceinline__ unsigned live_slices(const floatx4 (&z)[MI]) {
+  unsigned m = 0;
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      if (__any(z[mi][v] > 0.f)) m |= 1u << (4 * mi + v);
+  return m;
+}
+
+// Y[i][c] += sum_j z[i][j] P[j][c] for one 16-row j-block, z = max(0, L) >= 0: srcA = z (the
+// rectified L^T accumulator, register v <-> k-slice 4q + v), srcB from LDS.  A 16 x 4 slice
+// (mi, v) of z is one srcA operand; it contributes only if one of its entries is positive (bit
+// 4 mi + v of `live`), so the MFMAs of zero slices are skipped (S-hat is sparse).  `ring`
+// arrives holding the srcB operands of slices 0 and 1 (zb_read); slice v + 2 is read into the
+// slot of slice v once that slice's MFMAs are issued.  Returns the number of slices that ran.
 template <int RP, int MI>
-__device__ __forceinline__ void zb_tile(floatx4 (&y)[MI][RP / 16], const floatx4 (&z)[MI],
-                                        const float* tile, int jb, int q, int l16) {
-  constexpr int LS = RP + 4;
+__device__ __forceinline__ int zb_tile(floatx4 (&y)[MI][RP / 16], const floatx4 (&z)[MI],
+                                       unsigned live, float (&ring)[2][RP / 16],
+                                       const float* tile, int jb, int q, int l16) {
   constexpr int CB = RP / 16;
-  constexpr int N = 4 * CB;
-  constexpr int LA = N < 8 ? N : 8;
-  const float* b2 = &tile[(jb * 16 + 4 * q) * LS + l16];
-  auto at = [&](int k) { return b2[(k / CB) * LS + 16 * (k % CB)]; };
-  float bb[N];
+  // with fewer than 4 column blocks consecutive MFMAs of one row block would depend on each
+  // other, so there the row blocks are interleaved and a slice runs for all of them
+  constexpr bool PER_MI = CB >= 4;
+  int ran = 0;
 #pragma unroll
-  for (int k = 0; k < LA; ++k) bb[k] = at(k);
-  __builtin_amdgcn_sched_group_barrier(0x100, LA, 0);
+  for (int v = 0; v < 4; ++v) {
+    if constexpr (PER_MI) {
 #pragma unroll
-  for (int k = 0; k < N; ++k) {
-    const int v = k / CB, cb = k % CB;
-    if (k + LA < N) bb[k + LA] = at(k + LA);
+      for (int mi = 0; mi < MI; ++mi) {
+        if (live & (1u << (4 * mi + v))) {
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-      y[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(z[mi][v], bb[k], y[mi][cb], 0, 0, 0);
-    if (k + LA < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, MI, 0);
+          for (int cb = 0; cb < CB; ++cb)
+            y[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(z[mi][v], ring[v & 1][cb], y[mi][cb], 0, 0, 0);
+          ++ran;
+        }
+      }
+    } else {
+      unsigned any = 0;
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi) any |= live & (1u << (4 * mi + v));
+      if (any) {
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int mi = 0; mi < MI; ++mi)
+            y[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(z[mi][v], ring[v & 1][cb], y[mi][cb], 0, 0, 0);
+        ran += MI;
+      }
+    }
+    if (v + 2 < 4) zb_read<RP>(ring[v & 1], tile, jb, v + 2, q, l16);
   }
+  return ran;
 }
 
 #define NMD_RP_DISPATCH(rp, CALL) \

@@ -64,7 +64,8 @@ def lib() -> C.CDLL:
         "nmd_reset": (I32, [P]),
         "nmd_get_sweep_count": (I32, [P, C.POINTER(I64)]),
         "nmd_run_steps": (I32, [P, P, P, P, I32, P]),
-        "nmd_clamped_contraction": (I32, [P, I64, P, I64, I32, P, P]),
+        "nmd_rectified_contraction": (I32, [P, I64, P, I64, I32, P, P]),
+        "nmd_get_dense_blocks": (I32, [P, P, P, I32]),
         "nmd_get_kernel_timing": (I32, [P, I32, C.POINTER(C.c_double), C.POINTER(I64),
                                         C.POINTER(C.c_double), C.POINTER(C.c_double), I32]),
     }
@@ -198,15 +199,24 @@ class Context:
                                            C.byref(fl), C.byref(by), int(bool(reset))), self._p)
         return {"ms": ms.value, "launches": n.value, "flops": fl.value, "bytes": by.value}
 
+    def dense_blocks(self, reset=False):
+        """(run, total): slices (16 rows x 4 panel rows) of the dense contraction's second
+        product that ran, and that were examined, since creation or the last reset."""
+        run, tot = C.c_int64(), C.c_int64()
+        _check(lib().nmd_get_dense_blocks(self._p, C.byref(run), C.byref(tot), int(bool(reset))),
+               self._p)
+        return run.value, tot.value
 
-def clamped_contraction(A, B, Y=None, stream=None):
-    """Y = min(0, A B^T) B on the GPU (A: rows x r, B: blk x r, float32 CUDA tensors)."""
+
+def rectified_contraction(A, B, Y=None, stream=None):
+    """Y = max(0, A B^T) B on the GPU (A: rows x r, B: blk x r, float32 CUDA tensors)."""
     import torch
     rows, r = A.shape
     blk = B.shape[0]
     if Y is None:
         Y = torch.empty((rows, r), dtype=torch.float32, device=A.device)
-    _check(lib().nmd_clamped_contraction(_dev_ptr(A, (rows, r), "A"), int(rows),
-                                         _dev_ptr(B, (blk, r), "B"), int(blk), int(r),
-                                         _dev_ptr(Y, (rows, r), "Y"), _stream_handle(stream)), None)
+    _check(lib().nmd_rectified_contraction(_dev_ptr(A, (rows, r), "A"), int(rows),
+                                           _dev_ptr(B, (blk, r), "B"), int(blk), int(r),
+                                           _dev_ptr(Y, (rows, r), "Y"), _stream_handle(stream)),
+           None)
     return Y

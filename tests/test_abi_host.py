@@ -117,12 +117,21 @@ def test_no_positive_entry_and_state_errors(L):
     ctx.close()
 
 
-def test_clamped_contraction_argument_checks(L):
+def test_rectified_contraction_argument_checks(L):
     fake = C.c_void_p(0x1000)
-    for r in (8, 17, 96, 576):
-        assert L.nmd_clamped_contraction(fake, 10, fake, 10, r, fake, None) == nmd.EINVAL
-    assert L.nmd_clamped_contraction(fake, 0, fake, 10, 16, fake, None) == nmd.EINVAL
-    assert L.nmd_clamped_contraction(None, 10, fake, 10, 16, fake, None) == nmd.EINVAL
+    for r in (8, 17, 80, 96, 576):
+        assert L.nmd_rectified_contraction(fake, 10, fake, 10, r, fake, None) == nmd.EINVAL
+    assert L.nmd_rectified_contraction(fake, 0, fake, 10, 16, fake, None) == nmd.EINVAL
+    assert L.nmd_rectified_contraction(fake, 10, fake, 0, 16, fake, None) == nmd.EINVAL
+    assert L.nmd_rectified_contraction(None, 10, fake, 10, 16, fake, None) == nmd.EINVAL
+
+
+def test_dense_blocks_before_device_use(L):
+    """The skip counters of a context that has not touched the GPU read zero."""
+    ctx = nmd.Context(40, 30, 4, 16, 16)
+    assert ctx.dense_blocks() == (0, 0)
+    assert L.nmd_get_dense_blocks(None, None, None, 0) == nmd.EINVAL
+    ctx.close()
 
 
 def test_schedule_matches_golden_and_oracle(L):

@@ -4,7 +4,7 @@ Bars:
   * the block schedule and the per-block nonzero counts: bit-exact (checked on the host side
     in test_abi_host.py, repeated here for the GPU workloads);
   * W, H after one sweep and the objective: relative Frobenius error <= 1e-4;
-  * the standalone clamped contraction (one fp32 accumulation, no solve): <= 2e-5.
+  * the standalone rectified contraction (one fp32 accumulation, no solve): <= 2e-5.
 Every test prints the case it runs before touching the GPU.
 """
 
@@ -74,31 +74,59 @@ def test_gpu_is_gfx950():
 
 # ------------------------------------------------------------------ the dense kernel alone
 @pytest.mark.parametrize("r", [16, 32, 48, 64, 128, 192, 256, 320, 384, 448, 512])
-def test_clamped_contraction_kernel(r):
+def test_rectified_contraction_kernel(r):
     rows, blk = 333 + r % 7, 517
-    _say("clamped_contraction", rows, blk, r)
+    _say("rectified_contraction", rows, blk, r)
     g = np.random.default_rng(r)
     A = g.standard_normal((rows, r)).astype(np.float32)
     B = g.standard_normal((blk, r)).astype(np.float32)
-    Y = nmd.clamped_contraction(dev(A), dev(B))
+    Y = nmd.rectified_contraction(dev(A), dev(B))
     torch.cuda.synchronize()
-    want = salsa.clamped_contraction(A, B)
+    want = salsa.rectified_contraction(A, B)
     assert rel(Y.cpu().numpy(), want) < 2e-5
 
 
+def _sparse_sign_case(rows, blk, r, seed):
+    """A > 0 and B < 0 (S-hat = 0) except a few panel rows flipped positive, so that only some
+    16-row panel blocks (and within them only some entries) have a positive L."""
+    g = np.random.default_rng(seed)
+    A = np.abs(g.standard_normal((rows, r))).astype(np.float32)
+    B = -np.abs(g.standard_normal((blk, r))).astype(np.float32)
+    flip = g.choice(blk, max(1, blk // 40), replace=False)
+    B[flip] = g.standard_normal((flip.size, r)).astype(np.float32)
+    return A, B
+
+
+@pytest.mark.parametrize("r", [16, 48, 64, 256, 512])
+def test_rectified_contraction_skips_zero_blocks(r):
+    """Panel blocks without a positive L are skipped: the result still matches the oracle on a
+    mostly-zero S-hat with a ragged panel tail, and an all-negative L gives exactly zero."""
+    rows, blk = 300 + r % 5, 1000 + 9
+    _say("rectified_contraction sparse S-hat", rows, blk, r)
+    A, B = _sparse_sign_case(rows, blk, r, r + 1)
+    Y = nmd.rectified_contraction(dev(A), dev(B))
+    torch.cuda.synchronize()
+    want = salsa.rectified_contraction(A, B)
+    assert np.count_nonzero(want) > 0
+    assert rel(Y.cpu().numpy(), want) < 2e-5
+    Y0 = nmd.rectified_contraction(dev(A), dev(-np.abs(B)))
+    torch.cuda.synchronize()
+    assert not torch.any(Y0 != 0).item()
+
+
 @pytest.mark.parametrize("r", [16, 32, 64, 128])
-def test_clamped_contraction_paper_shape_sampled(r):
+def test_rectified_contraction_paper_shape_sampled(r):
     """The kernel at the shape of the paper's throughput table (A: 250000 x r, B: 2500 x r);
     64 sampled output rows against the oracle."""
     rows, blk = 250_000, 2500
-    _say("clamped_contraction paper shape", rows, blk, r)
+    _say("rectified_contraction paper shape", rows, blk, r)
     g = torch.Generator(device="cuda").manual_seed(r)
     A = torch.randn((rows, r), generator=g, device="cuda")
     B = torch.randn((blk, r), generator=g, device="cuda")
-    Y = nmd.clamped_contraction(A, B)
+    Y = nmd.rectified_contraction(A, B)
     torch.cuda.synchronize()
     idx = np.random.default_rng(r).choice(rows, 64, replace=False)
-    want = salsa.clamped_contraction(A[idx].cpu().numpy(), B.cpu().numpy())
+    want = salsa.rectified_contraction(A[idx].cpu().numpy(), B.cpu().numpy())
     assert rel(Y[idx].cpu().numpy(), want) < 2e-5
 
 

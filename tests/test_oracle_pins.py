@@ -263,6 +263,33 @@ def test_clamped_contraction_identity():
     np.testing.assert_allclose(lhs, brute, atol=1e-11)
 
 
+def test_rectified_contraction_and_delta_form():
+    """max(0, L) B_J by explicit loops, and the Delta form of the right-hand side that the
+    update uses: Delta_{:,J} B_J = Z_{:,J} B_J - A (B_J^T B_J) (eq. Delta with Z from eq. updateZ)
+    equals the sum over the nonzeros of (s - min(0, l)) b_j minus max(0, L) B_J."""
+    rng = np.random.default_rng(7)
+    m, n, r, j0, j1 = 10, 13, 4, 3, 11
+    S = np.where(rng.random((m, n)) < 0.3, rng.uniform(0.2, 2.0, (m, n)), 0.0)
+    A = rng.normal(size=(m, r))
+    B = rng.normal(size=(n, r))
+    BJ = B[j0:j1]
+    rect = salsa.rectified_contraction(A, BJ)
+    brute = np.zeros((m, r))
+    for i in range(m):
+        for j in range(BJ.shape[0]):
+            brute[i] += max(0.0, float(A[i] @ BJ[j])) * BJ[j]
+    np.testing.assert_allclose(rect, brute, atol=1e-12)
+    corr = np.zeros((m, r))
+    for i in range(m):
+        for j in range(j0, j1):
+            if S[i, j] > 0:
+                corr[i] += (S[i, j] - min(0.0, float(A[i] @ B[j]))) * B[j]
+    delta_b = salsa.zb_product(sp.csr_matrix(S), A, B, j0, j1) - A @ (BJ.T @ BJ)
+    np.testing.assert_allclose(corr - rect, delta_b, atol=1e-11)
+    # a sign-constrained pair (A > 0, B < 0) has S-hat = 0 (Sec. 4.3)
+    assert not np.any(salsa.rectified_contraction(np.abs(A), -np.abs(BJ)))
+
+
 def test_zb_product_brute_force():
     """Z_{:,J} B_J by explicit loops over eq. updateZ."""
     rng = np.random.default_rng(6)
