@@ -32,8 +32,45 @@ int padded_rank(int r) {
   return ((r + 63) / 64) * 64;
 }
 
+template <int RP>
+struct DenseLaunch;
+
+int dense_rows_per_wg(int rp);
+
+int dense_max_wgs(int64_t rows, int rp, int nsplit) {
+  const int rw = dense_rows_per_wg(rp);
+  return rw ? (int)(((rows + rw - 1) / rw) * nsplit) : 0;
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void glb_void;
+
+// Launch shape per padded rank.  MI: 16-row blocks of X per wave; WAVES: waves per workgroup
+// (8 puts two waves on each SIMD, so that one wave's MFMAs cover the other's LDS waits,
+// accumulator read-outs and branches); NT: panel rows per LDS tile.  DIRECT: direct
+// global->LDS loads into double-buffered tiles (for long rows; register staging there pushes
+// the VGPR budget into spills) instead of register staging through one tile (a direct load
+// moves 64 chunks of one row, so short rows would leave most lanes idle).
+template <int RP>
+struct DenseLaunch {
+  static constexpr int MI = DenseCfg<RP>::MI;
+  static constexpr int WAVES = 4;
+  static constexpr bool DIRECT = RP >= 320;
+  static constexpr int NT = DIRECT ? DenseCfg<RP>::NTD : DenseCfg<RP>::NT;
+};
+template <>
+struct DenseLaunch<256> {
+  static constexpr int MI = 1;
+  static constexpr int WAVES = 8;
+  static constexpr bool DIRECT = true;
+  static constexpr int NT = 64;
+};
+
+template <int RP>
+constexpr int dense_rows() { return 16 * DenseLaunch<RP>::MI * DenseLaunch<RP>::WAVES; }
+
 int dense_rows_per_wg(int rp) {
-#define RW(R) rows_per_wg<R>()
+#define RW(R) dense_rows<R>()
   switch (rp) {
     case 16: return RW(16);
     case 32: return RW(32);
@@ -51,38 +88,20 @@ int dense_rows_per_wg(int rp) {
   return 0;
 }
 
-int dense_max_wgs(int64_t rows, int rp, int nsplit) {
-  const int rw = dense_rows_per_wg(rp);
-  return rw ? (int)(((rows + rw - 1) / rw) * nsplit) : 0;
-}
-
-typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(1))) void glb_void;
-
-// Panel staging per padded rank: direct global->LDS loads into double-buffered tiles for the
-// long rows of RP >= 320 (register staging there pushes the VGPR budget into spills), register
-// staging through one LDS tile for shorter rows (a direct load moves 64 chunks of one row, so
-// short rows would leave most lanes idle).
 template <int RP>
-struct DenseStage {
-  static constexpr bool DIRECT = RP >= 320;
-  static constexpr int LS = RP + 4;
-  static constexpr int FLOATS = DIRECT ? 2 * DenseCfg<RP>::NTD * LS : DenseCfg<RP>::NT * LS;
-};
-
-template <int RP>
-__global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X, int64_t rows,
+__global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(const float* __restrict__ X, int64_t rows,
                                                     const float* __restrict__ P, int64_t blk,
                                                     float* __restrict__ Ypart, int64_t y_stride,
                                                     int nsplit, int64_t row_tiles, float sgn,
                                                     unsigned long long* __restrict__ gemm2_blocks) {
-  constexpr int MI = DenseCfg<RP>::MI;
+  constexpr int MI = DenseLaunch<RP>::MI;
+  constexpr int WAVES = DenseLaunch<RP>::WAVES;
   constexpr int CB = RP / 16;
   constexpr int LS = RP + 4;  // padded LDS row stride (floats)
-  constexpr bool DIRECT = DenseStage<RP>::DIRECT;
-  constexpr int NT = DIRECT ? DenseCfg<RP>::NTD : DenseCfg<RP>::NT;
-  static_assert(NT % 16 == 0, "tile shape");
-  __shared__ __attribute__((aligned(16))) float smem[DenseStage<RP>::FLOATS];
+  constexpr bool DIRECT = DenseLaunch<RP>::DIRECT;
+  constexpr int NT = DenseLaunch<RP>::NT;
+  static_assert(NT % 16 == 0 && NT % WAVES == 0, "tile shape");
+  __shared__ __attribute__((aligned(16))) float smem[(DIRECT ? 2 : 1) * NT * LS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -94,27 +113,35 @@ __global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X,
   const int64_t rt = logical - (int64_t)split * row_tiles;
   const int64_t jb0 = (int64_t)split * blk / nsplit;
   const int64_t jb1 = (int64_t)(split + 1) * blk / nsplit;
-  const int64_t row0 = rt * (64 * MI) + (int64_t)wave * (16 * MI);
+  const int64_t row0 = rt * dense_rows<RP>() + (int64_t)wave * (16 * MI);
 
   // Direct staging: panel rows j0 .. j0+NT-1 from global memory straight into a padded LDS
-  // tile; wave w fills rows w, w+4, ...; a direct load writes 64 consecutive 16-byte chunks
-  // (lane l -> chunk l), so each instruction covers up to 64 chunks of one row.  Rows past the
-  // split end repeat its last row (finite data; their L values are zeroed below).
+  // tile; wave w fills rows w, w + WAVES, ...; a direct load writes 64 consecutive 16-byte
+  // chunks (lane l -> chunk l), so each instruction covers up to 64 chunks of one row.  Rows
+  // past the split end are zero-filled with ordinary LDS stores (their L is then zero).
   constexpr int CPR = RP / 4;
   constexpr int IPR = (CPR + 63) / 64;
   auto issue = [&](float* dst, int64_t j0) {
 #pragma unroll
-    for (int rr = 0; rr < NT / 4; ++rr) {
-      const int r = wave + 4 * rr;
-      int64_t jr = j0 + r;
-      if (jr > jb1 - 1) jr = jb1 - 1;
-      const float* src = P + jr * RP;
+    for (int rr = 0; rr < NT / WAVES; ++rr) {
+      const int r = wave + WAVES * rr;
+      const int64_t jr = j0 + r;
+      if (jr < jb1) {
+        const float* src = P + jr * RP;
 #pragma unroll
-      for (int k = 0; k < IPR; ++k) {
-        const int c = 64 * k + lane;
-        if (CPR % 64 == 0 || c < CPR)
-          __builtin_amdgcn_global_load_lds((glb_void*)(src + 4 * c),
-                                           (lds_void*)(dst + r * LS + 256 * k), 16, 0, 0);
+        for (int k = 0; k < IPR; ++k) {
+          const int c = 64 * k + lane;
+          if (CPR % 64 == 0 || c < CPR)
+            __builtin_amdgcn_global_load_lds((glb_void*)(src + 4 * c),
+                                             (lds_void*)(dst + r * LS + 256 * k), 16, 0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < IPR; ++k) {
+          const int c = 64 * k + lane;
+          if (CPR % 64 == 0 || c < CPR)
+            *reinterpret_cast<float4*>(dst + r * LS + 4 * c) = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
       }
     }
   };
@@ -132,25 +159,17 @@ __global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X,
   auto consume = [&](const float* tile, int64_t j0) {
     const int left = (int)((jb1 - j0 + 15) / 16);
     const int njb = left < NT / 16 ? left : NT / 16;
-    const bool tail = j0 + NT > jb1;
     float4 pre[l_lookahead<RP>()];
     l_prefetch<RP>(pre, tile, 0, q, l16);
     for (int jb = 0; jb < njb; ++jb) {
-      // operands of the block's second product, in flight during its first product
+      // the block's second-product operands are read inside its first product
       float ring[2][CB];
-      zb_read<RP>(ring[0], tile, jb, 0, q, l16);
-      zb_read<RP>(ring[1], tile, jb, 1, q, l16);
       floatx4 lt[MI];
-      l_tile<RP, MI>(lt, a, pre, tile, jb, q, l16);
-      const int64_t jrow = j0 + 16 * jb + 4 * q;  // panel row of register v = jrow + v
+      l_tile<RP, MI, true>(lt, a, pre, ring, tile, jb, q, l16);
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          float z = lt[mi][v] > 0.f ? lt[mi][v] : 0.f;
-          if (DIRECT && tail && jrow + v >= jb1) z = 0.f;
-          lt[mi][v] = z;
-        }
+        for (int v = 0; v < 4; ++v) lt[mi][v] = lt[mi][v] > 0.f ? lt[mi][v] : 0.f;
       const unsigned live = live_slices<MI>(lt);
       // the next block's first panel fragments, in flight during this block's second product
       if (jb + 1 < njb) l_prefetch<RP>(pre, tile, jb + 1, q, l16);
@@ -170,7 +189,7 @@ __global__ __launch_bounds__(256) void dense_kernel(const float* __restrict__ X,
   } else {
     // register staging: the next tile's global loads are in flight while this one is consumed
     // (rows past the split end are stored as zeros)
-    PanelTile<RP> pt;
+    PanelTile<RP, NT, 64 * WAVES> pt;
     if (jb0 < jb1) pt.fetch(P, jb0, jb1, tid);
     for (int64_t j0 = jb0; j0 < jb1; j0 += NT) {
       __syncthreads();  // previous tile fully consumed
@@ -200,18 +219,19 @@ template <int RP>
 static hipError_t launch_dense_t(const float* X, int64_t rows, const float* P, int64_t blk,
                                  float* Ypart, int64_t y_stride, int nsplit, float sgn,
                                  unsigned long long* gemm2_blocks, hipStream_t st) {
-  const int64_t row_tiles = (rows + rows_per_wg<RP>() - 1) / rows_per_wg<RP>();
+  const int64_t row_tiles = (rows + dense_rows<RP>() - 1) / dense_rows<RP>();
   const int64_t total = row_tiles * nsplit;
   if (total <= 0) return hipSuccess;
   if (total > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((dense_kernel<RP>), dim3((unsigned)total), dim3(256), 0, st, X, rows, P, blk,
+  hipLaunchKernelGGL((dense_kernel<RP>), dim3((unsigned)total), dim3(64 * DenseLaunch<RP>::WAVES), 0, st, X, rows, P, blk,
                      Ypart, y_stride, nsplit, row_tiles, sgn, gemm2_blocks);
   return hipGetLastError();
 }
 
 template <int RP>
 static hipError_t wgs_per_cu_t(int* out) {
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(out, dense_kernel<RP>, 256, 0);
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(out, dense_kernel<RP>,
+                                                      64 * DenseLaunch<RP>::WAVES, 0);
 }
 
 hipError_t dense_wgs_per_cu(int rp, int* out) {

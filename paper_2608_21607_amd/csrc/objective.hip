@@ -64,7 +64,7 @@ __global__ __launch_bounds__(256) void objective_kernel(
   }
 
   double acc = 0.0;
-  PanelTile<RP> pt;
+  PanelTile<RP, NT> pt;
   if (jb0 < jb1) pt.fetch(P, jb0, jb1, tid);
   for (int64_t j0 = jb0; j0 < jb1; j0 += NT) {
     __syncthreads();
@@ -76,8 +76,9 @@ __global__ __launch_bounds__(256) void objective_kernel(
     for (int jb = 0; jb < njb; ++jb) {
       floatx4 lt[MI];
       float4 pre[l_lookahead<RP>()];
+      float unused[2][RP / 16];
       l_prefetch<RP>(pre, tile, jb, q, l16);
-      l_tile<RP, MI>(lt, a, pre, tile, jb, q, l16);
+      l_tile<RP, MI, false>(lt, a, pre, unused, tile, jb, q, l16);
       const int64_t c0 = j0 + 16 * jb + 4 * q;
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi) {

@@ -57,21 +57,22 @@ __device__ __forceinline__ void load_x_frags(float (&a)[MI][RP / 4], const float
   }
 }
 
-// Panel tile staging: NT rows of P (row stride RP) into LDS with row stride RP + 4; rows at or
-// past `jend` are zero.  fetch() issues the global loads into registers, stash() stores them.
-template <int RP>
+// Panel tile staging: NT rows of P (row stride RP) into LDS with row stride RP + 4 by THREADS
+// threads; rows at or past `jend` are zero.  fetch() issues the global loads into registers,
+// stash() stores them.
+template <int RP, int NT_, int THREADS = 256>
 struct PanelTile {
-  static constexpr int NT = DenseCfg<RP>::NT;
+  static constexpr int NT = NT_;
   static constexpr int LS = RP + 4;
   static constexpr int NV4 = NT * RP / 4;
-  static constexpr int NLD = (NV4 + 255) / 256;
+  static constexpr int NLD = (NV4 + THREADS - 1) / THREADS;
   float4 pf[NLD];
 
   __device__ __forceinline__ void fetch(const float* __restrict__ P, int64_t j0, int64_t jend,
                                         int tid) {
 #pragma unroll
     for (int u = 0; u < NLD; ++u) {
-      const int f = tid + 256 * u;
+      const int f = tid + THREADS * u;
       const int rr = f / (RP / 4), c4 = f - rr * (RP / 4);
       const int64_t j = j0 + rr;
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -82,7 +83,7 @@ struct PanelTile {
   __device__ __forceinline__ void stash(float* tile, int tid) const {
 #pragma unroll
     for (int u = 0; u < NLD; ++u) {
-      const int f = tid + 256 * u;
+      const int f = tid + THREADS * u;
       const int rr = f / (RP / 4), c4 = f - rr * (RP / 4);
       if (f < NV4) *reinterpret_cast<float4*>(&tile[rr * LS + 4 * c4]) = pf[u];
     }
@@ -106,17 +107,19 @@ __device__ __forceinline__ void l_prefetch(float4 (&pre)[l_lookahead<RP>()], con
 // Transposed L tile of one 16-row j-block: lt[mi] lane l, register v holds
 // L[i = row0 + 16 mi + l16][j = jb*16 + 4q + v] (srcA = panel rows, srcB = X rows, both over
 // the permuted k order 16t + 4q + c, one ds_read_b128 per four k-steps).  `pre` holds the first
-// fragment groups (l_prefetch); group t + LA is read while the MFMAs of group t run, so LDS
-// latency stays off the MFMA pipe.
-template <int RP, int MI>
+// fragment groups (l_prefetch).  Each k-group issues, in this order and fenced from the next
+// group: the read of group t + LA, two srcB operands of the block's second product (slices 0
+// and 1 into `ring`, when given), then its MFMAs, which take the NA accumulators round-robin
+// per k-step so that dependent MFMAs are at least four apart.
+template <int RP, int MI, bool RING>
 __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][RP / 4],
-                                       const float4 (&pre)[l_lookahead<RP>()], const float* tile,
-                                       int jb, int q, int l16) {
+                                       const float4 (&pre)[l_lookahead<RP>()],
+                                       float (&ring)[2][RP / 16], const float* tile, int jb, int q,
+                                       int l16) {
   constexpr int LS = RP + 4;
   constexpr int KG = RP / 16;
+  constexpr int CB = RP / 16;
   constexpr int LA = l_lookahead<RP>();
-  // NA accumulators per row block (k-groups taken round-robin) so that consecutive MFMAs of
-  // a wave never wait on each other's results
   constexpr int NA = MI >= 4 ? 1 : 4 / MI;
   floatx4 acc[NA][MI];
 #pragma unroll
@@ -124,6 +127,7 @@ __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][R
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) acc[h][mi] = floatx4{0.f, 0.f, 0.f, 0.f};
   const float* brow = &tile[(jb * 16 + l16) * LS + 4 * q];
+  const float* b2 = &tile[(jb * 16 + 4 * q) * LS + l16];
   float4 bf[KG];
 #pragma unroll
   for (int t = 0; t < LA; ++t) bf[t] = pre[t];
@@ -131,28 +135,25 @@ __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][R
   for (int t = 0; t < KG; ++t) {
     if (t + LA < KG)
       bf[t + LA] = *reinterpret_cast<const float4*>(brow + 16 * (t + LA));
-    const int h = t % NA;
+    if constexpr (RING) {
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-      acc[h][mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[t].x, a[mi][4 * t + 0], acc[h][mi], 0, 0, 0);
+      for (int e = 2 * t; e < 2 * t + 2; ++e) ring[e / CB][e % CB] = b2[(e / CB) * LS + 16 * (e % CB)];
+    }
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-      acc[h][mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[t].y, a[mi][4 * t + 1], acc[h][mi], 0, 0, 0);
+    for (int c = 0; c < 4; ++c) {
+      const int h = (4 * t + c) % NA;
+      const float bk = c == 0 ? bf[t].x : c == 1 ? bf[t].y : c == 2 ? bf[t].z : bf[t].w;
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-      acc[h][mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[t].z, a[mi][4 * t + 2], acc[h][mi], 0, 0, 0);
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-      acc[h][mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[t].w, a[mi][4 * t + 3], acc[h][mi], 0, 0, 0);
-    if (t + LA < KG) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // read of group t+LA
-    __builtin_amdgcn_sched_group_barrier(0x008, 4 * MI, 0);               // MFMAs of group t
+      for (int mi = 0; mi < MI; ++mi)
+        acc[h][mi] = __builtin_amdgcn_mfma_f32_16x16x4f32(bk, a[mi][4 * t + c], acc[h][mi], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
   for (int mi = 0; mi < MI; ++mi) {
     lt[mi] = acc[0][mi];
 #pragma unroll
-    for (int h = 1; h < NA; ++h)
-      if (h < KG) lt[mi] += acc[h][mi];
+    for (int h = 1; h < NA; ++h) lt[mi] += acc[h][mi];
   }
 }
 
