@@ -65,6 +65,13 @@ struct DenseLaunch<256> {
   static constexpr bool DIRECT = true;
   static constexpr int NT = 64;
 };
+template <>
+struct DenseLaunch<128> {
+  static constexpr int MI = 2;
+  static constexpr int WAVES = 8;
+  static constexpr bool DIRECT = true;
+  static constexpr int NT = 128;
+};
 
 template <int RP>
 constexpr int dense_rows() { return 16 * DenseLaunch<RP>::MI * DenseLaunch<RP>::WAVES; }
@@ -89,11 +96,10 @@ int dense_rows_per_wg(int rp) {
 }
 
 template <int RP>
-__global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(const float* __restrict__ X, int64_t rows,
-                                                    const float* __restrict__ P, int64_t blk,
-                                                    float* __restrict__ Ypart, int64_t y_stride,
-                                                    int nsplit, int64_t row_tiles, float sgn,
-                                                    unsigned long long* __restrict__ gemm2_blocks) {
+__global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
+    const float* __restrict__ X, int64_t rows, const float* __restrict__ P, int64_t blk,
+    float* __restrict__ Ypart, int64_t y_stride, int nsplit, int64_t row_tiles, float sgn,
+    unsigned long long* __restrict__ gemm2_blocks) {
   constexpr int MI = DenseLaunch<RP>::MI;
   constexpr int WAVES = DenseLaunch<RP>::WAVES;
   constexpr int CB = RP / 16;
@@ -223,7 +229,8 @@ static hipError_t launch_dense_t(const float* X, int64_t rows, const float* P, i
   const int64_t total = row_tiles * nsplit;
   if (total <= 0) return hipSuccess;
   if (total > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((dense_kernel<RP>), dim3((unsigned)total), dim3(64 * DenseLaunch<RP>::WAVES), 0, st, X, rows, P, blk,
+  hipLaunchKernelGGL((dense_kernel<RP>), dim3((unsigned)total),
+                     dim3(64 * DenseLaunch<RP>::WAVES), 0, st, X, rows, P, blk,
                      Ypart, y_stride, nsplit, row_tiles, sgn, gemm2_blocks);
   return hipGetLastError();
 }

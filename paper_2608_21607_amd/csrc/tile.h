@@ -183,8 +183,9 @@ __device__ __forceinline__ unsigned live_slices(const floatx4 (&z)[MI]) {
 // rectified L^T accumulator, register v <-> k-slice 4q + v), srcB from LDS.  A 16 x 4 slice
 // (mi, v) of z is one srcA operand; it contributes only if one of its entries is positive (bit
 // 4 mi + v of `live`), so the MFMAs of zero slices are skipped (S-hat is sparse).  `ring`
-// arrives holding the srcB operands of slices 0 and 1 (zb_read); slice v + 2 is read into the
-// slot of slice v once that slice's MFMAs are issued.  Returns the number of slices that ran.
+// arrives holding the srcB operands of slices 0 and 1 (read during the first product); slice
+// v + 2 is read into the slot of slice v once that slice's MFMAs are issued.  Returns the
+// number of slices that ran.
 template <int RP, int MI>
 __device__ __forceinline__ int zb_tile(floatx4 (&y)[MI][RP / 16], const floatx4 (&z)[MI],
                                        unsigned live, float (&ring)[2][RP / 16],
