@@ -47,7 +47,8 @@ typedef __attribute__((address_space(1))) void glb_void;
 
 // Launch shape per padded rank.  MI: 16-row blocks of X per wave; WAVES: waves per workgroup
 // (8 puts two waves on each SIMD, so that one wave's MFMAs cover the other's LDS waits,
-// accumulator read-outs and branches); NT: panel rows per LDS tile.  DIRECT: direct
+// accumulator read-outs and branches); NT: panel rows per LDS tile; RING: slices of the second
+// product whose operands are read during the first (4: all of them, where registers allow).  DIRECT: direct
 // global->LDS loads into double-buffered tiles (for long rows; register staging there pushes
 // the VGPR budget into spills) instead of register staging through one tile (a direct load
 // moves 64 chunks of one row, so short rows would leave most lanes idle).
@@ -57,6 +58,7 @@ struct DenseLaunch {
   static constexpr int WAVES = 4;
   static constexpr bool DIRECT = RP >= 320;
   static constexpr int NT = DIRECT ? DenseCfg<RP>::NTD : DenseCfg<RP>::NT;
+  static constexpr int RING = 2;
 };
 template <>
 struct DenseLaunch<256> {
@@ -64,6 +66,7 @@ struct DenseLaunch<256> {
   static constexpr int WAVES = 8;
   static constexpr bool DIRECT = true;
   static constexpr int NT = 64;
+  static constexpr int RING = 4;
 };
 template <>
 struct DenseLaunch<128> {
@@ -71,6 +74,7 @@ struct DenseLaunch<128> {
   static constexpr int WAVES = 8;
   static constexpr bool DIRECT = true;
   static constexpr int NT = 128;
+  static constexpr int RING = 4;
 };
 
 template <int RP>
@@ -93,6 +97,88 @@ int dense_rows_per_wg(int rp) {
   }
 #undef RW
   return 0;
+}
+
+// Direct staging of panel rows j0 .. j0+NT-1 from global memory straight into a padded LDS
+// tile; wave w fills rows w, w + WAVES, ...; a direct load writes 64 consecutive 16-byte chunks
+// (lane l -> chunk l), so each instruction covers up to 64 chunks of one row.  Rows past the
+// split end are zero-filled with ordinary LDS stores (their L is then zero).
+template <int RP>
+__device__ __forceinline__ void issue_tile(float* dst, const float* __restrict__ P, int64_t j0,
+                                           int64_t jb1, int wave, int lane) {
+  constexpr int WAVES = DenseLaunch<RP>::WAVES;
+  constexpr int NT = DenseLaunch<RP>::NT;
+  constexpr int LS = RP + 4;
+  constexpr int CPR = RP / 4;
+  constexpr int IPR = (CPR + 63) / 64;
+#pragma unroll
+  for (int rr = 0; rr < NT / WAVES; ++rr) {
+    const int r = wave + WAVES * rr;
+    const int64_t jr = j0 + r;
+    if (jr < jb1) {
+      const float* src = P + jr * RP;
+#pragma unroll
+      for (int k = 0; k < IPR; ++k) {
+        const int c = 64 * k + lane;
+        if (CPR % 64 == 0 || c < CPR)
+          __builtin_amdgcn_global_load_lds((glb_void*)(src + 4 * c),
+                                           (lds_void*)(dst + r * LS + 256 * k), 16, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < IPR; ++k) {
+        const int c = 64 * k + lane;
+        if (CPR % 64 == 0 || c < CPR)
+          *reinterpret_cast<float4*>(dst + r * LS + 4 * c) = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  }
+}
+
+// Both products over the panel rows j0 .. min(j0 + NT, jb1) - 1 held in the LDS tile; returns
+// the number of 16 x 4 slices of max(0, L) that ran the second product.
+template <int RP>
+__device__ __forceinline__ unsigned consume_tile(const float* tile, int64_t j0, int64_t jb1,
+                                                 const float (&a)[DenseLaunch<RP>::MI][RP / 4],
+                                                 floatx4 (&y)[DenseLaunch<RP>::MI][RP / 16],
+                                                 int q, int l16) {
+  constexpr int MI = DenseLaunch<RP>::MI;
+  constexpr int NT = DenseLaunch<RP>::NT;
+  constexpr int CB = RP / 16;
+  const int left = (int)((jb1 - j0 + 15) / 16);
+  const int njb = left < NT / 16 ? left : NT / 16;
+  unsigned done = 0;
+  float4 pre[l_lookahead<RP>()];
+  l_prefetch<RP>(pre, tile, 0, q, l16);
+  constexpr int NR = DenseLaunch<RP>::RING;
+  for (int jb = 0; jb < njb; ++jb) {
+    // the block's second-product operands are read inside its first product
+    float ring[NR][CB];
+    floatx4 lt[MI];
+    l_tile<RP, MI, NR>(lt, a, pre, ring, tile, jb, q, l16);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) lt[mi][v] = lt[mi][v] > 0.f ? lt[mi][v] : 0.f;
+    const unsigned live = live_slices<MI>(lt);
+    // the next block's first panel fragments, in flight during this block's second product
+    if (jb + 1 < njb) l_prefetch<RP>(pre, tile, jb + 1, q, l16);
+    done += zb_tile<RP, MI, NR>(y, lt, live, ring, tile, jb, q, l16);
+  }
+  return done;
+}
+
+// One step of the double-buffered direct pipeline: start the loads of the next tile into `nxt`
+// (when not null) and consume the current tile `cur`.  The two are distinct LDS buffers; the
+// restrict qualifiers tell the compiler that the reads of `cur` do not depend on the direct
+// loads into `nxt`, so it need not wait for those loads before the products start.
+template <int RP>
+__device__ __forceinline__ unsigned direct_step(
+    const float* __restrict__ cur, float* __restrict__ nxt, const float* __restrict__ P,
+    int64_t j0, int64_t jb1, const float (&a)[DenseLaunch<RP>::MI][RP / 4],
+    floatx4 (&y)[DenseLaunch<RP>::MI][RP / 16], int wave, int lane, int q, int l16) {
+  if (nxt) issue_tile<RP>(nxt, P, j0 + DenseLaunch<RP>::NT, jb1, wave, lane);
+  return consume_tile<RP>(cur, j0, jb1, a, y, q, l16);
 }
 
 template <int RP>
@@ -121,37 +207,6 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
   const int64_t jb1 = (int64_t)(split + 1) * blk / nsplit;
   const int64_t row0 = rt * dense_rows<RP>() + (int64_t)wave * (16 * MI);
 
-  // Direct staging: panel rows j0 .. j0+NT-1 from global memory straight into a padded LDS
-  // tile; wave w fills rows w, w + WAVES, ...; a direct load writes 64 consecutive 16-byte
-  // chunks (lane l -> chunk l), so each instruction covers up to 64 chunks of one row.  Rows
-  // past the split end are zero-filled with ordinary LDS stores (their L is then zero).
-  constexpr int CPR = RP / 4;
-  constexpr int IPR = (CPR + 63) / 64;
-  auto issue = [&](float* dst, int64_t j0) {
-#pragma unroll
-    for (int rr = 0; rr < NT / WAVES; ++rr) {
-      const int r = wave + WAVES * rr;
-      const int64_t jr = j0 + r;
-      if (jr < jb1) {
-        const float* src = P + jr * RP;
-#pragma unroll
-        for (int k = 0; k < IPR; ++k) {
-          const int c = 64 * k + lane;
-          if (CPR % 64 == 0 || c < CPR)
-            __builtin_amdgcn_global_load_lds((glb_void*)(src + 4 * c),
-                                             (lds_void*)(dst + r * LS + 256 * k), 16, 0, 0);
-        }
-      } else {
-#pragma unroll
-        for (int k = 0; k < IPR; ++k) {
-          const int c = 64 * k + lane;
-          if (CPR % 64 == 0 || c < CPR)
-            *reinterpret_cast<float4*>(dst + r * LS + 4 * c) = make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-      }
-    }
-  };
-
   float a[MI][RP / 4];
   load_x_frags<RP, MI>(a, X, rows, row0, q, l16);
 
@@ -162,35 +217,15 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
     for (int cb = 0; cb < CB; ++cb) y[mi][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   unsigned int done = 0;  // 16 x 4 slices of max(0, L) that ran the second contraction (wave)
-  auto consume = [&](const float* tile, int64_t j0) {
-    const int left = (int)((jb1 - j0 + 15) / 16);
-    const int njb = left < NT / 16 ? left : NT / 16;
-    float4 pre[l_lookahead<RP>()];
-    l_prefetch<RP>(pre, tile, 0, q, l16);
-    for (int jb = 0; jb < njb; ++jb) {
-      // the block's second-product operands are read inside its first product
-      float ring[2][CB];
-      floatx4 lt[MI];
-      l_tile<RP, MI, true>(lt, a, pre, ring, tile, jb, q, l16);
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) lt[mi][v] = lt[mi][v] > 0.f ? lt[mi][v] : 0.f;
-      const unsigned live = live_slices<MI>(lt);
-      // the next block's first panel fragments, in flight during this block's second product
-      if (jb + 1 < njb) l_prefetch<RP>(pre, tile, jb + 1, q, l16);
-      done += zb_tile<RP, MI>(y, lt, live, ring, tile, jb, q, l16);
-    }
-  };
 
   if constexpr (DIRECT) {
-    if (jb0 < jb1) issue(smem, jb0);
+    if (jb0 < jb1) issue_tile<RP>(smem, P, jb0, jb1, wave, lane);
     int cur = 0;
     for (int64_t j0 = jb0; j0 < jb1; j0 += NT, cur ^= 1) {
       __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the tile have landed
       __syncthreads();                // every wave's have; the other buffer is free again
-      if (j0 + NT < jb1) issue(smem + (cur ^ 1) * (NT * LS), j0 + NT);
-      consume(smem + cur * (NT * LS), j0);
+      done += direct_step<RP>(smem + cur * (NT * LS), j0 + NT < jb1 ? smem + (cur ^ 1) * (NT * LS) : nullptr,
+                              P, j0, jb1, a, y, wave, lane, q, l16);
     }
   } else {
     // register staging: the next tile's global loads are in flight while this one is consumed
@@ -202,7 +237,7 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
       pt.stash(smem, tid);
       __syncthreads();
       if (j0 + NT < jb1) pt.fetch(P, j0 + NT, jb1, tid);
-      consume(smem, j0);
+      done += consume_tile<RP>(smem, j0, jb1, a, y, q, l16);
     }
   }
 

@@ -76,9 +76,9 @@ __global__ __launch_bounds__(256) void objective_kernel(
     for (int jb = 0; jb < njb; ++jb) {
       floatx4 lt[MI];
       float4 pre[l_lookahead<RP>()];
-      float unused[2][RP / 16];
+      float unused[1][RP / 16];
       l_prefetch<RP>(pre, tile, jb, q, l16);
-      l_tile<RP, MI, false>(lt, a, pre, unused, tile, jb, q, l16);
+      l_tile<RP, MI, 0>(lt, a, pre, unused, tile, jb, q, l16);
       const int64_t c0 = j0 + 16 * jb + 4 * q;
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi) {

@@ -108,19 +108,20 @@ __device__ __forceinline__ void l_prefetch(float4 (&pre)[l_lookahead<RP>()], con
 // L[i = row0 + 16 mi + l16][j = jb*16 + 4q + v] (srcA = panel rows, srcB = X rows, both over
 // the permuted k order 16t + 4q + c, one ds_read_b128 per four k-steps).  `pre` holds the first
 // fragment groups (l_prefetch).  Each k-group issues, in this order and fenced from the next
-// group: the read of group t + LA, two srcB operands of the block's second product (slices 0
-// and 1 into `ring`, when given), then its MFMAs, which take the NA accumulators round-robin
-// per k-step so that dependent MFMAs are at least four apart.
-template <int RP, int MI, bool RING>
+// group: the read of group t + LA, its share of the srcB operands of the block's second product
+// (the NR slices of `ring`, NR = 0, 2 or 4), then its MFMAs, which take the NA accumulators
+// round-robin per k-step so that dependent MFMAs are at least two apart.
+template <int RP, int MI, int NR>
 __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][RP / 4],
                                        const float4 (&pre)[l_lookahead<RP>()],
-                                       float (&ring)[2][RP / 16], const float* tile, int jb, int q,
-                                       int l16) {
+                                       float (&ring)[NR > 0 ? NR : 1][RP / 16], const float* tile,
+                                       int jb, int q, int l16) {
   constexpr int LS = RP + 4;
   constexpr int KG = RP / 16;
   constexpr int CB = RP / 16;
   constexpr int LA = l_lookahead<RP>();
-  constexpr int NA = MI >= 4 ? 1 : 4 / MI;
+  constexpr int NA = MI >= 2 ? 1 : 2;
+  constexpr int PER = NR * CB / KG;  // ring values read per k-group (NR * CB = NR * KG)
   floatx4 acc[NA][MI];
 #pragma unroll
   for (int h = 0; h < NA; ++h)
@@ -135,9 +136,10 @@ __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][R
   for (int t = 0; t < KG; ++t) {
     if (t + LA < KG)
       bf[t + LA] = *reinterpret_cast<const float4*>(brow + 16 * (t + LA));
-    if constexpr (RING) {
+    if constexpr (NR > 0) {
 #pragma unroll
-      for (int e = 2 * t; e < 2 * t + 2; ++e) ring[e / CB][e % CB] = b2[(e / CB) * LS + 16 * (e % CB)];
+      for (int e = PER * t; e < PER * t + PER; ++e)
+        ring[e / CB][e % CB] = b2[(e / CB) * LS + 16 * (e % CB)];
     }
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -183,13 +185,14 @@ __device__ __forceinline__ unsigned live_slices(const floatx4 (&z)[MI]) {
 // rectified L^T accumulator, register v <-> k-slice 4q + v), srcB from LDS.  A 16 x 4 slice
 // (mi, v) of z is one srcA operand; it contributes only if one of its entries is positive (bit
 // 4 mi + v of `live`), so the MFMAs of zero slices are skipped (S-hat is sparse).  `ring`
-// arrives holding the srcB operands of slices 0 and 1 (read during the first product); slice
-// v + 2 is read into the slot of slice v once that slice's MFMAs are issued.  Returns the
-// number of slices that ran.
-template <int RP, int MI>
+// arrives holding the srcB operands of the first NR slices (read during the first product);
+// with NR = 2, slice v + 2 is read into the slot of slice v once that slice's MFMAs are issued.
+// Returns the number of slices that ran.
+template <int RP, int MI, int NR>
 __device__ __forceinline__ int zb_tile(floatx4 (&y)[MI][RP / 16], const floatx4 (&z)[MI],
-                                       unsigned live, float (&ring)[2][RP / 16],
+                                       unsigned live, float (&ring)[NR][RP / 16],
                                        const float* tile, int jb, int q, int l16) {
+  static_assert(NR == 2 || NR == 4, "ring depth");
   constexpr int CB = RP / 16;
   // with fewer than 4 column blocks consecutive MFMAs of one row block would depend on each
   // other, so there the row blocks are interleaved and a slice runs for all of them
@@ -197,13 +200,14 @@ __device__ __forceinline__ int zb_tile(floatx4 (&y)[MI][RP / 16], const floatx4 
   int ran = 0;
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
+    const int slot = NR == 4 ? v : (v & 1);
     if constexpr (PER_MI) {
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi) {
         if (live & (1u << (4 * mi + v))) {
 #pragma unroll
           for (int cb = 0; cb < CB; ++cb)
-            y[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(z[mi][v], ring[v & 1][cb], y[mi][cb], 0, 0, 0);
+            y[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(z[mi][v], ring[slot][cb], y[mi][cb], 0, 0, 0);
           ++ran;
         }
       }
@@ -216,11 +220,13 @@ __device__ __forceinline__ int zb_tile(floatx4 (&y)[MI][RP / 16], const floatx4 
         for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
           for (int mi = 0; mi < MI; ++mi)
-            y[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(z[mi][v], ring[v & 1][cb], y[mi][cb], 0, 0, 0);
+            y[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(z[mi][v], ring[slot][cb], y[mi][cb], 0, 0, 0);
         ran += MI;
       }
     }
-    if (v + 2 < 4) zb_read<RP>(ring[v & 1], tile, jb, v + 2, q, l16);
+    if constexpr (NR == 2) {
+      if (v + 2 < 4) zb_read<RP>(ring[v & 1], tile, jb, v + 2, q, l16);
+    }
   }
   return ran;
 }
