@@ -30,6 +30,13 @@ HIPFLAGS = [
 ]
 
 
+# Per-source additions.  The dense kernel keeps its MFMA accumulators in ordinary VGPRs: with
+# accumulation registers the compiler copies the output tiles between the two register files
+# on every panel block at small ranks (measured: r = 16 at 53% of the fp32 MFMA peak instead of
+# 72%), and the large ranks are unaffected.
+EXTRA_FLAGS = {"dense.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if cand and os.path.exists(cand):
@@ -38,7 +45,7 @@ def hipcc() -> str:
 
 
 def _compile(src: str, obj: str, verbose: bool) -> None:
-    cmd = [hipcc(), *HIPFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *HIPFLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

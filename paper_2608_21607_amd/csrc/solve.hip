@@ -436,6 +436,124 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Yp
   if (bad) flag(status, STATUS_NONFINITE, step_id);
 }
 
+// Apply for r_p >= 64: a workgroup takes RW rows; each of its 4 waves computes all RW rows for
+// a quarter of the columns (column blocks w, w + 4, ...), so G^-1 is read from L2 once per RW
+// rows and quarter instead of once per 16 rows.  U (the sum of the partial outputs, formed in
+// fp64) is staged in LDS as fp32: it carries fp32 accuracy anyway, and the small tile lets two
+// workgroups share a CU, so one's loads overlap the other's MFMAs.  RW is chosen per launch
+// (taller tiles need fewer G^-1 reads, but must leave enough workgroups to fill the CUs).
+template <int RP, int RW>
+struct WideCfg {
+  static constexpr int NRB = RW / 16;   // row blocks per wave
+  static constexpr int NCB = RP / 64;   // column blocks per wave
+};
+
+// Tallest row tile whose accumulators (RW x r_p / 4 doubles per wave) stay within 64 doubles.
+template <int RP>
+constexpr int wide_max_rw() { return (16384 / RP) >= 64 ? 64 : ((16384 / RP) >= 32 ? 32 : 16); }
+
+template <int RP, int RW>
+__global__ __launch_bounds__(256, 2) void apply_wide_kernel(const float* __restrict__ Ypart,
+                                                         int64_t y_stride, int nsplit,
+                                                         const float* __restrict__ Ysp,
+                                                         const double* __restrict__ Gneg,
+                                                         float* __restrict__ X,
+                                                         float* __restrict__ V, int64_t rows,
+                                                         float eta, float gamma, int* status,
+                                                         int step_id) {
+  using C = WideCfg<RP, RW>;
+  constexpr int NRB = C::NRB, NCB = C::NCB;
+  constexpr int LS = RP + 1;
+  constexpr int PD = 2;  // prefetch distance in k-steps
+  __shared__ float ys[RW * LS];
+  if (*(volatile const int*)status != 0) return;  // an earlier step failed: factors stay
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int q = lane >> 4, l16 = lane & 15;
+  const int64_t r0 = (int64_t)blockIdx.x * RW;
+  for (int e = tid; e < RW * RP / 4; e += 256) {
+    const int i = e / (RP / 4), c4 = e - i * (RP / 4);
+    const int64_t row = r0 + i;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    if (row < rows) {
+      const float* src = Ypart + row * RP + 4 * c4;
+      for (int sp = 0; sp < nsplit; ++sp) {
+        const float4 v = *reinterpret_cast<const float4*>(src + (int64_t)sp * y_stride);
+        s0 += (double)v.x;
+        s1 += (double)v.y;
+        s2 += (double)v.z;
+        s3 += (double)v.w;
+      }
+      if (Ysp) {
+        const float4 w = *reinterpret_cast<const float4*>(Ysp + row * RP + 4 * c4);
+        s0 += (double)w.x;
+        s1 += (double)w.y;
+        s2 += (double)w.z;
+        s3 += (double)w.w;
+      }
+    }
+    float* d = &ys[i * LS + 4 * c4];
+    d[0] = (float)s0;
+    d[1] = (float)s1;
+    d[2] = (float)s2;
+    d[3] = (float)s3;
+  }
+  __syncthreads();
+  doublex4 acc[NRB][NCB];
+#pragma unroll
+  for (int a = 0; a < NRB; ++a)
+#pragma unroll
+    for (int b = 0; b < NCB; ++b) acc[a][b] = doublex4{0.0, 0.0, 0.0, 0.0};
+  const double* gcol = Gneg + 16 * wave + l16;  // column block b of this wave: + 64 b
+  double pre[PD][NCB];
+#pragma unroll
+  for (int d = 0; d < PD; ++d)
+#pragma unroll
+    for (int b = 0; b < NCB; ++b) pre[d][b] = gcol[(int64_t)(4 * d + q) * RP + 64 * b];
+  for (int k0 = 0; k0 < RP; k0 += 4 * PD) {
+#pragma unroll
+    for (int d = 0; d < PD; ++d) {
+      const int k = k0 + 4 * d;
+      double bv[NCB];
+#pragma unroll
+      for (int b = 0; b < NCB; ++b) bv[b] = pre[d][b];
+      const int kn = k + 4 * PD;
+      if (kn < RP) {
+#pragma unroll
+        for (int b = 0; b < NCB; ++b) pre[d][b] = gcol[(int64_t)(kn + q) * RP + 64 * b];
+      }
+#pragma unroll
+      for (int a = 0; a < NRB; ++a) {
+        const double av = (double)ys[(16 * a + l16) * LS + k + q];
+#pragma unroll
+        for (int b = 0; b < NCB; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv[b], acc[a][b], 0, 0, 0);
+      }
+    }
+  }
+  bool bad = false;
+#pragma unroll
+  for (int a = 0; a < NRB; ++a)
+#pragma unroll
+    for (int b = 0; b < NCB; ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t row = r0 + 16 * a + 4 * v + q;
+        if (row < rows) {
+          const int64_t o = row * RP + 16 * (wave + 4 * b) + l16;
+          const double stepv = -acc[a][b][v];
+          const double xa = (double)X[o];
+          const double vn = (double)gamma * (double)V[o] + (double)eta * stepv;
+          const float xf = (float)(xa + vn);
+          const float vf = (float)vn;
+          bad |= !isfinite(xf) || !isfinite(vf);
+          X[o] = xf;
+          V[o] = vf;
+        }
+      }
+  if (bad) flag(status, STATUS_NONFINITE, step_id);
+}
+
 hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const float* Ysp,
                         const double* Gneg,
                         float* X, float* V, int64_t rows, int rp, float eta, float gamma,
@@ -449,12 +567,33 @@ hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const 
                        step_id);                                                             \
     break;                                                                                   \
   }
+  // row tile: the tallest allowed one that still gives 4096 workgroups, else 16 rows
+  const int rw_max = rp >= 64 ? (16384 / rp >= 64 ? 64 : (16384 / rp >= 32 ? 32 : 16)) : 16;
+  int rw = 16;
+  for (int cand = rw_max; cand > 16; cand /= 2)
+    if ((rows + cand - 1) / cand >= 4096) {
+      rw = cand;
+      break;
+    }
+#define WIDE_RW(R, W)                                                                        \
+  hipLaunchKernelGGL((apply_wide_kernel<R, W>), dim3((unsigned)((rows + W - 1) / W)), dim3(256), \
+                     0, st, Ypart, y_stride, nsplit, Ysp, Gneg, X, V, rows, eta, gamma, status,   \
+                     step_id)
+#define WIDE(R)                                                                              \
+  case R: {                                                                                  \
+    if (rw >= 64 && wide_max_rw<R>() >= 64) WIDE_RW(R, (wide_max_rw<R>() >= 64 ? 64 : 16)); \
+    else if (rw >= 32 && wide_max_rw<R>() >= 32) WIDE_RW(R, (wide_max_rw<R>() >= 32 ? 32 : 16)); \
+    else WIDE_RW(R, 16);                                                                     \
+    break;                                                                                   \
+  }
   switch (rp) {
-    CASE(16) CASE(32) CASE(48) CASE(64) CASE(128) CASE(192) CASE(256) CASE(320) CASE(384)
-    CASE(448) CASE(512)
+    CASE(16) CASE(32) CASE(48)
+    WIDE(64) WIDE(128) WIDE(192) WIDE(256) WIDE(320) WIDE(384) WIDE(448) WIDE(512)
     default: return hipErrorInvalidValue;
   }
 #undef CASE
+#undef WIDE
+#undef WIDE_RW
   return hipGetLastError();
 }
 
