@@ -166,7 +166,8 @@ def main():
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop)
     log(f"timed {args.steps} sweeps: {ms:.1f} ms")
-    f1 = ctx.objective(W, H)
+    m1 = ctx.metrics(W, H)
+    f1 = m1["objective"]
     assert np.isfinite(f1)
 
     rp = ((p.r + 15) // 16) * 16 if p.r <= 64 else ((p.r + 63) // 64) * 64  # padded rank
@@ -215,6 +216,7 @@ def main():
             "gram_inverse": factor["ms"] / args.steps, "solve_apply": apply_["ms"] / args.steps,
         },
         "objective_before_after": [f0, f1],
+        "rmse_wjd_after": [m1["rmse"], m1["wjd"]],
         "roofline": {
             "bound": "mfma",
             "achieved": dense_tflops,

@@ -109,6 +109,16 @@ int nmd_als_block_sweep(nmd_ctx* ctx, float* W, float* H, int32_t n_sweeps, void
  */
 int nmd_objective(nmd_ctx* ctx, const float* W, const float* H, double* out_obj, void* hip_stream);
 
+/*
+ * nmd_metrics - the objective together with the two reconstruction measures of S-hat =
+ * max(0, W H) (eq. rectify), from one pass over L: out[0] = the objective of nmd_objective,
+ * out[1] = ||S - S-hat||_F / ||S||_F (eq. RMSE), out[2] = 1 - sum min(S, S-hat) /
+ * sum max(S, S-hat) (eq. WJD; 1 when both sums vanish).  `out` is host memory for 3 doubles.
+ * W, H as in nmd_als_block_sweep (read only).  Products are formed in fp32 and summed in fp64.
+ * Synchronises the stream.  Errors as for nmd_objective.
+ */
+int nmd_metrics(nmd_ctx* ctx, const float* W, const float* H, double* out, void* hip_stream);
+
 /* nmd_destroy - frees the context and its device memory; NULL-safe. */
 void nmd_destroy(nmd_ctx* ctx);
 

@@ -384,7 +384,7 @@ int ensure_device(nmd_ctx* c) {
         dalloc(&c->VA, mpad * rp) != hipSuccess || dalloc(&c->VB, npad * rp) != hipSuccess ||
         dalloc(&c->G, rp * rp) != hipSuccess || dalloc(&c->Gtmp, rp * rp + 64 * 64) != hipSuccess ||
         dalloc(&c->Gpart, (int64_t)c->gram_chunks_max * rp * rp) != hipSuccess ||
-        dalloc(&c->objout, 4) != hipSuccess || dalloc(&c->status, 2) != hipSuccess ||
+        dalloc(&c->objout, 8) != hipSuccess || dalloc(&c->status, 2) != hipSuccess ||
         dalloc(&c->g2, 1) != hipSuccess) {
       free_device(c);
       return fail(c, NMD_ENOMEM, "device allocation of the factor workspaces failed");
@@ -408,7 +408,7 @@ int ensure_device(nmd_ctx* c) {
                   (long long)c->ypart_floats);
     }
     if (hipHostMalloc((void**)&c->h_status, 2 * sizeof(int)) != hipSuccess ||
-        hipHostMalloc((void**)&c->h_obj, 4 * sizeof(double)) != hipSuccess) {
+        hipHostMalloc((void**)&c->h_obj, 8 * sizeof(double)) != hipSuccess) {
       free_device(c);
       return fail(c, NMD_ENOMEM, "pinned host allocation failed");
     }
@@ -457,7 +457,7 @@ int ensure_device(nmd_ctx* c) {
     }
     c->scratch_floats = std::max<int64_t>(1, std::max(c->ws.max_slots, c->hs.max_slots)) * c->rp;
     // objective partials: one per (row tile, column block, sub-split)
-    c->objpart_count = (int64_t)nmd::dense_max_wgs(c->m, c->rp, 1) * c->ws.nblk() * kObjSubMax + 1;
+    c->objpart_count = 5 * (int64_t)nmd::dense_max_wgs(c->m, c->rp, 1) * c->ws.nblk() * kObjSubMax + 1;
     if (dalloc(&c->scratch, c->scratch_floats) != hipSuccess ||
         dalloc(&c->objpart, c->objpart_count) != hipSuccess) {
       free_sparse_device(c);
@@ -639,6 +639,33 @@ int check_ready(nmd_ctx* c, const void* W, const void* H) {
   c->err.clear();
   if (!W || !H) return fail(c, NMD_EINVAL, "W and H must be non-NULL device pointers");
   if (!c->has_S) return fail(c, NMD_ESTATE, "nmd_set_sparse_csr has not been called");
+  return NMD_OK;
+}
+
+// The sums of the objective kernel (one, or five with `metrics`), reduced on the device in a
+// fixed order and copied to q[].
+int objective_sums(nmd_ctx* c, const float* W, const float* H, hipStream_t st, bool metrics,
+                   double* q) {
+  int rc;
+  if ((rc = ensure_device(c))) return rc;
+  if ((rc = load_factors(c, W, H, st))) return rc;
+  const Side& sd = c->ws;
+  const int64_t rw = nmd::dense_rows_per_wg(c->rp);
+  const int64_t units = ((c->m + rw - 1) / rw) * sd.nblk();
+  int64_t min_len = c->n;
+  for (int32_t b = 0; b < sd.nblk(); ++b) min_len = std::min(min_len, sd.bounds[b + 1] - sd.bounds[b]);
+  int nsub = (int)std::min<int64_t>(kObjSubMax, std::max<int64_t>(1, (kTargetWgs + units - 1) / units));
+  nsub = (int)std::max<int64_t>(1, std::min<int64_t>(nsub, min_len / 16));
+  int64_t npart = 0;
+  HIP_TRY(c, nmd::launch_objective(c->A, c->m, c->B, sd.d_bounds, sd.nblk(), nsub, sd.d_rowptr,
+                                   sd.d_idx, sd.d_val, c->rp, metrics, c->objpart, &npart, st));
+  const int nq = metrics ? 5 : 1;
+  if (nq * npart > c->objpart_count) return fail(c, NMD_EDEVICE, "internal: objective buffer");
+  for (int k = 0; k < nq; ++k)
+    HIP_TRY(c, nmd::launch_sum(c->objpart + (int64_t)k * npart, npart, c->objout + k, st));
+  HIP_TRY(c, hipMemcpyAsync(c->h_obj, c->objout, nq * sizeof(double), hipMemcpyDeviceToHost, st));
+  HIP_TRY(c, hipStreamSynchronize(st));
+  for (int k = 0; k < 5; ++k) q[k] = k < nq ? c->h_obj[k] : 0.0;
   return NMD_OK;
 }
 
@@ -841,26 +868,22 @@ int nmd_objective(nmd_ctx* c, const float* W, const float* H, double* out_obj, v
   int rc = check_ready(c, W, H);
   if (rc) return rc;
   if (!out_obj) return fail(c, NMD_EINVAL, "out_obj must be non-NULL");
-  hipStream_t st = (hipStream_t)hip_stream;
-  if ((rc = ensure_device(c))) return rc;
-  if ((rc = load_factors(c, W, H, st))) return rc;
-  const Side& sd = c->ws;
-  const int64_t rw = nmd::dense_rows_per_wg(c->rp);
-  const int64_t units = ((c->m + rw - 1) / rw) * sd.nblk();
-  int64_t min_len = c->n;
-  for (int32_t b = 0; b < sd.nblk(); ++b) min_len = std::min(min_len, sd.bounds[b + 1] - sd.bounds[b]);
-  int nsub = (int)std::min<int64_t>(kObjSubMax, std::max<int64_t>(1, (kTargetWgs + units - 1) / units));
-  nsub = (int)std::max<int64_t>(1, std::min<int64_t>(nsub, min_len / 16));
-  int64_t npart = 0;
-  HIP_TRY(c, nmd::launch_objective(c->A, c->m, c->B, sd.d_bounds, sd.nblk(), nsub, sd.d_rowptr,
-                                   sd.d_idx, sd.d_val, c->rp, c->objpart, &npart, st));
-  if (npart + 1 > c->objpart_count) return fail(c, NMD_EDEVICE, "internal: objective buffer");
-  HIP_TRY(c, nmd::launch_sum(c->objpart, npart, c->objout, st));
-  HIP_TRY(c, hipMemcpyAsync(c->h_obj, c->objout, sizeof(double), hipMemcpyDeviceToHost, st));
-  HIP_TRY(c, hipStreamSynchronize(st));
-  double tot = c->h_obj[0];
-  if (tot < 0.0) tot = 0.0;
-  *out_obj = std::sqrt(tot) / c->s_norm;
+  double q[5];
+  if ((rc = objective_sums(c, W, H, (hipStream_t)hip_stream, false, q))) return rc;
+  *out_obj = std::sqrt(std::max(q[0], 0.0)) / c->s_norm;
+  return NMD_OK;
+}
+
+int nmd_metrics(nmd_ctx* c, const float* W, const float* H, double* out, void* hip_stream) {
+  int rc = check_ready(c, W, H);
+  if (rc) return rc;
+  if (!out) return fail(c, NMD_EINVAL, "out must be non-NULL");
+  double q[5];
+  if ((rc = objective_sums(c, W, H, (hipStream_t)hip_stream, true, q))) return rc;
+  const double s2 = c->s_norm;
+  out[0] = std::sqrt(std::max(q[0] + q[1], 0.0)) / s2;
+  out[1] = std::sqrt(std::max(q[0] + q[2], 0.0)) / s2;
+  out[2] = q[4] > 0.0 ? 1.0 - q[3] / q[4] : 1.0;
   return NMD_OK;
 }
 

@@ -77,11 +77,13 @@ hipError_t launch_transpose_out(const float* B, int rp, int64_t n, float* H, int
 hipError_t launch_zero(float* p, int64_t count, hipStream_t st);
 
 // Objective: per-workgroup fp64 sums of the eq. SLloss terms over (row tile, column block,
-// sub-split); rowptr holds, per column block, the row pointers of the W-side entries.
+// sub-split); rowptr holds, per column block, the row pointers of the W-side entries.  With
+// `metrics`, five sums (objective and reconstruction measures) laid out as
+// partial[k * npartial + workgroup], k = 0..4; otherwise one.
 hipError_t launch_objective(const float* X, int64_t rows, const float* P, const int64_t* cbounds,
                             int nblk, int nsub, const int64_t* rowptr, const int32_t* idx,
-                            const float* val, int rp, double* partial, int64_t* npartial,
-                            hipStream_t st);
+                            const float* val, int rp, bool metrics, double* partial,
+                            int64_t* npartial, hipStream_t st);
 hipError_t launch_sum(const double* partial, int64_t count, double* out, hipStream_t st);
 
 int dense_max_wgs(int64_t rows, int rp, int nsplit);

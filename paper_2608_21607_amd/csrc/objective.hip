@@ -1,5 +1,11 @@
 // Objective of eq. auxCost with Z eliminated (eq. SLloss):
-//   f^2 ||S||_F^2 = sum_{S_ij = 0} max(0, L_ij)^2 + sum_{S_ij > 0} (S_ij - L_ij)^2,  L = X P^T.
+//   f^2 ||S||_F^2 = sum_{S_ij = 0} max(0, L_ij)^2 + sum_{S_ij > 0} (S_ij - L_ij)^2,  L = X P^T,
+// and, in the metrics variant, the reconstruction measures of S-hat = max(0, L) (eq. rectify):
+//   RMSE (eq. RMSE)  E^2 ||S||_F^2 = sum_{S_ij = 0} S-hat_ij^2 + sum_{S_ij > 0} (S_ij - S-hat_ij)^2,
+//   WJD  (eq. WJD)   J = 1 - sum min(S, S-hat) / sum max(S, S-hat).
+// Off the nonzeros the three share max(0, L)^2 and max(0, L), so the kernel keeps five sums:
+// q0 = sum_{S=0} max(0, L)^2, q1 = sum_{S>0} (S - L)^2, q2 = sum_{S>0} (S - S-hat)^2,
+// q3 = sum_{S>0} min(S, S-hat), q4 = sum_{S=0} max(0, L) + sum_{S>0} max(S, S-hat).
 //
 // Every entry of L is formed once, on MFMA, exactly as in the fused contraction (same tiles,
 // same transposed layout).  Each lane owns one row i and four columns 4q..4q+3 of every
@@ -15,7 +21,9 @@
 
 namespace nmd {
 
-template <int RP>
+// Per workgroup: partial[k * gridDim.x + workgroup] = its share of sum k (k = 0 only, or 0..4
+// in the metrics variant).
+template <int RP, bool METRICS>
 __global__ __launch_bounds__(256) void objective_kernel(
     const float* __restrict__ X, int64_t rows, const float* __restrict__ P,
     const int64_t* __restrict__ cbounds, int nsub, const int64_t* __restrict__ rowptr,
@@ -23,6 +31,7 @@ __global__ __launch_bounds__(256) void objective_kernel(
     double* __restrict__ partial) {
   constexpr int MI = DenseCfg<RP>::MI;
   constexpr int NT = DenseCfg<RP>::NT;
+  constexpr int NQ = METRICS ? 5 : 1;
   __shared__ __attribute__((aligned(16))) float tile[NT * (RP + 4)];
   __shared__ double red[256];
 
@@ -63,7 +72,8 @@ __global__ __launch_bounds__(256) void objective_kernel(
     }
   }
 
-  double acc = 0.0;
+  double acc = 0.0;                            // q0, or f^2 ||S||^2 when !METRICS
+  double qs = 0.0, qr = 0.0, qmin = 0.0, qmax = 0.0;  // q1 .. q4
   PanelTile<RP, NT> pt;
   if (jb0 < jb1) pt.fetch(P, jb0, jb1, tid);
   for (int64_t j0 = jb0; j0 < jb1; j0 += NT) {
@@ -101,48 +111,69 @@ __global__ __launch_bounds__(256) void objective_kernel(
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const float l = lt[mi][u];
+          const double p = (double)fmaxf(l, 0.f);
           if (hit[u]) {
-            const double d = (double)sv[u] - (double)l;
-            acc += d * d;
+            const double sd = (double)sv[u];
+            const double d = sd - (double)l;
+            if constexpr (METRICS) {
+              const double e = sd - p;
+              qs += d * d;
+              qr += e * e;
+              qmin += fmin(sd, p);
+              qmax += fmax(sd, p);
+            } else {
+              acc += d * d;
+            }
           } else {
-            const double p = (double)fmaxf(l, 0.f);
             acc += p * p;
+            if constexpr (METRICS) qmax += p;
           }
         }
       }
     }
   }
 
-  red[tid] = acc;
-  __syncthreads();
-  for (int k = 128; k > 0; k >>= 1) {
-    if (tid < k) red[tid] += red[tid + k];
+  const double mine[5] = {acc, qs, qr, qmin, qmax};
+#pragma unroll
+  for (int k = 0; k < NQ; ++k) {
+    red[tid] = mine[k];
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+      if (tid < h) red[tid] += red[tid + h];
+      __syncthreads();
+    }
+    if (tid == 0) partial[(int64_t)k * gridDim.x + logical] = red[0];
     __syncthreads();
   }
-  if (tid == 0) partial[logical] = red[0];
 }
 
 template <int RP>
 static hipError_t launch_objective_t(const float* X, int64_t rows, const float* P,
                                      const int64_t* cbounds, int nblk, int nsub,
                                      const int64_t* rowptr, const int32_t* idx, const float* val,
-                                     double* partial, int64_t* npartial, hipStream_t st) {
+                                     bool metrics, double* partial, int64_t* npartial,
+                                     hipStream_t st) {
   const int64_t row_tiles = (rows + rows_per_wg<RP>() - 1) / rows_per_wg<RP>();
   const int64_t total = row_tiles * nblk * nsub;
   *npartial = total;
   if (total <= 0) return hipSuccess;
   if (total > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((objective_kernel<RP>), dim3((unsigned)total), dim3(256), 0, st, X, rows, P,
-                     cbounds, nsub, rowptr, idx, val, row_tiles, partial);
+  if (metrics)
+    hipLaunchKernelGGL((objective_kernel<RP, true>), dim3((unsigned)total), dim3(256), 0, st, X,
+                       rows, P, cbounds, nsub, rowptr, idx, val, row_tiles, partial);
+  else
+    hipLaunchKernelGGL((objective_kernel<RP, false>), dim3((unsigned)total), dim3(256), 0, st, X,
+                       rows, P, cbounds, nsub, rowptr, idx, val, row_tiles, partial);
   return hipGetLastError();
 }
 
 hipError_t launch_objective(const float* X, int64_t rows, const float* P, const int64_t* cbounds,
                             int nblk, int nsub, const int64_t* rowptr, const int32_t* idx,
-                            const float* val, int rp, double* partial, int64_t* npartial,
-                            hipStream_t st) {
-#define CALL(R) \
-  launch_objective_t<R>(X, rows, P, cbounds, nblk, nsub, rowptr, idx, val, partial, npartial, st)
+                            const float* val, int rp, bool metrics, double* partial,
+                            int64_t* npartial, hipStream_t st) {
+#define CALL(R)                                                                                \
+  launch_objective_t<R>(X, rows, P, cbounds, nblk, nsub, rowptr, idx, val, metrics, partial, \
+                        npartial, st)
   NMD_RP_DISPATCH(rp, CALL)
 #undef CALL
 }

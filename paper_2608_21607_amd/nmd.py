@@ -56,6 +56,7 @@ def lib() -> C.CDLL:
         "nmd_set_sparse_csr": (I32, [P, I64, P, P, P]),
         "nmd_als_block_sweep": (I32, [P, P, P, I32, P]),
         "nmd_objective": (I32, [P, P, P, C.POINTER(C.c_double), P]),
+        "nmd_metrics": (I32, [P, P, P, P, P]),
         "nmd_destroy": (None, [P]),
         "nmd_last_error": (C.c_char_p, [P]),
         "nmd_get_schedule": (I32, [P, I64, P, I64]),
@@ -167,6 +168,14 @@ class Context:
                                    _dev_ptr(H, (self.r, self.n), "H"), C.byref(out),
                                    _stream_handle(stream)), self._p)
         return out.value
+
+    def metrics(self, W, H, stream=None) -> dict:
+        """Objective, RMSE and weighted Jaccard distance of S-hat = max(0, W H), one pass."""
+        out = (C.c_double * 3)()
+        _check(lib().nmd_metrics(self._p, _dev_ptr(W, (self.m, self.r), "W"),
+                                 _dev_ptr(H, (self.r, self.n), "H"), out,
+                                 _stream_handle(stream)), self._p)
+        return {"objective": out[0], "rmse": out[1], "wjd": out[2]}
 
     def schedule(self, t):
         cap = 1 << 20

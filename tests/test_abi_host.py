@@ -107,7 +107,12 @@ def test_no_positive_entry_and_state_errors(L):
     assert L.nmd_als_block_sweep(ctx._p, None, fake, 1, None) == nmd.EINVAL
     out = C.c_double()
     assert L.nmd_objective(ctx._p, fake, fake, C.byref(out), None) == nmd.ESTATE
+    out3 = (C.c_double * 3)()
+    assert L.nmd_metrics(ctx._p, fake, fake, out3, None) == nmd.ESTATE
+    assert L.nmd_metrics(None, fake, fake, out3, None) == nmd.EINVAL
     ctx.set_sparse_csr(*_csr_case())
+    assert L.nmd_metrics(ctx._p, fake, fake, None, None) == nmd.EINVAL
+    assert L.nmd_metrics(ctx._p, None, fake, out3, None) == nmd.EINVAL
     assert L.nmd_als_block_sweep(ctx._p, fake, fake, 0, None) == nmd.EINVAL
     steps = (C.c_int32 * 1)(3)
     assert L.nmd_run_steps(ctx._p, fake, fake, steps, 1, None) == nmd.EINVAL

@@ -265,6 +265,52 @@ def test_odd_shapes(case):
     assert abs(f - salsa.objective(S, Wg, Hg)) <= TOL * f
 
 
+# ---------------------------------------------------------- objective and reconstruction metrics
+def test_metrics_calibration_and_fit():
+    """eqs. RMSE and WJD: at the sign-constrained start S-hat = 0, so both equal 1 (their
+    calibration); after three deterministic sweeps all three measures match the oracle
+    at the same factors, and the objective bounds the RMSE from above (Prop. 9)."""
+    p = gen.config(1)
+    _say("metrics, config 1")
+    ctx = make_ctx(p)
+    S = salsa.csr_matrix(p.m, p.n, p.row_ptr, p.col, p.val)
+    m0 = ctx.metrics(dev(p.W0), dev(p.H0))
+    # ||S||_F summed on the device over the host's ||S||_F: equal up to fp64 summation order
+    assert abs(m0["rmse"] - 1.0) <= 1e-12 and m0["wjd"] == 1.0
+    assert abs(m0["objective"] - ctx.objective(dev(p.W0), dev(p.H0))) <= 1e-12
+    W, H = dev(p.W0), dev(p.H0)
+    ctx.sweep(W, H, 3)
+    Wg, Hg = W.cpu().numpy(), H.cpu().numpy()
+    m3 = ctx.metrics(W, H)
+    assert abs(m3["objective"] - salsa.objective(S, Wg, Hg)) <= TOL * m3["objective"]
+    assert abs(m3["rmse"] - salsa.rmse(S, Wg, Hg)) <= TOL * m3["rmse"]
+    assert abs(m3["wjd"] - salsa.wjd(S, Wg, Hg)) <= TOL * m3["wjd"]
+    assert m3["objective"] >= m3["rmse"] and m3["rmse"] < 1.0 and m3["wjd"] < 1.0
+    assert abs(m3["objective"] - ctx.objective(W, H)) <= 1e-12 * m3["objective"]
+
+
+@pytest.mark.parametrize("case", [(300, 410, 64), (333, 290, 100), (700, 600, 256), (600, 900, 512)],
+                         ids=lambda c: f"{c[0]}x{c[1]}r{c[2]}")
+def test_metrics_random_factors(case):
+    """All three measures at random Gaussian factors (S-hat about half positive), every padded
+    rank path of the objective kernel, against the oracle."""
+    m, n, r = case
+    _say("metrics, random factors", case)
+    row_ptr, col, val = gen.random_sparse(m, n, 0.05, m + n + r, heavy_row_frac=0.3)
+    g = np.random.default_rng(r)
+    W0 = (g.standard_normal((m, r)) / math.sqrt(r)).astype(np.float32)
+    H0 = g.standard_normal((r, n)).astype(np.float32)
+    p = gen.Problem("metrics", m, n, r, row_ptr, col, val, W0, H0, 128, 128, "deterministic",
+                    1.0, 0.0, 7)
+    ctx = make_ctx(p)
+    S = salsa.csr_matrix(m, n, row_ptr, col, val)
+    got = ctx.metrics(dev(W0), dev(H0))
+    assert abs(got["objective"] - salsa.objective(S, W0, H0)) <= TOL * got["objective"]
+    assert abs(got["rmse"] - salsa.rmse(S, W0, H0)) <= TOL * got["rmse"]
+    assert abs(got["wjd"] - salsa.wjd(S, W0, H0)) <= TOL * got["wjd"]
+    assert got["objective"] >= got["rmse"]
+
+
 def test_bitwise_determinism():
     p = gen.config(3, scale=0.0625)
     p.block_m = p.block_n = 256
