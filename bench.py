@@ -62,11 +62,12 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(p, frac=8):
+def cpu_baseline(p, frac=1):
     """fp64 oracle on the host over a bounded sample of the workload: the first W-step and the
-    first H-step of sweep 0 at full size, each evaluated for every `frac`-th row of the factor
-    it updates (the Gram solve and the block slicing still run in full).  Scaled to one sweep
-    of C W-steps and R H-steps: sweep time = frac * (C t_W + R t_H)."""
+    first H-step of sweep 0 at full size (about 15 s on 16 threads for the graph workload),
+    each evaluated for every `frac`-th row of the factor it updates (the Gram solve and the
+    block slicing run in full).  Scaled to one sweep of C W-steps and R H-steps: sweep time =
+    frac * (C t_W + R t_H)."""
     import numpy as np
     from oracle import partition, salsa, schedule
 
@@ -98,8 +99,9 @@ def cpu_baseline(p, frac=8):
         "cores": int(threads),
         "kind": "oracle",
         "sample": (f"fp64 oracle at full size: first W-step ({t1 - t0:.1f} s) and first "
-                   f"H-step ({t2 - t1:.1f} s) of sweep 0 on every {frac}th row; sweep time = "
-                   f"{frac} x ({C} W-steps + {R} H-steps)"),
+                   f"H-step ({t2 - t1:.1f} s) of sweep 0, "
+                   + ("all rows" if frac == 1 else f"every {frac}th row")
+                   + f"; sweep time = {frac} x ({C} W-steps + {R} H-steps)"),
     }
 
 
