@@ -215,6 +215,50 @@ def test_hypercube_completion():
     assert salsa.objective(sp.csr_matrix(S), a, b.T) < 1e-10
 
 
+# ----------------------------------------------------------- P8: block-diagonal matrices
+@pytest.mark.parametrize("k,m,n,density", [(3, 3, 4, 1.0), (5, 4, 6, 0.6), (8, 3, 5, 0.8)])
+def test_block_diagonal_completion(k, m, n, density):
+    """Lemma 1 (eq. blocks, eq. hadamard): for k equal m x n nonnegative blocks S_b, the matrix
+    L = (1_k kron [S_1 ... S_k]) hadamard (Omega kron 1_m 1_n^T), with Omega the completion of
+    I_k (eq. Omega), satisfies max(0, L) = S and has rank <= 3m, independent of k.  Rank-3m
+    factors W[(a,i),(p,q)] = [i = p] w_a[q], H[(p,q),(b,j)] = S_b[p,j] h_b[q] reproduce L, give
+    objective 0, and are a fixed point of the deterministic sweep.  (The printed all-ones
+    factor 1_m must be 1_k for the sizes km x kn to agree.)"""
+    rng = np.random.default_rng(k * 100 + m * 10 + n)
+    blocks = [np.where(rng.random((m, n)) < density, rng.uniform(0.2, 2.0, (m, n)), 0.0)
+              for _ in range(k)]
+    for Sb in blocks:  # every row and column of a block keeps a positive entry
+        Sb[np.arange(m), np.arange(m) % n] = rng.uniform(0.5, 1.5, m)
+        Sb[np.arange(n) % m, np.arange(n)] = rng.uniform(0.5, 1.5, n)
+    S = np.zeros((k * m, k * n))
+    for b, Sb in enumerate(blocks):
+        S[b * m:(b + 1) * m, b * n:(b + 1) * n] = Sb
+    # eq. Omega for I_k
+    c = math.cos(2 * math.pi / k)
+    th = 2 * math.pi * np.arange(k) / k
+    Wo = np.stack([np.cos(th), np.sin(th), np.ones(k)], axis=1)
+    Ho = np.stack([np.cos(th), np.sin(th), -c * np.ones(k)], axis=0) / (1 - c)
+    Omega = Wo @ Ho
+    L = np.kron(np.ones((k, 1)), np.hstack(blocks)) * np.kron(Omega, np.ones((m, n)))
+    np.testing.assert_allclose(np.maximum(0.0, L), S, atol=1e-12)
+    sv = np.linalg.svd(L, compute_uv=False)
+    assert np.sum(sv > 1e-10 * sv[0]) <= 3 * m
+    W = np.zeros((k * m, 3 * m))
+    H = np.zeros((3 * m, k * n))
+    for a in range(k):
+        for i in range(m):
+            W[a * m + i, i * 3:(i + 1) * 3] = Wo[a]
+    for b, Sb in enumerate(blocks):
+        for pidx in range(m):
+            for q in range(3):
+                H[pidx * 3 + q, b * n:(b + 1) * n] = Sb[pidx] * Ho[q, b]
+    np.testing.assert_allclose(W @ H, L, atol=1e-12)
+    Ssp = sp.csr_matrix(S)
+    assert salsa.objective(Ssp, W, H) < 1e-9
+    st = _exact_state_sweep(Ssp, W, H, block=(k * m, k * n))
+    assert np.linalg.norm(st.W @ st.H - L) / np.linalg.norm(L) < 1e-9
+
+
 # --------------------------------------------------------------- P9 / P10: the objective
 def test_objective_routes_agree_and_bound_rmse():
     """eq. SLloss (Z eliminated) equals eq. auxCost evaluated with the optimal Z, and by
