@@ -33,7 +33,8 @@ METRIC = "ALS sweeps/sec and dense-equiv TFLOP/s (4mnr/sweep), % of fp32 MFMA pe
 # WRITE_SIZE) scaled by the same counters on a plain copy of known size; valid only for the
 # kernel sources it was taken on.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dense_r256_graph139255_traffic.json")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f) for f in ("tile.h", "dense.hip")]
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f)
+                  for f in ("tile.h", "dense_kernel.h", "dense.hip")]
 
 
 def kernel_source_hash():

@@ -18,7 +18,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnmd.so")
-SOURCES = ["host.cpp", "dense.hip", "objective.hip", "sparse.hip", "solve.hip", "layout.hip"]
+SOURCES = ["host.cpp", "dense.hip", "dense_large.hip", "objective.hip", "sparse.hip", "solve.hip",
+           "layout.hip"]
 ARCH = "gfx950"
 
 # Packed-fp32 instructions are kept out of the generated code on purpose.
@@ -30,10 +31,12 @@ HIPFLAGS = [
 ]
 
 
-# Per-source additions.  The dense kernel keeps its MFMA accumulators in ordinary VGPRs: with
-# accumulation registers the compiler copies the output tiles between the two register files
-# on every panel block at small ranks (measured: r = 16 at 53% of the fp32 MFMA peak instead of
-# 72%), and the large ranks are unaffected.
+# Per-source additions.  The dense kernel for r_p <= 256 keeps its MFMA accumulators in ordinary
+# VGPRs: with accumulation registers the compiler copies the output tiles between the two
+# register files on every panel block at small ranks (measured: r = 16 at 53% of the fp32 MFMA
+# peak instead of 72%).  The r_p >= 320 instantiations (dense_large.hip) keep the default: at
+# one wave per SIMD the output tiles sit in accumulation registers and leave the VGPRs to the
+# operands (r = 512: 3-4% faster).
 EXTRA_FLAGS = {"dense.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 

@@ -1,0 +1,249 @@
+// Fused dense contraction Y = sgn * max(0, X P^T) P on gfx950 fp32 MFMA (kernel templates; the
+// instantiations live in dense.hip for r_p <= 256 and in dense_large.hip for larger ranks, which
+// are compiled with different register-allocation flags).
+//
+// With L = X P_J^T and S-hat = max(0, L) (eq. rectify), the difference matrix of eq. updateD
+// gives Delta_{:J} P_J = sum over the nonzeros of S of (S - min(0, L)) p_j  -  S-hat P_J, and
+// the least-squares update is X <- X + Delta_{:J} P_J (P_J^T P_J)^-1 (eqs. spLsqA, lsqA_sto).
+// This kernel forms the dense term -S-hat P_J (sgn = -1); the sparse correction adds the first
+// term.  S-hat is mostly zero (the factors start with opposite signs and the fit keeps it sparse,
+// Sec. 4.3), so a wave skips the MFMAs of every 16 x 4 operand slice of S-hat that holds no
+// positive entry.  The L tile is produced by MFMA, rectified in registers and
+// consumed by MFMA; neither L nor S-hat reaches memory (the IO-aware fusion of Sec. 4.2, with
+// the raw panel P instead of a pseudo-inverse).
+//
+// Data flow (one workgroup = 4 waves, one per SIMD):
+//   * X: rows x RP row-major (RP = padded rank, zero columns beyond r).  Each wave keeps
+//     16*MI rows of X resident in VGPRs as MFMA operands for the whole launch.
+//   * P rows of the split's range stream through LDS (row stride RP + 4 floats, which keeps
+//     both read patterns free of bank conflicts); the next tile is in flight while the current
+//     one is consumed.
+//   * GEMM1 builds the transposed tile L^T (16 j x 16 i); the accumulator of lane l, register
+//     v holds L[i = l%16][j = 4(l/16) + v], which is exactly the srcA layout of GEMM2 for the
+//     k-slice {4(l/16) + v}: the rectified tile feeds GEMM2 with no data movement.
+//   * GEMM2: Y[i][c] += sum_j max(0, L[i][j]) P[j][c], srcB read from LDS as single floats.
+//   * Split-J: the workgroups of one row tile may be spread over `nsplit` disjoint ranges of P
+//     rows, each writing its own partial Y; the solve kernel sums them in fp64.
+
+#pragma once
+
+#include "tile.h"
+
+namespace nmd {
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void glb_void;
+
+// Launch shape per padded rank.  MI: 16-row blocks of X per wave; WAVES: waves per workgroup
+// (8 puts two waves on each SIMD, so that one wave's MFMAs cover the other's LDS waits,
+// accumulator read-outs and branches); NT: panel rows per LDS tile; RING: slices of the second
+// product whose operands are read during the first (4: all of them, where registers allow);
+// DIRECT: direct global->LDS loads into double-buffered tiles (for long rows; register staging
+// there pushes the VGPR budget into spills) instead of register staging through one tile (a
+// direct load moves 64 chunks of one row, so short rows would leave most lanes idle).
+template <int RP>
+struct DenseLaunch {
+  static constexpr int MI = DenseCfg<RP>::MI;
+  static constexpr int WAVES = 4;
+  static constexpr bool DIRECT = RP >= 320;
+  static constexpr int NT = DIRECT ? DenseCfg<RP>::NTD : DenseCfg<RP>::NT;
+  static constexpr int RING = RP >= 320 ? 4 : 2;
+};
+template <>
+struct DenseLaunch<256> {
+  static constexpr int MI = 1;
+  static constexpr int WAVES = 8;
+  static constexpr bool DIRECT = true;
+  static constexpr int NT = 64;
+  static constexpr int RING = 4;
+};
+template <>
+struct DenseLaunch<128> {
+  static constexpr int MI = 2;
+  static constexpr int WAVES = 8;
+  static constexpr bool DIRECT = true;
+  static constexpr int NT = 128;
+  static constexpr int RING = 4;
+};
+
+template <int RP>
+constexpr int dense_rows() { return 16 * DenseLaunch<RP>::MI * DenseLaunch<RP>::WAVES; }
+
+// Direct staging of panel rows j0 .. j0+NT-1 from global memory straight into a padded LDS
+// tile; wave w fills rows w, w + WAVES, ...; a direct load writes 64 consecutive 16-byte chunks
+// (lane l -> chunk l), so each instruction covers up to 64 chunks of one row.  Rows past the
+// split end are zero-filled with ordinary LDS stores (their L is then zero).
+template <int RP>
+__device__ __forceinline__ void issue_tile(float* dst, const float* __restrict__ P, int64_t j0,
+                                           int64_t jb1, int wave, int lane) {
+  constexpr int WAVES = DenseLaunch<RP>::WAVES;
+  constexpr int NT = DenseLaunch<RP>::NT;
+  constexpr int LS = RP + 4;
+  constexpr int CPR = RP / 4;
+  constexpr int IPR = (CPR + 63) / 64;
+#pragma unroll
+  for (int rr = 0; rr < NT / WAVES; ++rr) {
+    const int r = wave + WAVES * rr;
+    const int64_t jr = j0 + r;
+    if (jr < jb1) {
+      const float* src = P + jr * RP;
+#pragma unroll
+      for (int k = 0; k < IPR; ++k) {
+        const int c = 64 * k + lane;
+        if (CPR % 64 == 0 || c < CPR)
+          __builtin_amdgcn_global_load_lds((glb_void*)(src + 4 * c),
+                                           (lds_void*)(dst + r * LS + 256 * k), 16, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < IPR; ++k) {
+        const int c = 64 * k + lane;
+        if (CPR % 64 == 0 || c < CPR)
+          *reinterpret_cast<float4*>(dst + r * LS + 4 * c) = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  }
+}
+
+// Both products over the panel rows j0 .. min(j0 + NT, jb1) - 1 held in the LDS tile; returns
+// the number of 16 x 4 slices of max(0, L) that ran the second product.
+template <int RP>
+__device__ __forceinline__ unsigned consume_tile(const float* tile, int64_t j0, int64_t jb1,
+                                                 const float (&a)[DenseLaunch<RP>::MI][RP / 4],
+                                                 floatx4 (&y)[DenseLaunch<RP>::MI][RP / 16],
+                                                 int q, int l16) {
+  constexpr int MI = DenseLaunch<RP>::MI;
+  constexpr int NT = DenseLaunch<RP>::NT;
+  constexpr int CB = RP / 16;
+  const int left = (int)((jb1 - j0 + 15) / 16);
+  const int njb = left < NT / 16 ? left : NT / 16;
+  unsigned done = 0;
+  float4 pre[l_lookahead<RP>()];
+  l_prefetch<RP>(pre, tile, 0, q, l16);
+  constexpr int NR = DenseLaunch<RP>::RING;
+  for (int jb = 0; jb < njb; ++jb) {
+    // the block's second-product operands are read inside its first product
+    float ring[NR][CB];
+    floatx4 lt[MI];
+    l_tile<RP, MI, NR>(lt, a, pre, ring, tile, jb, q, l16);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) lt[mi][v] = lt[mi][v] > 0.f ? lt[mi][v] : 0.f;
+    const unsigned live = live_slices<MI>(lt);
+    // the next block's first panel fragments, in flight during this block's second product
+    if (jb + 1 < njb) l_prefetch<RP>(pre, tile, jb + 1, q, l16);
+    done += zb_tile<RP, MI, NR>(y, lt, live, ring, tile, jb, q, l16);
+  }
+  return done;
+}
+
+// One step of the double-buffered direct pipeline: start the loads of the next tile into `nxt`
+// (when not null) and consume the current tile `cur`.  The two are distinct LDS buffers; the
+// restrict qualifiers tell the compiler that the reads of `cur` do not depend on the direct
+// loads into `nxt`, so it need not wait for those loads before the products start.
+template <int RP>
+__device__ __forceinline__ unsigned direct_step(
+    const float* __restrict__ cur, float* __restrict__ nxt, const float* __restrict__ P,
+    int64_t j0, int64_t jb1, const float (&a)[DenseLaunch<RP>::MI][RP / 4],
+    floatx4 (&y)[DenseLaunch<RP>::MI][RP / 16], int wave, int lane, int q, int l16) {
+  if (nxt) issue_tile<RP>(nxt, P, j0 + DenseLaunch<RP>::NT, jb1, wave, lane);
+  return consume_tile<RP>(cur, j0, jb1, a, y, q, l16);
+}
+
+template <int RP>
+__global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
+    const float* __restrict__ X, int64_t rows, const float* __restrict__ P, int64_t blk,
+    float* __restrict__ Ypart, int64_t y_stride, int nsplit, int64_t row_tiles, float sgn,
+    unsigned long long* __restrict__ gemm2_blocks) {
+  constexpr int MI = DenseLaunch<RP>::MI;
+  constexpr int WAVES = DenseLaunch<RP>::WAVES;
+  constexpr int CB = RP / 16;
+  constexpr int LS = RP + 4;  // padded LDS row stride (floats)
+  constexpr bool DIRECT = DenseLaunch<RP>::DIRECT;
+  constexpr int NT = DenseLaunch<RP>::NT;
+  static_assert(NT % 16 == 0 && NT % WAVES == 0, "tile shape");
+  __shared__ __attribute__((aligned(16))) float smem[(DIRECT ? 2 : 1) * NT * LS];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int q = lane >> 4, l16 = lane & 15;
+
+  const int64_t logical = xcd_logical(blockIdx.x, (int64_t)gridDim.x);
+  const int split = (int)(logical / row_tiles);
+  const int64_t rt = logical - (int64_t)split * row_tiles;
+  const int64_t jb0 = (int64_t)split * blk / nsplit;
+  const int64_t jb1 = (int64_t)(split + 1) * blk / nsplit;
+  const int64_t row0 = rt * dense_rows<RP>() + (int64_t)wave * (16 * MI);
+
+  float a[MI][RP / 4];
+  load_x_frags<RP, MI>(a, X, rows, row0, q, l16);
+
+  floatx4 y[MI][CB];
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) y[mi][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  unsigned int done = 0;  // 16 x 4 slices of max(0, L) that ran the second contraction (wave)
+
+  if constexpr (DIRECT) {
+    if (jb0 < jb1) issue_tile<RP>(smem, P, jb0, jb1, wave, lane);
+    int cur = 0;
+    for (int64_t j0 = jb0; j0 < jb1; j0 += NT, cur ^= 1) {
+      __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the tile have landed
+      __syncthreads();                // every wave's have; the other buffer is free again
+      done += direct_step<RP>(smem + cur * (NT * LS), j0 + NT < jb1 ? smem + (cur ^ 1) * (NT * LS) : nullptr,
+                              P, j0, jb1, a, y, wave, lane, q, l16);
+    }
+  } else {
+    // register staging: the next tile's global loads are in flight while this one is consumed
+    // (rows past the split end are stored as zeros)
+    PanelTile<RP, NT, 64 * WAVES> pt;
+    if (jb0 < jb1) pt.fetch(P, jb0, jb1, tid);
+    for (int64_t j0 = jb0; j0 < jb1; j0 += NT) {
+      __syncthreads();  // previous tile fully consumed
+      pt.stash(smem, tid);
+      __syncthreads();
+      if (j0 + NT < jb1) pt.fetch(P, j0 + NT, jb1, tid);
+      done += consume_tile<RP>(smem, j0, jb1, a, y, q, l16);
+    }
+  }
+
+  // Y block (16 x 16): lane l, register v holds Y[row0 + 16 mi + 4q + v][16 cb + l16].
+  float* Y = Ypart + (int64_t)split * y_stride;
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t row = row0 + 16 * mi + 4 * q + v;
+      if (row < rows) {
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) Y[row * RP + 16 * cb + l16] = sgn * y[mi][cb][v];
+      }
+    }
+  if (gemm2_blocks && lane == 0) atomicAdd(gemm2_blocks, (unsigned long long)done);
+}
+
+template <int RP>
+static hipError_t launch_dense_t(const float* X, int64_t rows, const float* P, int64_t blk,
+                                 float* Ypart, int64_t y_stride, int nsplit, float sgn,
+                                 unsigned long long* gemm2_blocks, hipStream_t st) {
+  const int64_t row_tiles = (rows + dense_rows<RP>() - 1) / dense_rows<RP>();
+  const int64_t total = row_tiles * nsplit;
+  if (total <= 0) return hipSuccess;
+  if (total > 0x7fffffffLL) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((dense_kernel<RP>), dim3((unsigned)total),
+                     dim3(64 * DenseLaunch<RP>::WAVES), 0, st, X, rows, P, blk,
+                     Ypart, y_stride, nsplit, row_tiles, sgn, gemm2_blocks);
+  return hipGetLastError();
+}
+
+template <int RP>
+static hipError_t wgs_per_cu_t(int* out) {
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(out, dense_kernel<RP>,
+                                                      64 * DenseLaunch<RP>::WAVES, 0);
+}
+
+}  // namespace nmd

@@ -32,6 +32,11 @@ int dense_rows_per_wg(int rp);
 
 // Workgroups of the dense kernel for padded rank rp that one CU holds at once.
 hipError_t dense_wgs_per_cu(int rp, int* out);
+// The same two for r_p >= 320, whose instantiations are in their own translation unit.
+hipError_t dense_wgs_per_cu_large(int rp, int* out);
+hipError_t launch_dense_large(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
+                              float* Ypart, int64_t y_stride, int nsplit, float sgn,
+                              unsigned long long* gemm2_blocks, hipStream_t st);
 
 // Y_s = sgn * max(0, X P^T) P over the split s of the rows of P (rows of X: `rows`).  Ypart
 // holds nsplit buffers of y_stride floats each (row-major rows x rp).  When gemm2_blocks is not
