@@ -179,11 +179,14 @@ def main():
     sweeps_per_s = args.steps / (ms / 1e3)
     dense_equiv = 4.0 * p.m * p.n * p.r * sweeps_per_s / 1e12
     actual = 8.0 * p.m * p.n * p.r * sweeps_per_s / 1e12
-    # The second product of the dense kernel runs only on the slices where max(0, L) has a
-    # positive entry; its algorithmic flops are the first product's times that fraction.
-    g2_run, g2_total = ctx.dense_blocks()
+    # The second product of the dense kernel runs its own MFMAs only for the 16 x 4 slices of
+    # max(0, L) with several positive entries; slices with a few have their entries packed four
+    # to a gathered slice (2 r useful flops each) and the others are skipped.  Its algorithmic
+    # flops are the first product's times the fraction of slices run whole plus 2 r per
+    # gathered entry.
+    g2_run, g2_total, g2_entries = ctx.dense_blocks()
     g2_frac = g2_run / g2_total if g2_total else 1.0
-    dense_alg_flops = dense["flops"] * (0.5 + 0.5 * g2_frac)
+    dense_alg_flops = dense["flops"] * (0.5 + 0.5 * g2_frac) + 2.0 * p.r * g2_entries
     dense_s = dense["ms"] / 1e3
     dense_tflops = dense_alg_flops / dense_s / 1e12 if dense_s > 0 else 0.0
     dense_equiv_kernel = dense["flops"] / dense_s / 1e12 if dense_s > 0 else 0.0
@@ -232,6 +235,7 @@ def main():
             "avg_launch_ms": dense["ms"] / max(1, dense["launches"]),
             "flops_per_launch": dense_alg_flops / max(1, dense["launches"]),
             "second_product_fraction_run": g2_frac,
+            "second_product_entries_gathered_per_launch": g2_entries / max(1, dense["launches"]),
             "dense_equiv_kernel_tflops": dense_equiv_kernel,
         },
     }

@@ -180,12 +180,17 @@ int nmd_rectified_contraction(const float* A, int64_t rows, const float* B, int6
 
 /*
  * nmd_get_dense_blocks - how much of the second product of the dense contraction the sweeps
- * ran: *run = slices of 16 rows x 4 panel rows where max(0, L) had a positive entry and the
- * product ran, *total = slices examined, both since the context was created or last reset
- * here (the second product's flops are run/total of its dense count).  Synchronises the device.  reset != 0 clears both after
- * reading.  Either output pointer may be NULL.
+ * ran, since the context was created or last reset here.  The second product is organised in
+ * slices of 16 rows x 4 panel rows of max(0, L) (Sec. 4.3: S-hat is sparse): a slice with no
+ * positive entry is skipped, the entries of a slice with only a few are packed four to a
+ * gathered slice (r_p = 256), and the others run their own MFMAs.  *run = slices that ran
+ * whole, *total = slices examined, *entries = positive entries taken through gathered slices
+ * (so the second product's useful work is run/total of its dense count plus 2 r flops per
+ * entry).  Synchronises the device.
+ * reset != 0 clears all three after reading.  Any output pointer may be NULL.
  */
-int nmd_get_dense_blocks(nmd_ctx* ctx, int64_t* run, int64_t* total, int32_t reset);
+int nmd_get_dense_blocks(nmd_ctx* ctx, int64_t* run, int64_t* total, int64_t* entries,
+                         int32_t reset);
 
 /*
  * nmd_get_kernel_timing - with NMD_FLAG_TIMING set, the summed device time (HIP events on the

@@ -8,9 +8,10 @@
 // This kernel forms the dense term -S-hat P_J (sgn = -1); the sparse correction adds the first
 // term.  S-hat is mostly zero (the factors start with opposite signs and the fit keeps it sparse,
 // Sec. 4.3), so a wave skips the MFMAs of every 16 x 4 operand slice of S-hat that holds no
-// positive entry.  The L tile is produced by MFMA, rectified in registers and
-// consumed by MFMA; neither L nor S-hat reaches memory (the IO-aware fusion of Sec. 4.2, with
-// the raw panel P instead of a pseudo-inverse).
+// positive entry, and (at r_p = 256) packs the entries of slices with only a few of them four
+// to a slice (gathered slices, below).  The L tile is produced by MFMA, rectified in registers
+// and consumed by MFMA; neither L nor S-hat reaches memory (the IO-aware fusion of Sec. 4.2,
+// with the raw panel P instead of a pseudo-inverse).
 //
 // Data flow (one workgroup = 4 waves, one per SIMD):
 //   * X: rows x RP row-major (RP = padded rank, zero columns beyond r).  Each wave keeps
@@ -40,7 +41,9 @@ typedef __attribute__((address_space(1))) void glb_void;
 // product whose operands are read during the first (4: all of them, where registers allow);
 // DIRECT: direct global->LDS loads into double-buffered tiles (for long rows; register staging
 // there pushes the VGPR budget into spills) instead of register staging through one tile (a
-// direct load moves 64 chunks of one row, so short rows would leave most lanes idle).
+// direct load moves 64 chunks of one row, so short rows would leave most lanes idle); SPARSE:
+// when nonzero, slices of the second product with at most that many positive entries go
+// through the gathered path below and no operand ring is kept (RING unused).
 template <int RP>
 struct DenseLaunch {
   static constexpr int MI = DenseCfg<RP>::MI;
@@ -48,6 +51,7 @@ struct DenseLaunch {
   static constexpr bool DIRECT = RP >= 320;
   static constexpr int NT = DIRECT ? DenseCfg<RP>::NTD : DenseCfg<RP>::NT;
   static constexpr int RING = RP >= 320 ? 4 : 2;
+  static constexpr int SPARSE = 0;
 };
 template <>
 struct DenseLaunch<256> {
@@ -56,6 +60,7 @@ struct DenseLaunch<256> {
   static constexpr bool DIRECT = true;
   static constexpr int NT = 64;
   static constexpr int RING = 4;
+  static constexpr int SPARSE = 3;
 };
 template <>
 struct DenseLaunch<128> {
@@ -64,6 +69,7 @@ struct DenseLaunch<128> {
   static constexpr bool DIRECT = true;
   static constexpr int NT = 128;
   static constexpr int RING = 4;
+  static constexpr int SPARSE = 0;
 };
 
 template <int RP>
@@ -107,33 +113,110 @@ __device__ __forceinline__ void issue_tile(float* dst, const float* __restrict__
 
 // Both products over the panel rows j0 .. min(j0 + NT, jb1) - 1 held in the LDS tile; returns
 // the number of 16 x 4 slices of max(0, L) that ran the second product.
+// Thin slices of the second product.  A 16 x 4 slice (v) of z = max(0, L) with at most
+// SPARSE positive entries does not run its own MFMAs: its entries (row i in the block, panel
+// row j in the tile, value z) are appended to a short per-wave list in LDS, and every four
+// listed entries, whatever their rows and columns, make one gathered srcA slice: lane group k
+// holds entry k, A[i][k] = z_k where i = i_k and 0 elsewhere, with srcB row k = P[j_k].  So
+// the matrix cores spend one slice per four positive entries instead of one per live slice.
+// The list is a ring of ELIST entries (packed i | j << 4, z); a wave appends with one store
+// per slice (ballot prefix counts give the slots) and drains four at a time.
+constexpr int ELIST = 32;
+
+// Appends the positive entries of slice v of j-block jb (bits = ballot of z > 0) at
+// tail .. tail + popcount(bits) - 1.
+__device__ __forceinline__ void elist_push(uint2* el, unsigned tail, unsigned long long bits,
+                                           float z, int jb, int v, int q, int l16) {
+  if (z > 0.f) {
+    const unsigned below = __builtin_amdgcn_mbcnt_hi((unsigned)(bits >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((unsigned)bits, 0u));
+    el[(tail + below) % ELIST] =
+        make_uint2((unsigned)l16 | (unsigned)((16 * jb + 4 * q + v) << 4), __float_as_uint(z));
+  }
+}
+
+// One gathered slice from the `cnt` (1..4) list entries at head .. head + cnt - 1.
+template <int RP>
+__device__ __forceinline__ void elist_slice(floatx4 (&y)[RP / 16], const uint2* el, unsigned head,
+                                            int cnt, const float* tile, int q, int l16) {
+  constexpr int CB = RP / 16;
+  const uint2 e = el[(head + q) % ELIST];
+  const bool valid = q < cnt;
+  const int row = valid ? (int)(e.x >> 4) : 0;
+  const float a = valid && l16 == (int)(e.x & 15u) ? __uint_as_float(e.y) : 0.f;
+  const float* prow = &tile[row * (RP + 4) + l16];
+  float bb[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) bb[cb] = prow[16 * cb];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb)
+    y[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb[cb], y[cb], 0, 0, 0);
+}
+
 template <int RP>
 __device__ __forceinline__ unsigned consume_tile(const float* tile, int64_t j0, int64_t jb1,
                                                  const float (&a)[DenseLaunch<RP>::MI][RP / 4],
                                                  floatx4 (&y)[DenseLaunch<RP>::MI][RP / 16],
-                                                 int q, int l16) {
+                                                 int q, int l16, unsigned& entries, uint2* el) {
   constexpr int MI = DenseLaunch<RP>::MI;
   constexpr int NT = DenseLaunch<RP>::NT;
   constexpr int CB = RP / 16;
+  constexpr int SPARSE = DenseLaunch<RP>::SPARSE;
   const int left = (int)((jb1 - j0 + 15) / 16);
   const int njb = left < NT / 16 ? left : NT / 16;
   unsigned done = 0;
   float4 pre[l_lookahead<RP>()];
   l_prefetch<RP>(pre, tile, 0, q, l16);
-  constexpr int NR = DenseLaunch<RP>::RING;
-  for (int jb = 0; jb < njb; ++jb) {
-    // the block's second-product operands are read inside its first product
-    float ring[NR][CB];
-    floatx4 lt[MI];
-    l_tile<RP, MI, NR>(lt, a, pre, ring, tile, jb, q, l16);
+  if constexpr (SPARSE > 0) {
+    static_assert(MI == 1, "gathered second product: one 16-row block per wave");
+    // at most 3 entries are left after a block, and a block adds at most 4 * SPARSE
+    static_assert(3 + 4 * SPARSE <= ELIST, "entry list length");
+    unsigned head = 0, tail = 0;  // wave-uniform list positions
+    for (int jb = 0; jb < njb; ++jb) {
+      float ring[1][CB];
+      floatx4 lt[1];
+      l_tile<RP, 1, 0>(lt, a, pre, ring, tile, jb, q, l16);
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
+      for (int v = 0; v < 4; ++v) lt[0][v] = lt[0][v] > 0.f ? lt[0][v] : 0.f;
+      if (jb + 1 < njb) l_prefetch<RP>(pre, tile, jb + 1, q, l16);
 #pragma unroll
-      for (int v = 0; v < 4; ++v) lt[mi][v] = lt[mi][v] > 0.f ? lt[mi][v] : 0.f;
-    const unsigned live = live_slices<MI>(lt);
-    // the next block's first panel fragments, in flight during this block's second product
-    if (jb + 1 < njb) l_prefetch<RP>(pre, tile, jb + 1, q, l16);
-    done += zb_tile<RP, MI, NR>(y, lt, live, ring, tile, jb, q, l16);
+      for (int v = 0; v < 4; ++v) {
+        const unsigned long long bits = __ballot(lt[0][v] > 0.f);
+        if (!bits) continue;
+        const int cnt = __popcll(bits);
+        if (cnt <= SPARSE) {
+          elist_push(el, tail, bits, lt[0][v], jb, v, q, l16);
+          tail += cnt;
+          entries += cnt;
+        } else {
+          float bb[CB];
+          zb_read<RP>(bb, tile, jb, v, q, l16);
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb)
+            y[0][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(lt[0][v], bb[cb], y[0][cb], 0, 0, 0);
+          ++done;
+        }
+      }
+      for (; tail - head >= 4; head += 4) elist_slice<RP>(y[0], el, head, 4, tile, q, l16);
+    }
+    // the rest refers to this tile's rows: drain it before the buffer is reused
+    if (tail != head) elist_slice<RP>(y[0], el, head, (int)(tail - head), tile, q, l16);
+  } else {
+    constexpr int NR = DenseLaunch<RP>::RING;
+    for (int jb = 0; jb < njb; ++jb) {
+      // the block's second-product operands are read inside its first product
+      float ring[NR][CB];
+      floatx4 lt[MI];
+      l_tile<RP, MI, NR>(lt, a, pre, ring, tile, jb, q, l16);
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) lt[mi][v] = lt[mi][v] > 0.f ? lt[mi][v] : 0.f;
+      const unsigned live = live_slices<MI>(lt);
+      // the next block's first panel fragments, in flight during this block's second product
+      if (jb + 1 < njb) l_prefetch<RP>(pre, tile, jb + 1, q, l16);
+      done += zb_tile<RP, MI, NR>(y, lt, live, ring, tile, jb, q, l16);
+    }
   }
   return done;
 }
@@ -146,9 +229,10 @@ template <int RP>
 __device__ __forceinline__ unsigned direct_step(
     const float* __restrict__ cur, float* __restrict__ nxt, const float* __restrict__ P,
     int64_t j0, int64_t jb1, const float (&a)[DenseLaunch<RP>::MI][RP / 4],
-    floatx4 (&y)[DenseLaunch<RP>::MI][RP / 16], int wave, int lane, int q, int l16) {
+    floatx4 (&y)[DenseLaunch<RP>::MI][RP / 16], int wave, int lane, int q, int l16,
+    unsigned& entries, uint2* el) {
   if (nxt) issue_tile<RP>(nxt, P, j0 + DenseLaunch<RP>::NT, jb1, wave, lane);
-  return consume_tile<RP>(cur, j0, jb1, a, y, q, l16);
+  return consume_tile<RP>(cur, j0, jb1, a, y, q, l16, entries, el);
 }
 
 template <int RP>
@@ -164,11 +248,14 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
   constexpr int NT = DenseLaunch<RP>::NT;
   static_assert(NT % 16 == 0 && NT % WAVES == 0, "tile shape");
   __shared__ __attribute__((aligned(16))) float smem[(DIRECT ? 2 : 1) * NT * LS];
+  // per-wave lists of the gathered second product (unused where SPARSE is 0)
+  __shared__ uint2 elists[DenseLaunch<RP>::SPARSE > 0 ? WAVES * ELIST : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q = lane >> 4, l16 = lane & 15;
+  uint2* el = &elists[DenseLaunch<RP>::SPARSE > 0 ? wave * ELIST : 0];
 
   const int64_t logical = xcd_logical(blockIdx.x, (int64_t)gridDim.x);
   const int split = (int)(logical / row_tiles);
@@ -186,7 +273,8 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) y[mi][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  unsigned int done = 0;  // 16 x 4 slices of max(0, L) that ran the second contraction (wave)
+  unsigned int done = 0;     // 16 x 4 slices of max(0, L) whose second product ran whole
+  unsigned int entries = 0;  // positive entries of max(0, L) taken through gathered slices
 
   if constexpr (DIRECT) {
     if (jb0 < jb1) issue_tile<RP>(smem, P, jb0, jb1, wave, lane);
@@ -195,7 +283,7 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
       __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the tile have landed
       __syncthreads();                // every wave's have; the other buffer is free again
       done += direct_step<RP>(smem + cur * (NT * LS), j0 + NT < jb1 ? smem + (cur ^ 1) * (NT * LS) : nullptr,
-                              P, j0, jb1, a, y, wave, lane, q, l16);
+                              P, j0, jb1, a, y, wave, lane, q, l16, entries, el);
     }
   } else {
     // register staging: the next tile's global loads are in flight while this one is consumed
@@ -207,7 +295,7 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
       pt.stash(smem, tid);
       __syncthreads();
       if (j0 + NT < jb1) pt.fetch(P, j0 + NT, jb1, tid);
-      done += consume_tile<RP>(smem, j0, jb1, a, y, q, l16);
+      done += consume_tile<RP>(smem, j0, jb1, a, y, q, l16, entries, el);
     }
   }
 
@@ -223,7 +311,10 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
         for (int cb = 0; cb < CB; ++cb) Y[row * RP + 16 * cb + l16] = sgn * y[mi][cb][v];
       }
     }
-  if (gemm2_blocks && lane == 0) atomicAdd(gemm2_blocks, (unsigned long long)done);
+  if (gemm2_blocks && lane == 0) {
+    atomicAdd(gemm2_blocks, (unsigned long long)done);
+    if (entries) atomicAdd(gemm2_blocks + 1, (unsigned long long)entries);
+  }
 }
 
 template <int RP>

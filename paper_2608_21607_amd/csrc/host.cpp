@@ -237,7 +237,8 @@ struct nmd_ctx {
   int64_t objpart_count = 0;
   double* objout = nullptr;
   int* status = nullptr;
-  unsigned long long* g2 = nullptr;  // S-hat slices that ran the second contraction
+  unsigned long long* g2 = nullptr;  // [0] S-hat slices whose second product ran whole,
+                                     // [1] S-hat entries taken through gathered slices
   int64_t g2_total = 0;              // slices examined (host count)
   int64_t dense_slots = 0;           // dense workgroups resident at once (CUs x per CU)
   hipStream_t side = nullptr;     // Gram and inverse run here, beside the contraction
@@ -385,7 +386,7 @@ int ensure_device(nmd_ctx* c) {
         dalloc(&c->G, rp * rp) != hipSuccess || dalloc(&c->Gtmp, rp * rp + 64 * 64) != hipSuccess ||
         dalloc(&c->Gpart, (int64_t)c->gram_chunks_max * rp * rp) != hipSuccess ||
         dalloc(&c->objout, 8) != hipSuccess || dalloc(&c->status, 2) != hipSuccess ||
-        dalloc(&c->g2, 1) != hipSuccess) {
+        dalloc(&c->g2, 2) != hipSuccess) {
       free_device(c);
       return fail(c, NMD_ENOMEM, "device allocation of the factor workspaces failed");
     }
@@ -425,7 +426,7 @@ int ensure_device(nmd_ctx* c) {
     }
     HIP_TRY(c, hipMemset(c->status, 0, sizeof(int)));
     HIP_TRY(c, hipMemset(c->status + 1, 0x7f, sizeof(int)));
-    HIP_TRY(c, hipMemset(c->g2, 0, sizeof(unsigned long long)));
+    HIP_TRY(c, hipMemset(c->g2, 0, 2 * sizeof(unsigned long long)));
     HIP_TRY(c, hipDeviceSynchronize());
     c->dev_ready = true;
   } else {
@@ -979,16 +980,18 @@ int nmd_get_kernel_timing(nmd_ctx* c, int32_t kernel, double* total_ms, int64_t*
   return NMD_OK;
 }
 
-int nmd_get_dense_blocks(nmd_ctx* c, int64_t* run, int64_t* total, int32_t reset) {
+int nmd_get_dense_blocks(nmd_ctx* c, int64_t* run, int64_t* total, int64_t* entries,
+                         int32_t reset) {
   if (!c) return NMD_EINVAL;
-  unsigned long long v = 0;
+  unsigned long long v[2] = {0, 0};
   if (c->dev_ready) {
     HIP_TRY(c, hipSetDevice(c->device));
     HIP_TRY(c, hipDeviceSynchronize());
-    HIP_TRY(c, hipMemcpy(&v, c->g2, sizeof v, hipMemcpyDeviceToHost));
+    HIP_TRY(c, hipMemcpy(v, c->g2, sizeof v, hipMemcpyDeviceToHost));
   }
-  if (run) *run = (int64_t)v;
+  if (run) *run = (int64_t)v[0];
   if (total) *total = c->g2_total;
+  if (entries) *entries = (int64_t)v[1];
   if (reset) {
     if (c->dev_ready) {
       HIP_TRY(c, hipMemset(c->g2, 0, sizeof v));

@@ -66,7 +66,7 @@ def lib() -> C.CDLL:
         "nmd_get_sweep_count": (I32, [P, C.POINTER(I64)]),
         "nmd_run_steps": (I32, [P, P, P, P, I32, P]),
         "nmd_rectified_contraction": (I32, [P, I64, P, I64, I32, P, P]),
-        "nmd_get_dense_blocks": (I32, [P, P, P, I32]),
+        "nmd_get_dense_blocks": (I32, [P, P, P, P, I32]),
         "nmd_get_kernel_timing": (I32, [P, I32, C.POINTER(C.c_double), C.POINTER(I64),
                                         C.POINTER(C.c_double), C.POINTER(C.c_double), I32]),
     }
@@ -209,12 +209,13 @@ class Context:
         return {"ms": ms.value, "launches": n.value, "flops": fl.value, "bytes": by.value}
 
     def dense_blocks(self, reset=False):
-        """(run, total): slices (16 rows x 4 panel rows) of the dense contraction's second
-        product that ran, and that were examined, since creation or the last reset."""
-        run, tot = C.c_int64(), C.c_int64()
-        _check(lib().nmd_get_dense_blocks(self._p, C.byref(run), C.byref(tot), int(bool(reset))),
-               self._p)
-        return run.value, tot.value
+        """(run, total, entries): slices (16 rows x 4 panel rows) of the dense contraction's
+        second product that ran whole, slices examined, and positive entries taken through
+        gathered slices, since creation or the last reset."""
+        run, tot, ent = C.c_int64(), C.c_int64(), C.c_int64()
+        _check(lib().nmd_get_dense_blocks(self._p, C.byref(run), C.byref(tot), C.byref(ent),
+                                          int(bool(reset))), self._p)
+        return run.value, tot.value, ent.value
 
 
 def rectified_contraction(A, B, Y=None, stream=None):

@@ -134,8 +134,8 @@ def test_rectified_contraction_argument_checks(L):
 def test_dense_blocks_before_device_use(L):
     """The skip counters of a context that has not touched the GPU read zero."""
     ctx = nmd.Context(40, 30, 4, 16, 16)
-    assert ctx.dense_blocks() == (0, 0)
-    assert L.nmd_get_dense_blocks(None, None, None, 0) == nmd.EINVAL
+    assert ctx.dense_blocks() == (0, 0, 0)
+    assert L.nmd_get_dense_blocks(None, None, None, None, 0) == nmd.EINVAL
     ctx.close()
 
 

@@ -114,6 +114,37 @@ def test_rectified_contraction_skips_zero_blocks(r):
     assert not torch.any(Y0 != 0).item()
 
 
+def _thin_positive_case(rows, blk, r, seed, terms=8, p=0.06):
+    """A > 0 and B < 0, plus `terms` rank-one terms u v^T with sparse random supports in the
+    last columns: L is positive only where some term has both its row and its panel row, so
+    most 16 x 4 slices of max(0, L) hold 0 to 4 positive entries at scattered positions."""
+    g = np.random.default_rng(seed)
+    A = np.abs(g.standard_normal((rows, r))).astype(np.float32)
+    B = -np.abs(g.standard_normal((blk, r))).astype(np.float32)
+    big = np.float32(2.0 * np.sqrt(r))
+    for t in range(terms):
+        c = r - 1 - t
+        A[:, c] = np.where(g.random(rows) < p, big, 0.0)
+        B[:, c] = np.where(g.random(blk) < p, big, 0.0)
+    return A, B
+
+
+@pytest.mark.parametrize("r", [128, 256, 512])
+def test_rectified_contraction_thin_slices(r):
+    """Scattered positive entries of max(0, L) (few per 16 x 4 slice, the regime of the
+    sweeps): matches the oracle, with ragged row and panel counts."""
+    rows, blk = 300 + r % 7, 1000 + 9
+    _say("rectified_contraction thin slices", rows, blk, r)
+    A, B = _thin_positive_case(rows, blk, r, 7 * r + 1)
+    want = salsa.rectified_contraction(A, B)
+    L = A.astype(np.float64) @ B.astype(np.float64).T
+    density = float(np.mean(L > 0))
+    assert 0.002 < density < 0.05, density
+    Y = nmd.rectified_contraction(dev(A), dev(B))
+    torch.cuda.synchronize()
+    assert rel(Y.cpu().numpy(), want) < 2e-5
+
+
 @pytest.mark.parametrize("r", [16, 32, 64, 128])
 def test_rectified_contraction_paper_shape_sampled(r):
     """The kernel at the shape of the paper's throughput table (A: 250000 x r, B: 2500 x r);
