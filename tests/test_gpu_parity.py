@@ -161,6 +161,32 @@ def test_rectified_contraction_paper_shape_sampled(r):
     assert rel(Y[idx].cpu().numpy(), want) < 2e-5
 
 
+def test_graph_tenth_two_sweeps_gathered_second_product():
+    """The graph workload at a tenth of its size (13926 x 13926, r = 256, ~1.7M nonzeros), two
+    stochastic sweeps.  Sweep 0 starts with S-hat = 0; in sweep 1 S-hat is sparse and positive,
+    and nearly all of the dense kernel's second product goes through gathered slices (the
+    counters show it).  W, H and the objective against the oracle."""
+    p = gen.config(4, scale=0.1)
+    _say("graph workload at scale 0.1, two sweeps", p.m, p.n, p.nnz)
+    ctx = make_ctx(p)
+    W, H = dev(p.W0), dev(p.H0)
+    ctx.sweep(W, H, 1)
+    ctx.dense_blocks(reset=True)
+    ctx.sweep(W, H, 1)
+    run, total, entries = ctx.dense_blocks()
+    print(f"second sweep: {run} of {total} slices run whole, {entries} entries gathered")
+    assert total > 0 and 0 <= run <= total and entries > 0
+    assert ctx.dense_blocks(reset=True) == (run, total, entries)
+    assert ctx.dense_blocks() == (0, 0, 0)
+    Wg, Hg = W.cpu().numpy(), H.cpu().numpy()
+    Wo, Ho, S = oracle_run(p, 2)
+    ew, eh = rel(Wg, Wo), rel(Hg, Ho)
+    print(f"two sweeps: rel err W {ew:.2e} H {eh:.2e}")
+    assert ew < TOL and eh < TOL
+    f = ctx.objective(W, H)
+    assert abs(f - salsa.objective(S, Wg, Hg)) <= TOL * f
+
+
 # -------------------------------------------------------------- whole sweeps, small problems
 def test_config1_deterministic_three_sweeps():
     p = gen.config(1)
