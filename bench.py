@@ -38,11 +38,17 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f)
 
 
 def kernel_source_hash():
+    """SHA-256 of the dense kernel's sources with // comments, trailing blanks and blank lines
+    removed, so that it changes with the code and not with its comments."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f) as fh:
+            for line in fh:
+                code = re.sub(r"//.*", "", line).rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
     return h.hexdigest()
 
 

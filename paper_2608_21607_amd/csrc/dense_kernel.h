@@ -13,7 +13,7 @@
 // and consumed by MFMA; neither L nor S-hat reaches memory (the IO-aware fusion of Sec. 4.2,
 // with the raw panel P instead of a pseudo-inverse).
 //
-// Data flow (one workgroup = 4 waves, one per SIMD):
+// Data flow (one workgroup = WAVES waves: 8 at r_p = 128 and 256, two per SIMD; 4 elsewhere):
 //   * X: rows x RP row-major (RP = padded rank, zero columns beyond r).  Each wave keeps
 //     16*MI rows of X resident in VGPRs as MFMA operands for the whole launch.
 //   * P rows of the split's range stream through LDS (row stride RP + 4 floats, which keeps
@@ -22,7 +22,9 @@
 //   * GEMM1 builds the transposed tile L^T (16 j x 16 i); the accumulator of lane l, register
 //     v holds L[i = l%16][j = 4(l/16) + v], which is exactly the srcA layout of GEMM2 for the
 //     k-slice {4(l/16) + v}: the rectified tile feeds GEMM2 with no data movement.
-//   * GEMM2: Y[i][c] += sum_j max(0, L[i][j]) P[j][c], srcB read from LDS as single floats.
+//   * GEMM2: Y[i][c] += sum_j max(0, L[i][j]) P[j][c], srcB read from LDS as single floats,
+//     per 16 x 4 slice of max(0, L): skipped when zero, packed into gathered slices when it
+//     holds only a few positive entries (r_p = 256), run whole otherwise.
 //   * Split-J: the workgroups of one row tile may be spread over `nsplit` disjoint ranges of P
 //     rows, each writing its own partial Y; the solve kernel sums them in fp64.
 
