@@ -42,8 +42,10 @@ enum {
 enum { NMD_DETERMINISTIC = 0, NMD_STOCHASTIC = 1 };
 
 enum {
-  NMD_FLAG_ASYNC = 1u, /* do not synchronise at the end of a sweep; device-detected errors
-                          are then reported by the next synchronising call               */
+  NMD_FLAG_ASYNC = 1u, /* do not synchronise at the end of a call that runs steps; a step
+                          the device rejects is then not reported, the factors written
+                          back are unspecified and later steps are skipped until
+                          nmd_reset                                                       */
   NMD_FLAG_TIMING = 2u /* record HIP events around every kernel class (see
                           nmd_get_kernel_timing); adds a few microseconds per step        */
 };
@@ -95,9 +97,11 @@ int nmd_set_sparse_csr(nmd_ctx* ctx, int64_t nnz, const int64_t* row_ptr, const 
  * B <- B + Delta^T A (A^T A)^-1 over all rows (eqs. spLsqA, spLsqB), with eta and gamma
  * applied as in the stochastic update.  The sweep counter t and the momentum buffers persist
  * across calls (nmd_reset clears them).  Returns NMD_ESTATE without S, NMD_EINVAL on NULL
- * pointers or n_sweeps < 1, NMD_ENOTPD / NMD_ENONFINITE when the device flags a step (later
- * steps are then skipped; nmd_last_error names the sweep and step), NMD_EDEVICE on a HIP
- * failure.  Unless NMD_FLAG_ASYNC is set the call synchronises the stream before returning.
+ * pointers or n_sweeps < 1, NMD_ENOTPD / NMD_ENONFINITE when the device rejects a step: the
+ * later steps are skipped, W and H receive the factors after the last completed step (the
+ * momenta are kept at that state too) and nmd_last_error names the sweep and step.
+ * NMD_EDEVICE on a HIP failure.  Unless NMD_FLAG_ASYNC is set the call synchronises the stream
+ * before returning.
  */
 int nmd_als_block_sweep(nmd_ctx* ctx, float* W, float* H, int32_t n_sweeps, void* hip_stream);
 
@@ -148,7 +152,8 @@ int nmd_get_block_nnz(const nmd_ctx* ctx, int32_t side, int64_t* out, int64_t ca
  * returns K + 1 or a negative code.  Host only. */
 int nmd_get_block_bounds(const nmd_ctx* ctx, int32_t side, int64_t* out, int64_t cap);
 
-/* nmd_reset - zeroes the momentum buffers and the sweep counter. */
+/* nmd_reset - zeroes the momentum buffers and the sweep counter, and clears a step rejection
+ * left pending on the device (see NMD_FLAG_ASYNC).  Synchronises the device. */
 int nmd_reset(nmd_ctx* ctx);
 
 /* nmd_get_sweep_count - *t = number of sweeps run since creation or the last reset. */

@@ -225,7 +225,12 @@ struct nmd_ctx {
   bool dev_ready = false;
   bool sparse_uploaded = false;
   int device = -1;
+  // Factors (padded, B = H^T) and momenta: the current buffers and a second one of each.  A
+  // step reads the current factor and momentum and writes the other pair, which then becomes
+  // current, so a step the device rejects leaves the state of the last completed step intact.
   float *A = nullptr, *B = nullptr, *VA = nullptr, *VB = nullptr;
+  float *A2 = nullptr, *B2 = nullptr, *VA2 = nullptr, *VB2 = nullptr;
+  std::vector<std::pair<int, bool>> enqueued;  // (step id, W-step) of the call's steps, in order
   float* Ypart = nullptr;
   int64_t ypart_floats = 0;
   float* scratch = nullptr;
@@ -311,6 +316,10 @@ void free_device(nmd_ctx* c) {
   dfree(c->B);
   dfree(c->VA);
   dfree(c->VB);
+  dfree(c->A2);
+  dfree(c->B2);
+  dfree(c->VA2);
+  dfree(c->VB2);
   dfree(c->Ypart);
   dfree(c->G);
   dfree(c->Gtmp);
@@ -383,6 +392,8 @@ int ensure_device(nmd_ctx* c) {
     const int64_t mpad = c->m + 256, npad = c->n + 256;
     if (dalloc(&c->A, mpad * rp) != hipSuccess || dalloc(&c->B, npad * rp) != hipSuccess ||
         dalloc(&c->VA, mpad * rp) != hipSuccess || dalloc(&c->VB, npad * rp) != hipSuccess ||
+        dalloc(&c->A2, mpad * rp) != hipSuccess || dalloc(&c->B2, npad * rp) != hipSuccess ||
+        dalloc(&c->VA2, mpad * rp) != hipSuccess || dalloc(&c->VB2, npad * rp) != hipSuccess ||
         dalloc(&c->G, rp * rp) != hipSuccess || dalloc(&c->Gtmp, rp * rp + 64 * 64) != hipSuccess ||
         dalloc(&c->Gpart, (int64_t)c->gram_chunks_max * rp * rp) != hipSuccess ||
         dalloc(&c->objout, 8) != hipSuccess || dalloc(&c->status, 2) != hipSuccess ||
@@ -413,10 +424,10 @@ int ensure_device(nmd_ctx* c) {
       free_device(c);
       return fail(c, NMD_ENOMEM, "pinned host allocation failed");
     }
-    HIP_TRY(c, hipMemset(c->VA, 0, (size_t)mpad * rp * sizeof(float)));
-    HIP_TRY(c, hipMemset(c->VB, 0, (size_t)npad * rp * sizeof(float)));
-    HIP_TRY(c, hipMemset(c->A, 0, (size_t)mpad * rp * sizeof(float)));
-    HIP_TRY(c, hipMemset(c->B, 0, (size_t)npad * rp * sizeof(float)));
+    for (float* p : {c->VA, c->VA2, c->A, c->A2})
+      HIP_TRY(c, hipMemset(p, 0, (size_t)mpad * rp * sizeof(float)));
+    for (float* p : {c->VB, c->VB2, c->B, c->B2})
+      HIP_TRY(c, hipMemset(p, 0, (size_t)npad * rp * sizeof(float)));
     // default priority on purpose: every stream of the library runs at the same priority
     if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess ||
         hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
@@ -526,6 +537,17 @@ int collect_timing(nmd_ctx* c) {
 // ---------------------------------------------------------------------- one update step --
 // wstep: update A = W from column block `block` (all column blocks if block < 0); otherwise
 // update B = H^T from row block `block` (all row blocks if block < 0).
+// The other buffers of one side's factor and momentum become current.
+void swap_side(nmd_ctx* c, bool wside) {
+  if (wside) {
+    std::swap(c->A, c->A2);
+    std::swap(c->VA, c->VA2);
+  } else {
+    std::swap(c->B, c->B2);
+    std::swap(c->VB, c->VB2);
+  }
+}
+
 int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, int step_id,
                 hipStream_t st) {
   Side& sd = wstep ? c->ws : c->hs;
@@ -587,9 +609,13 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
   HIP_TRY(c, hipStreamWaitEvent(st, c->ev_join, 0));
   {
     Scope sc(c, st, K_APPLY, 2.0 * rows * (double)rp * rp, 4.0 * rows * rp * (ns + 4));
-    HIP_TRY(c, nmd::launch_apply(c->Ypart, y_stride, (int)ns, nullptr, Gneg, X, V, rows, rp, eta,
-                                 gamma, c->status, step_id, st));
+    float* Xout = wstep ? c->A2 : c->B2;
+    float* Vout = wstep ? c->VA2 : c->VB2;
+    HIP_TRY(c, nmd::launch_apply(c->Ypart, y_stride, (int)ns, nullptr, Gneg, X, V, Xout, Vout, rows,
+                                 rp, eta, gamma, c->status, step_id, st));
   }
+  swap_side(c, wstep);
+  c->enqueued.emplace_back(step_id, wstep);
   return NMD_OK;
 }
 
@@ -617,13 +643,27 @@ std::string describe_step(nmd_ctx* c, int step_id, int64_t first_sweep, int32_t 
   return buf;
 }
 
-int finish(nmd_ctx* c, hipStream_t st, int64_t first_sweep, int32_t steps_per) {
-  if (c->opt.flags & NMD_FLAG_ASYNC) return NMD_OK;
+// Ends a call that ran steps: copies the factors back to W and H and, unless NMD_FLAG_ASYNC is
+// set, reports a step the device rejected.  Then the factors stored are those after the last
+// completed step: the buffers each side had before the call, swapped once per completed step
+// of that side (a rejected step and every step after it wrote only to buffers not current).
+int conclude(nmd_ctx* c, float* W, float* H, hipStream_t st, int64_t first_sweep,
+             int32_t steps_per) {
+  if (c->opt.flags & NMD_FLAG_ASYNC) return store_factors(c, W, H, st);
   HIP_TRY(c, hipMemcpyAsync(c->h_status, c->status, 2 * sizeof(int), hipMemcpyDeviceToHost, st));
   HIP_TRY(c, hipStreamSynchronize(st));
   const int flags = c->h_status[0];
-  if (flags == 0) return NMD_OK;
+  if (flags == 0) {
+    int rc = store_factors(c, W, H, st);
+    if (rc) return rc;
+    HIP_TRY(c, hipStreamSynchronize(st));
+    return NMD_OK;
+  }
   const int step = c->h_status[1];
+  for (auto it = c->enqueued.rbegin(); it != c->enqueued.rend(); ++it)
+    if (it->first >= step) swap_side(c, it->second);  // undo the steps from the rejected one on
+  int rc = store_factors(c, W, H, st);
+  if (rc) return rc;
   HIP_TRY(c, hipMemsetAsync(c->status, 0, sizeof(int), st));
   HIP_TRY(c, hipMemsetAsync(c->status + 1, 0x7f, sizeof(int), st));
   HIP_TRY(c, hipStreamSynchronize(st));
@@ -814,6 +854,7 @@ static int run(nmd_ctx* c, float* W, float* H, const std::vector<std::vector<int
   int rc = ensure_device(c);
   if (rc) return rc;
   if ((rc = load_factors(c, W, H, st))) return rc;
+  c->enqueued.clear();
   int step_id = 0;
   for (const auto& list : lists) {
     if (full_halves) {
@@ -830,7 +871,7 @@ static int run(nmd_ctx* c, float* W, float* H, const std::vector<std::vector<int
       ++step_id;
     }
   }
-  return store_factors(c, W, H, st);
+  return NMD_OK;
 }
 
 int nmd_als_block_sweep(nmd_ctx* c, float* W, float* H, int32_t n_sweeps, void* hip_stream) {
@@ -846,7 +887,7 @@ int nmd_als_block_sweep(nmd_ctx* c, float* W, float* H, int32_t n_sweeps, void* 
   rc = run(c, W, H, lists, !sto, st);
   if (rc) return rc;
   c->t += n_sweeps;
-  return finish(c, st, first, c->hs.nblk() + c->ws.nblk());
+  return conclude(c, W, H, st, first, c->hs.nblk() + c->ws.nblk());
 }
 
 int nmd_run_steps(nmd_ctx* c, float* W, float* H, const int32_t* steps, int32_t n_steps,
@@ -862,7 +903,7 @@ int nmd_run_steps(nmd_ctx* c, float* W, float* H, const int32_t* steps, int32_t 
   std::vector<std::vector<int32_t>> lists(1, std::vector<int32_t>(steps, steps + n_steps));
   rc = run(c, W, H, lists, false, (hipStream_t)hip_stream);
   if (rc) return rc;
-  return finish(c, (hipStream_t)hip_stream, 0, 0);
+  return conclude(c, W, H, (hipStream_t)hip_stream, 0, 0);
 }
 
 int nmd_objective(nmd_ctx* c, const float* W, const float* H, double* out_obj, void* hip_stream) {
@@ -934,6 +975,8 @@ int nmd_reset(nmd_ctx* c) {
     HIP_TRY(c, hipDeviceSynchronize());
     HIP_TRY(c, hipMemset(c->VA, 0, (size_t)(c->m + 256) * c->rp * sizeof(float)));
     HIP_TRY(c, hipMemset(c->VB, 0, (size_t)(c->n + 256) * c->rp * sizeof(float)));
+    HIP_TRY(c, hipMemset(c->status, 0, sizeof(int)));
+    HIP_TRY(c, hipMemset(c->status + 1, 0x7f, sizeof(int)));
     HIP_TRY(c, hipDeviceSynchronize());
   }
   return NMD_OK;

@@ -62,13 +62,15 @@ hipError_t launch_gram(const float* P, int64_t blk, int r, int rp, double* Gpart
 // Gsw <- -G^-1 by block sweeps; flags status on a non-positive pivot.  Gtmp: scratch rp x rp.
 hipError_t launch_inverse(double* G, double* Gtmp, int rp, int* status, int step_id,
                           double** result, hipStream_t st);
-// V <- gamma V + eta U (-Gneg), X <- X + V, where U = Delta P_J is the sum (fp64) of the nsplit
-// partial outputs plus, when Ysp is not NULL, a separate correction buffer (rows x rp), and
-// -Gneg = (P_J^T P_J)^-1.
+// Vout = gamma Vin + eta U (-Gneg), Xout = Xin + Vout, where U = Delta P_J is the sum (fp64)
+// of the nsplit partial outputs plus, when Ysp is not NULL, a separate correction buffer
+// (rows x rp), and -Gneg = (P_J^T P_J)^-1.  The outputs are other buffers than the inputs, so
+// a step that a later check rejects leaves its inputs intact.  Nothing is written once status
+// holds a failure from an earlier kernel.
 hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const float* Ysp,
-                        const double* Gneg,
-                        float* X, float* V, int64_t rows, int rp, float eta, float gamma,
-                        int* status, int step_id, hipStream_t st);
+                        const double* Gneg, const float* Xin, const float* Vin, float* Xout,
+                        float* Vout, int64_t rows, int rp, float eta, float gamma, int* status,
+                        int step_id, hipStream_t st);
 
 // Layout helpers between the caller's W (m x r), H (r x n) and the padded panels.
 hipError_t launch_pad_rows(const float* src, int64_t rows, int r, float* dst, int rp,

@@ -338,9 +338,12 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Yp
                                                     int64_t y_stride, int nsplit,
                                                     const float* __restrict__ Ysp,
                                                     const double* __restrict__ Gneg,
-                                                    float* __restrict__ X, float* __restrict__ V,
-                                                    int64_t rows, float eta, float gamma,
-                                                    int* status, int step_id) {
+                                                    const float* __restrict__ Xin,
+                                                    const float* __restrict__ Vin,
+                                                    float* __restrict__ Xout,
+                                                    float* __restrict__ Vout, int64_t rows,
+                                                    float eta, float gamma, int* status,
+                                                    int step_id) {
   using C = ApplyCfg<RP>;
   constexpr int RW = C::RW, NRB = C::NRB, NCB = C::NCB;
   constexpr int LS = RP + 1;
@@ -424,13 +427,13 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Yp
         if (row < rows) {
           const int64_t o = row * RP + 16 * cblock(b) + l16;
           const double stepv = -acc[a][b][v];
-          const double xa = (double)X[o];
-          const double vn = (double)gamma * (double)V[o] + (double)eta * stepv;
+          const double xa = (double)Xin[o];
+          const double vn = (double)gamma * (double)Vin[o] + (double)eta * stepv;
           const float xf = (float)(xa + vn);
           const float vf = (float)vn;
           bad |= !isfinite(xf) || !isfinite(vf);
-          X[o] = xf;
-          V[o] = vf;
+          Xout[o] = xf;
+          Vout[o] = vf;
         }
       }
   if (bad) flag(status, STATUS_NONFINITE, step_id);
@@ -457,8 +460,10 @@ __global__ __launch_bounds__(256, 2) void apply_wide_kernel(const float* __restr
                                                          int64_t y_stride, int nsplit,
                                                          const float* __restrict__ Ysp,
                                                          const double* __restrict__ Gneg,
-                                                         float* __restrict__ X,
-                                                         float* __restrict__ V, int64_t rows,
+                                                         const float* __restrict__ Xin,
+                                                         const float* __restrict__ Vin,
+                                                         float* __restrict__ Xout,
+                                                         float* __restrict__ Vout, int64_t rows,
                                                          float eta, float gamma, int* status,
                                                          int step_id) {
   using C = WideCfg<RP, RW>;
@@ -542,13 +547,13 @@ __global__ __launch_bounds__(256, 2) void apply_wide_kernel(const float* __restr
         if (row < rows) {
           const int64_t o = row * RP + 16 * (wave + 4 * b) + l16;
           const double stepv = -acc[a][b][v];
-          const double xa = (double)X[o];
-          const double vn = (double)gamma * (double)V[o] + (double)eta * stepv;
+          const double xa = (double)Xin[o];
+          const double vn = (double)gamma * (double)Vin[o] + (double)eta * stepv;
           const float xf = (float)(xa + vn);
           const float vf = (float)vn;
           bad |= !isfinite(xf) || !isfinite(vf);
-          X[o] = xf;
-          V[o] = vf;
+          Xout[o] = xf;
+          Vout[o] = vf;
         }
       }
   if (bad) flag(status, STATUS_NONFINITE, step_id);
@@ -556,15 +561,16 @@ __global__ __launch_bounds__(256, 2) void apply_wide_kernel(const float* __restr
 
 hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const float* Ysp,
                         const double* Gneg,
-                        float* X, float* V, int64_t rows, int rp, float eta, float gamma,
-                        int* status, int step_id, hipStream_t st) {
+                        const float* Xin, const float* Vin, float* Xout, float* Vout,
+                        int64_t rows, int rp, float eta, float gamma, int* status, int step_id,
+                        hipStream_t st) {
   if (rows <= 0) return hipSuccess;
 #define CASE(R)                                                                              \
   case R: {                                                                                  \
     constexpr int RW = ApplyCfg<R>::RW;                                                      \
     hipLaunchKernelGGL((apply_kernel<R>), dim3((unsigned)((rows + RW - 1) / RW)), dim3(256), 0, \
-                       st, Ypart, y_stride, nsplit, Ysp, Gneg, X, V, rows, eta, gamma, status,    \
-                       step_id);                                                             \
+                       st, Ypart, y_stride, nsplit, Ysp, Gneg, Xin, Vin, Xout, Vout, rows, eta,   \
+                       gamma, status, step_id);                                              \
     break;                                                                                   \
   }
   // row tile: the tallest allowed one that still gives 4096 workgroups, else 16 rows
@@ -577,8 +583,8 @@ hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const 
     }
 #define WIDE_RW(R, W)                                                                        \
   hipLaunchKernelGGL((apply_wide_kernel<R, W>), dim3((unsigned)((rows + W - 1) / W)), dim3(256), \
-                     0, st, Ypart, y_stride, nsplit, Ysp, Gneg, X, V, rows, eta, gamma, status,   \
-                     step_id)
+                     0, st, Ypart, y_stride, nsplit, Ysp, Gneg, Xin, Vin, Xout, Vout, rows, eta,  \
+                     gamma, status, step_id)
 #define WIDE(R)                                                                              \
   case R: {                                                                                  \
     if (rw >= 64 && wide_max_rw<R>() >= 64) WIDE_RW(R, (wide_max_rw<R>() >= 64 ? 64 : 16)); \

@@ -407,6 +407,43 @@ def test_singular_gram_is_reported_and_later_steps_skipped():
     assert np.array_equal(H.cpu().numpy(), H0)
 
 
+def test_rejected_step_keeps_last_completed_step():
+    """A NaN in H outside the first W-step's column block: step 0 (that W-step) completes, the
+    H-step after it carries the NaN into its output and is rejected.  W must come back exactly
+    as after step 0 alone and H as given (the rejected step and the skipped ones leave the
+    factors and momenta of the last completed step); after nmd_reset the context runs again."""
+    p = gen.config(1)
+    _say("NaN in H, rejected at step 1")
+    first = gen_first_w_block(p)
+    col = first[1] % p.n if first[1] < p.n else 0  # a column outside the first W block
+    assert not (first[0] <= col < first[1])
+    H0 = p.H0.copy()
+    H0[3, col] = np.nan
+    R, C = partition.num_blocks(p.m, p.block_m), partition.num_blocks(p.n, p.block_n)
+    steps = schedule.sweep_schedule(p.seed, 0, R, C, True)[:3]
+    assert steps[0] > 0 and steps[1] < 0
+    kw = dict(mode="stochastic", eta=1.0, mom=0.9)
+    ref = make_ctx(p, **kw)
+    Wr, Hr = dev(p.W0), dev(H0)
+    ref.run_steps(Wr, Hr, steps[:1])
+    ctx = make_ctx(p, **kw)
+    W, H = dev(p.W0), dev(H0)
+    with pytest.raises(nmd.NmdError) as e:
+        ctx.run_steps(W, H, steps)
+    assert e.value.code == -6 and "step 1" in e.value.message
+    assert np.array_equal(W.cpu().numpy(), Wr.cpu().numpy())
+    assert np.array_equal(H.cpu().numpy(), H0, equal_nan=True)
+    # after nmd_reset the context runs the same steps exactly as the reference does
+    ctx.reset()
+    ref.reset()
+    W2, H2 = dev(p.W0), dev(p.H0)
+    W3, H3 = dev(p.W0), dev(p.H0)
+    ctx.run_steps(W2, H2, steps)
+    ref.run_steps(W3, H3, steps)
+    assert np.array_equal(W2.cpu().numpy(), W3.cpu().numpy())
+    assert np.array_equal(H2.cpu().numpy(), H3.cpu().numpy())
+
+
 def gen_first_w_block(p):
     R, C = partition.num_blocks(p.m, p.block_m), partition.num_blocks(p.n, p.block_n)
     code = schedule.sweep_schedule(p.seed, 0, R, C, True)[0]
