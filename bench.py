@@ -13,6 +13,7 @@ a bounded sample of the same workload (the first W-step and the first H-step of 
 size), scaled to sweeps/s.
 
     python bench.py [--steps K] [--warmup W] [--config 4] [--no-cpu-baseline]
+    python bench.py --kernel-mb      (the fused kernel alone, shape of the paper's kernel table)
 """
 
 import argparse
@@ -63,6 +64,51 @@ def measured_traffic(config):
     if t.get("kernel_source_sha256") != kernel_source_hash() or t.get("config") != config:
         return None
     return t.get("traffic_bytes_per_launch")
+
+
+# The paper's fused TF32 kernel at m = 250000 rows, a 2500-row panel (its kernel throughput
+# table, Sec. 4.2): TFLOP/s on an H100 PCIe and on an RTX Pro 6000 Blackwell.  Context only:
+# other hardware, and TF32 (gfx950 has no TF32 matrix instructions; this build is fp32).
+PAPER_FUSED_TF32 = {16: (215.30, 191.72), 32: (283.73, 203.06), 64: (285.10, 206.11),
+                    128: (279.19, 189.80)}
+
+
+def kernel_mb(steps, warmup):
+    """The fused rectified contraction Y = max(0, A B^T) B alone at the shape of the paper's
+    kernel table: A 250000 x r, B 2500 x r, N(0,1) entries.  About half of L is positive, so
+    every 16 x 4 slice of the second product runs and the work is 4 rows blk r flops."""
+    import torch
+
+    import paper_2608_21607_amd as nmd
+
+    rows, blk = 250_000, 2500
+    res = []
+    for r in (16, 32, 64, 128):
+        g = torch.Generator(device="cuda").manual_seed(r)
+        A = torch.randn((rows, r), generator=g, device="cuda")
+        B = torch.randn((blk, r), generator=g, device="cuda")
+        Y = torch.empty((rows, r), device="cuda")
+        for _ in range(warmup):
+            nmd.rectified_contraction(A, B, Y)
+        start = torch.cuda.Event(enable_timing=True)
+        stop = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(steps):
+            nmd.rectified_contraction(A, B, Y)
+        stop.record()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(stop) / steps
+        tflops = 4.0 * rows * blk * r / (ms / 1e3) / 1e12
+        h100, rtx = PAPER_FUSED_TF32[r]
+        res.append({"r": r, "ms_per_launch": ms, "tflops": tflops,
+                    "frac_of_fp32_peak": tflops / PEAK_FP32_MFMA,
+                    "paper_tf32_h100_pcie": h100, "paper_tf32_rtx_pro_6000": rtx})
+        log(f"r = {r}: {ms:.3f} ms per launch, {tflops:.1f} TFLOP/s")
+    return {"metric": "fused rectified contraction TFLOP/s (4 rows blk r per launch)",
+            "unit": "TFLOP/s", "dtype": "f32", "data": "synthetic",
+            "config": {"workload": "kernel alone, A 250000 x r, B 2500 x r, N(0,1)"},
+            "steps": steps, "warmup": warmup, "results": res}
 
 
 def log(*a):
@@ -119,6 +165,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernel-mb", action="store_true",
+                    help="time the fused kernel alone at the shape of the paper's kernel table")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first run one plain 1 GiB copy kernel (calibrates rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -134,6 +182,9 @@ def main():
     from workloads import gen
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.kernel_mb:
+        print(json.dumps(kernel_mb(max(args.steps, 20), max(args.warmup, 2))), flush=True)
+        return
     if args.copy_probe:
         src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
         dst = torch.empty_like(src)
@@ -212,7 +263,10 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": p.name + " (synthetic stand-in for the paper's connectome matrix)",
+            "workload": p.name + {
+                4: " (synthetic stand-in for the paper's connectome matrix)",
+                5: " (synthetic stand-in for the paper's bigram-count matrix)",
+            }.get(args.config, " (synthetic)"),
             "m": p.m, "n": p.n, "r": p.r, "nnz": p.nnz,
             "block_m": p.block_m, "block_n": p.block_n,
             "mode": p.mode, "eta": p.eta, "momentum": p.momentum, "seed": p.seed,
