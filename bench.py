@@ -68,7 +68,7 @@ def measured_traffic(config):
 
 # The paper's fused TF32 kernel at m = 250000 rows, a 2500-row panel (its kernel throughput
 # table, Sec. 4.2): TFLOP/s on an H100 PCIe and on an RTX Pro 6000 Blackwell.  Context only:
-# other hardware, and TF32 (gfx950 has no TF32 matrix instructions; this build is fp32).
+# other hardware, and TF32 (gfx950 has no TF32 matrix instructions; the kernel here is fp32).
 PAPER_FUSED_TF32 = {16: (215.30, 191.72), 32: (283.73, 203.06), 64: (285.10, 206.11),
                     128: (279.19, 189.80)}
 
@@ -171,8 +171,7 @@ def main():
                     help="first run one plain 1 GiB copy kernel (calibrates rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(the sharded design is described in DESIGN.md)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library has no multi-GPU path", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
