@@ -26,6 +26,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA = 157.3   # TFLOP/s, MI355X dense fp32 matrix
+PEAK_BF16_MFMA = 2500.0  # TFLOP/s, MI355X dense bf16 matrix
 PEAK_HBM = 8.0e3         # GB/s, MI355X HBM3E
 
 METRIC = "ALS sweeps/sec and dense-equiv TFLOP/s (4mnr/sweep), % of fp32 MFMA peak"
@@ -33,18 +34,25 @@ METRIC = "ALS sweeps/sec and dense-equiv TFLOP/s (4mnr/sweep), % of fp32 MFMA pe
 # HBM traffic of the fused dense kernel, from two rocprofv3 --pmc passes (FETCH_SIZE, then
 # WRITE_SIZE) scaled by the same counters on a plain copy of known size; valid only for the
 # kernel sources it was taken on.
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dense_r256_graph139255_traffic.json")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f)
-                  for f in ("tile.h", "dense_kernel.h", "dense.hip")]
+TRAFFIC_FILES = {
+    "fp32": os.path.join(ROOT, "profiles", "dense_r256_graph139255_traffic.json"),
+    "split_bf16": os.path.join(ROOT, "profiles", "dense_split_r256_graph139255_traffic.json"),
+}
+KERNEL_SOURCES = {
+    "fp32": [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f)
+             for f in ("tile.h", "dense_kernel.h", "dense.hip")],
+    "split_bf16": [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f)
+                   for f in ("tile.h", "dense_kernel.h", "dense_split.h", "dense_split.hip")],
+}
 
 
-def kernel_source_hash():
+def kernel_source_hash(variant="fp32"):
     """SHA-256 of the dense kernel's sources with // comments, trailing blanks and blank lines
     removed, so that it changes with the code and not with its comments."""
     import hashlib
     import re
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_SOURCES[variant]:
         with open(f) as fh:
             for line in fh:
                 code = re.sub(r"//.*", "", line).rstrip()
@@ -53,15 +61,15 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def measured_traffic(config):
+def measured_traffic(config, variant="fp32"):
     """Bytes per dense-kernel launch from the committed counter summary, or None when the
     summary is missing, was taken on another workload, or the kernel has changed since."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(TRAFFIC_FILES[variant]) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_sha256") != kernel_source_hash() or t.get("config") != config:
+    if t.get("kernel_source_sha256") != kernel_source_hash(variant) or t.get("config") != config:
         return None
     return t.get("traffic_bytes_per_launch")
 
@@ -167,6 +175,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-mb", action="store_true",
                     help="time the fused kernel alone at the shape of the paper's kernel table")
+    ap.add_argument("--split-bf16", action="store_true",
+                    help="opt-in r = 256 variant: first product of the dense kernel as three "
+                         "bf16 MFMA products of a two-term split (fp32 stays the default)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first run one plain 1 GiB copy kernel (calibrates rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -197,7 +208,8 @@ def main():
         f"({time.perf_counter() - t0:.1f} s to generate)")
 
     ctx = nmd.Context(p.m, p.n, p.r, p.block_m, p.block_n, seed=p.seed, mode=p.mode,
-                      eta=p.eta, momentum=p.momentum, flags=nmd.FLAG_TIMING)
+                      eta=p.eta, momentum=p.momentum,
+                      flags=nmd.FLAG_TIMING | (nmd.FLAG_SPLIT_BF16 if args.split_bf16 else 0))
     t0 = time.perf_counter()
     ctx.set_sparse_csr(p.row_ptr, p.col, p.val)
     log(f"ingest {time.perf_counter() - t0:.1f} s")
@@ -247,6 +259,16 @@ def main():
     dense_tflops = dense_alg_flops / dense_s / 1e12 if dense_s > 0 else 0.0
     dense_equiv_kernel = dense["flops"] / dense_s / 1e12 if dense_s > 0 else 0.0
     sparse_gbs = sparse["bytes"] / (sparse["ms"] / 1e3) / 1e9 if sparse["ms"] > 0 else 0.0
+    split = args.split_bf16 and rp == 256
+    if split:
+        # The split variant runs the first product as three bf16 products at the bf16 peak and
+        # the second on fp32 MFMA: the roofline is the time those would take at their peaks,
+        # stated as the equivalent rate for the kernel's algorithmic flops.
+        f1 = 0.5 * dense["flops"]
+        f2 = dense_alg_flops - f1
+        peak = dense_alg_flops / (3.0 * f1 / PEAK_BF16_MFMA + f2 / PEAK_FP32_MFMA)
+    else:
+        peak = PEAK_FP32_MFMA
 
     out = {
         "metric": METRIC,
@@ -259,7 +281,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16x3 split / f32" if split else "f32",
         "data": "synthetic",
         "config": {
             "workload": p.name + {
@@ -285,11 +307,11 @@ def main():
         "roofline": {
             "bound": "mfma",
             "achieved": dense_tflops,
-            "peak": PEAK_FP32_MFMA,
+            "peak": peak,
             "unit": "TFLOP/s",
-            "frac": dense_tflops / PEAK_FP32_MFMA,
-            "traffic": measured_traffic(args.config),
-            "kernel": f"dense_kernel<{rp}>",
+            "frac": dense_tflops / peak,
+            "traffic": measured_traffic(args.config, "split_bf16" if split else "fp32"),
+            "kernel": "dense_split_kernel" if split else f"dense_kernel<{rp}>",
             "launches": dense["launches"],
             "avg_launch_ms": dense["ms"] / max(1, dense["launches"]),
             "flops_per_launch": dense_alg_flops / max(1, dense["launches"]),

@@ -5,7 +5,7 @@ ctypes binding and `build` compiles it in-tree.
 """
 
 from .nmd import (  # noqa: F401
-    Context, NmdError, rectified_contraction, lib, header_functions,
-    DETERMINISTIC, STOCHASTIC, FLAG_ASYNC, FLAG_TIMING,
+    Context, NmdError, rectified_contraction, rectified_contraction_split, lib,
+    header_functions, DETERMINISTIC, STOCHASTIC, FLAG_ASYNC, FLAG_TIMING, FLAG_SPLIT_BF16,
     KERNEL_DENSE, KERNEL_SPARSE, KERNEL_FACTOR, KERNEL_APPLY,
 )

@@ -232,6 +232,7 @@ struct nmd_ctx {
   float *A2 = nullptr, *B2 = nullptr, *VA2 = nullptr, *VB2 = nullptr;
   std::vector<std::pair<int, bool>> enqueued;  // (step id, W-step) of the call's steps, in order
   float* Ypart = nullptr;
+  float* Psplit = nullptr;  // split-bf16 panel (NMD_FLAG_SPLIT_BF16 at r_p = 256), max(m, n) x 256
   int64_t ypart_floats = 0;
   float* scratch = nullptr;
   int64_t scratch_floats = 0;
@@ -321,6 +322,7 @@ void free_device(nmd_ctx* c) {
   dfree(c->VA2);
   dfree(c->VB2);
   dfree(c->Ypart);
+  dfree(c->Psplit);
   dfree(c->G);
   dfree(c->Gtmp);
   dfree(c->Gpart);
@@ -414,7 +416,9 @@ int ensure_device(nmd_ctx* c) {
     need = std::max(need, nsplit_for(c->m, c->n, c->rp, c->dense_slots) * c->m);
     need = std::max(need, nsplit_for(c->n, c->m, c->rp, c->dense_slots) * c->n);
     c->ypart_floats = need * rp;
-    if (dalloc(&c->Ypart, c->ypart_floats) != hipSuccess) {
+    if (dalloc(&c->Ypart, c->ypart_floats) != hipSuccess ||
+        ((c->opt.flags & NMD_FLAG_SPLIT_BF16) && rp == 256 &&
+         dalloc(&c->Psplit, std::max(c->m, c->n) * 256) != hipSuccess)) {
       free_device(c);
       return fail(c, NMD_ENOMEM, "device allocation of %lld partial-output floats failed",
                   (long long)c->ypart_floats);
@@ -580,8 +584,14 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
     // U = Delta_{:J} P_J starts as -max(0, X P_J^T) P_J (eq. updateD off the nonzeros); the
     // second contraction is skipped on the 16 x 4 slices where that rectified tile is zero
     Scope sc(c, st, K_DENSE, 4.0 * rows * (double)blk * c->r, 4.0 * (2.0 * rows + blk) * c->r);
-    HIP_TRY(c, nmd::launch_dense(X, rows, PJ, blk, rp, c->Ypart, y_stride, (int)ns, -1.0f, c->g2,
-                                 st));
+    if (c->Psplit) {  // split-bf16 first product: the panel is split once per step
+      HIP_TRY(c, nmd::launch_split_panel(PJ, blk, c->Psplit, st));
+      HIP_TRY(c, nmd::launch_dense_split(X, rows, c->Psplit, blk, c->Ypart, y_stride, (int)ns,
+                                         -1.0f, c->g2, st));
+    } else {
+      HIP_TRY(c, nmd::launch_dense(X, rows, PJ, blk, rp, c->Ypart, y_stride, (int)ns, -1.0f,
+                                   c->g2, st));
+    }
     // slices of 16 rows x 4 panel rows examined (those entirely past the last row never run)
     int64_t jblocks = 0;
     for (int64_t s = 0; s < ns; ++s) jblocks += ((s + 1) * blk / ns - s * blk / ns + 15) / 16;
@@ -740,6 +750,8 @@ int nmd_create(nmd_ctx** out, int64_t m, int64_t n, int32_t r, int32_t block_m, 
     return fail(nullptr, NMD_EINVAL, "eta must be finite and >= 0");
   if (!(o.momentum >= 0.0f && o.momentum < 1.0f))
     return fail(nullptr, NMD_EINVAL, "momentum must lie in [0, 1)");
+  if (o.flags & ~(uint32_t)(NMD_FLAG_ASYNC | NMD_FLAG_TIMING | NMD_FLAG_SPLIT_BF16))
+    return fail(nullptr, NMD_EINVAL, "unknown option flags 0x%x", o.flags);
   std::vector<int64_t> rb = balanced_bounds(m, block_m), cb = balanced_bounds(n, block_n);
   int64_t min_rb = m, min_cb = n;
   for (size_t k = 0; k + 1 < rb.size(); ++k) min_rb = std::min(min_rb, rb[k + 1] - rb[k]);
@@ -999,6 +1011,21 @@ int nmd_rectified_contraction(const float* A, int64_t rows, const float* B, int6
                 "r = %d unsupported: use 16, 32, 48, 64 or a multiple of 64 up to 512", r);
   hipError_t e =
       nmd::launch_dense(A, rows, B, blk, r, Y, 0, 1, 1.0f, nullptr, (hipStream_t)hip_stream);
+  if (e != hipSuccess) return fail(nullptr, NMD_EDEVICE, "launch failed: %s", hipGetErrorString(e));
+  return NMD_OK;
+}
+
+int nmd_rectified_contraction_split(const float* A, int64_t rows, const float* B, int64_t blk,
+                                    int32_t r, float* Bsplit, float* Y, void* hip_stream) {
+  g_create_error.clear();
+  if (!A || !B || !Bsplit || !Y)
+    return fail(nullptr, NMD_EINVAL, "A, B, Bsplit and Y must be non-NULL");
+  if (rows < 1 || blk < 1 || rows > INT32_MAX)
+    return fail(nullptr, NMD_EINVAL, "rows and blk must be >= 1");
+  if (r != 256) return fail(nullptr, NMD_EINVAL, "the split-bf16 contraction needs r = 256 (got %d)", r);
+  hipStream_t st = (hipStream_t)hip_stream;
+  hipError_t e = nmd::launch_split_panel(B, blk, Bsplit, st);
+  if (e == hipSuccess) e = nmd::launch_dense_split(A, rows, Bsplit, blk, Y, 0, 1, 1.0f, nullptr, st);
   if (e != hipSuccess) return fail(nullptr, NMD_EDEVICE, "launch failed: %s", hipGetErrorString(e));
   return NMD_OK;
 }

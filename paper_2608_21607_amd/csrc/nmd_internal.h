@@ -46,6 +46,15 @@ hipError_t launch_dense(const float* X, int64_t rows, const float* P, int64_t bl
                         float* Ypart, int64_t y_stride, int nsplit, float sgn,
                         unsigned long long* gemm2_blocks, hipStream_t st);
 
+// Split-bf16 first product (r_p = 256 only): launch_split_panel writes the rows x 256 panel
+// P as rows of 1 KB (32 groups of 8 bf16 hi then 8 bf16 lo, x = hi + lo + O(2^-17 x)) to out
+// (rows x 256 floats of space); launch_dense_split is launch_dense at r_p = 256 with the first
+// product on bf16 MFMA from that split panel.
+hipError_t launch_split_panel(const float* P, int64_t rows, float* out, hipStream_t st);
+hipError_t launch_dense_split(const float* X, int64_t rows, const float* Psplit, int64_t blk,
+                              float* Ypart, int64_t y_stride, int nsplit, float sgn,
+                              unsigned long long* gemm2_blocks, hipStream_t st);
+
 // Sparse correction: for every item, c = sum over its entries of (s - min(0, x_row . p_j)) p_j;
 // a row with a single item gets Y[row] = c (accumulate = 0) or Y[row] += c (accumulate = 1);
 // a row split over several items has its slots summed in order by the fix-up, which writes or

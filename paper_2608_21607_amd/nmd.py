@@ -22,7 +22,7 @@ OK, EINVAL, ENOMEM, EDEVICE, ENOTPD, ESTATE, ENONFINITE = 0, -1, -2, -3, -4, -5,
 CODE_NAMES = {0: "NMD_OK", -1: "NMD_EINVAL", -2: "NMD_ENOMEM", -3: "NMD_EDEVICE",
               -4: "NMD_ENOTPD", -5: "NMD_ESTATE", -6: "NMD_ENONFINITE"}
 DETERMINISTIC, STOCHASTIC = 0, 1
-FLAG_ASYNC, FLAG_TIMING = 1, 2
+FLAG_ASYNC, FLAG_TIMING, FLAG_SPLIT_BF16 = 1, 2, 4
 KERNEL_DENSE, KERNEL_SPARSE, KERNEL_FACTOR, KERNEL_APPLY = 0, 1, 2, 3
 
 
@@ -66,6 +66,7 @@ def lib() -> C.CDLL:
         "nmd_get_sweep_count": (I32, [P, C.POINTER(I64)]),
         "nmd_run_steps": (I32, [P, P, P, P, I32, P]),
         "nmd_rectified_contraction": (I32, [P, I64, P, I64, I32, P, P]),
+        "nmd_rectified_contraction_split": (I32, [P, I64, P, I64, I32, P, P, P]),
         "nmd_get_dense_blocks": (I32, [P, P, P, P, I32]),
         "nmd_get_kernel_timing": (I32, [P, I32, C.POINTER(C.c_double), C.POINTER(I64),
                                         C.POINTER(C.c_double), C.POINTER(C.c_double), I32]),
@@ -229,4 +230,21 @@ def rectified_contraction(A, B, Y=None, stream=None):
                                            _dev_ptr(B, (blk, r), "B"), int(blk), int(r),
                                            _dev_ptr(Y, (rows, r), "Y"), _stream_handle(stream)),
            None)
+    return Y
+
+
+def rectified_contraction_split(A, B, Y=None, work=None, stream=None):
+    """Y = max(0, A B^T) B at r = 256 with the first product on split bf16 MFMA (A: rows x 256,
+    B: blk x 256, float32 CUDA tensors; work: blk x 256 float32 workspace for the split panel)."""
+    import torch
+    rows, r = A.shape
+    blk = B.shape[0]
+    if Y is None:
+        Y = torch.empty((rows, r), dtype=torch.float32, device=A.device)
+    if work is None:
+        work = torch.empty((blk, r), dtype=torch.float32, device=A.device)
+    _check(lib().nmd_rectified_contraction_split(
+        _dev_ptr(A, (rows, r), "A"), int(rows), _dev_ptr(B, (blk, r), "B"), int(blk), int(r),
+        _dev_ptr(work, (blk, r), "work"), _dev_ptr(Y, (rows, r), "Y"), _stream_handle(stream)),
+        None)
     return Y

@@ -34,8 +34,8 @@ def test_every_declared_symbol_is_exported(L):
         assert core in names
 
 
-def _create(m, n, r, bm, bn, seed=1, mode=nmd.STOCHASTIC, eta=1.0, mom=0.0, size=None):
-    opts = nmd.Options(C.sizeof(nmd.Options) if size is None else size, mode, eta, mom, 0)
+def _create(m, n, r, bm, bn, seed=1, mode=nmd.STOCHASTIC, eta=1.0, mom=0.0, size=None, flags=0):
+    opts = nmd.Options(C.sizeof(nmd.Options) if size is None else size, mode, eta, mom, flags)
     p = C.c_void_p()
     rc = nmd.lib().nmd_create(C.byref(p), m, n, r, bm, bn, seed, C.byref(opts))
     return rc, p
@@ -57,6 +57,11 @@ def test_create_rejects_bad_options(L):
     assert _create(10, 10, 2, 5, 5, eta=float("nan"))[0] == nmd.EINVAL
     assert _create(10, 10, 2, 5, 5, mom=1.0)[0] == nmd.EINVAL
     assert _create(10, 10, 2, 5, 5, size=4)[0] == nmd.EINVAL
+    assert _create(10, 10, 2, 5, 5, flags=8)[0] == nmd.EINVAL  # unknown option flag
+    for f in (nmd.FLAG_ASYNC, nmd.FLAG_TIMING, nmd.FLAG_SPLIT_BF16):
+        rc, p = _create(10, 10, 2, 5, 5, flags=f)
+        assert rc == 0
+        L.nmd_destroy(p)
     # deterministic mode accepts r above the block size
     rc, p = _create(100, 100, 30, 25, 25, mode=nmd.DETERMINISTIC)
     assert rc == 0
@@ -129,6 +134,11 @@ def test_rectified_contraction_argument_checks(L):
     assert L.nmd_rectified_contraction(fake, 0, fake, 10, 16, fake, None) == nmd.EINVAL
     assert L.nmd_rectified_contraction(fake, 10, fake, 0, 16, fake, None) == nmd.EINVAL
     assert L.nmd_rectified_contraction(None, 10, fake, 10, 16, fake, None) == nmd.EINVAL
+    split = L.nmd_rectified_contraction_split
+    for r in (16, 128, 512):  # the split-bf16 contraction is for r = 256 only
+        assert split(fake, 10, fake, 10, r, fake, fake, None) == nmd.EINVAL
+    assert split(fake, 10, fake, 10, 256, None, fake, None) == nmd.EINVAL
+    assert split(fake, 0, fake, 10, 256, fake, fake, None) == nmd.EINVAL
 
 
 def test_dense_blocks_before_device_use(L):

@@ -91,11 +91,11 @@ def test_config4_block_structure_and_initial_objective(config4):
     assert abs(f_gpu - f_orc) <= TOL * f_orc
 
 
-def stepwise_sampled(p, S, ST, n_steps=None, nsample=96):
+def stepwise_sampled(p, S, ST, n_steps=None, nsample=96, flags=0):
     """Run sweep 0 step by step on the GPU; before each step copy the state to the host and
     let the oracle recompute that step for sampled rows (with their momentum)."""
     ctx = nmd.Context(p.m, p.n, p.r, p.block_m, p.block_n, seed=p.seed, mode=p.mode, eta=p.eta,
-                      momentum=p.momentum)
+                      momentum=p.momentum, flags=flags)
     ctx.set_sparse_csr(p.row_ptr, p.col, p.val)
     rb = partition.bounds(p.m, p.block_m)
     cb = partition.bounds(p.n, p.block_n)
@@ -143,6 +143,14 @@ def test_config4_full_sweep_stepwise_sampled(config4):
     p, S, ST = config4
     _say("config 4 full sweep, every step checked on sampled rows")
     stepwise_sampled(p, S, ST)
+
+
+def test_config4_split_bf16_first_steps_sampled(config4):
+    """The split-bf16 first product on the full graph workload: the first six steps of sweep 0,
+    each checked on sampled rows against the oracle."""
+    p, S, ST = config4
+    _say("config 4 split bf16, first steps checked on sampled rows")
+    stepwise_sampled(p, S, ST, n_steps=6, flags=nmd.FLAG_SPLIT_BF16)
 
 
 def test_config5_first_steps_sampled():
