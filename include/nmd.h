@@ -48,7 +48,8 @@ enum {
                           nmd_reset                                                       */
   NMD_FLAG_TIMING = 2u, /* record HIP events around every kernel class (see
                           nmd_get_kernel_timing); adds a few microseconds per step        */
-  NMD_FLAG_SPLIT_BF16 = 4u /* r_p = 256 only (other ranks ignore it): the first product of
+  NMD_FLAG_SPLIT_BF16 = 4u /* padded rank r_p = 256, i.e. r in 193..256 (other ranks
+                          ignore it): the first product of
                           the dense contraction, L = A B_J^T, runs on bf16 MFMA with every
                           operand split in two (x = bf16(x) + bf16(x - bf16(x)), three
                           products, fp32 accumulation; relative error of L about 2^-16 of
@@ -193,9 +194,9 @@ int nmd_rectified_contraction(const float* A, int64_t rows, const float* B, int6
 /*
  * nmd_rectified_contraction_split - the same product Y = max(0, A B^T) B at r = 256 with the
  * first product on split bf16 MFMA (see NMD_FLAG_SPLIT_BF16).  Bsplit: device workspace of
- * blk x 256 floats that receives the split panel (caller-owned, overwritten).  Padding columns
- * as above.  Asynchronous on hip_stream; allocates nothing.  NMD_EINVAL on NULL pointers, r
- * other than 256 or bad sizes, NMD_EDEVICE if a launch fails.
+ * blk x 256 floats that receives the split panel (caller-owned, overwritten).  Asynchronous on
+ * hip_stream; allocates nothing.  NMD_EINVAL on NULL pointers, r other than 256 or bad sizes,
+ * NMD_EDEVICE if a launch fails.
  */
 int nmd_rectified_contraction_split(const float* A, int64_t rows, const float* B, int64_t blk,
                                     int32_t r, float* Bsplit, float* Y, void* hip_stream);
