@@ -1,0 +1,46 @@
+// Launchers of the rectified contraction with both products on split bf16 MFMA (kernels in
+// dense_bf16.h), at padded ranks 32, 64, 128 and 256.
+
+#include "dense_bf16.h"
+#include "nmd_internal.h"
+
+namespace nmd {
+
+int64_t bf16x3_work_floats(int64_t blk, int rp) { return (blk + (blk + 31) / 32 * 32) * rp; }
+
+template <int RP>
+static hipError_t bx_launch_t(const float* X, int64_t rows, const float* P, int64_t blk,
+                              float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
+                              hipStream_t st) {
+  using C = bx::Cfg<RP>;
+  const int64_t npair = (blk + 31) / 32;
+  float* rowm = work;
+  float* trans = work + blk * RP;
+  const int64_t threads = blk * (RP / 8) + npair * 4 * RP;
+  hipLaunchKernelGGL(bx::bx_split_kernel<RP>, dim3((unsigned)((threads + 255) / 256)), dim3(256),
+                     0, st, P, blk, npair, reinterpret_cast<bx::u32x4*>(rowm),
+                     reinterpret_cast<bx::u32x4*>(trans));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t row_tiles = (rows + C::ROWS - 1) / C::ROWS;
+  const int64_t total = row_tiles * nsplit;
+  if (total <= 0) return hipSuccess;
+  if (total > 0x7fffffffLL) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(bx::bx_kernel<RP>, dim3((unsigned)total), dim3(64 * C::WAVES), 0, st, X, rows,
+                     rowm, trans, blk, Ypart, y_stride, nsplit, row_tiles, sgn);
+  return hipGetLastError();
+}
+
+hipError_t launch_bf16x3(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
+                         float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
+                         hipStream_t st) {
+  switch (rp) {
+    case 32: return bx_launch_t<32>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, st);
+    case 64: return bx_launch_t<64>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, st);
+    case 128: return bx_launch_t<128>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, st);
+    case 256: return bx_launch_t<256>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace nmd

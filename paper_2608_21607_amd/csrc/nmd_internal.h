@@ -51,6 +51,14 @@ hipError_t launch_dense(const float* X, int64_t rows, const float* P, int64_t bl
 // (rows x 256 floats of space); launch_dense_split is launch_dense at r_p = 256 with the first
 // product on bf16 MFMA from that split panel.
 hipError_t launch_split_panel(const float* P, int64_t rows, float* out, hipStream_t st);
+
+// Both products on split bf16 MFMA (dense_bf16.h), rp in {32, 64, 128, 256}: splits the blk x rp
+// panel P into `work` (bf16x3_work_floats(blk, rp) floats: row-major and transposed split
+// copies), then Y_s = sgn * max(0, X P_s^T) P_s for each of nsplit pair-aligned panel ranges.
+int64_t bf16x3_work_floats(int64_t blk, int rp);
+hipError_t launch_bf16x3(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
+                         float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
+                         hipStream_t st);
 hipError_t launch_dense_split(const float* X, int64_t rows, const float* Psplit, int64_t blk,
                               float* Ypart, int64_t y_stride, int nsplit, float sgn,
                               unsigned long long* gemm2_blocks, hipStream_t st);

@@ -67,6 +67,8 @@ def lib() -> C.CDLL:
         "nmd_run_steps": (I32, [P, P, P, P, I32, P]),
         "nmd_rectified_contraction": (I32, [P, I64, P, I64, I32, P, P]),
         "nmd_rectified_contraction_split": (I32, [P, I64, P, I64, I32, P, P, P]),
+        "nmd_rectified_contraction_bf16x3": (I32, [P, I64, P, I64, I32, P, P, P]),
+        "nmd_bf16x3_workspace_floats": (I64, [I64, I32]),
         "nmd_get_dense_blocks": (I32, [P, P, P, P, I32]),
         "nmd_get_kernel_timing": (I32, [P, I32, C.POINTER(C.c_double), C.POINTER(I64),
                                         C.POINTER(C.c_double), C.POINTER(C.c_double), I32]),
@@ -230,6 +232,33 @@ def rectified_contraction(A, B, Y=None, stream=None):
                                            _dev_ptr(B, (blk, r), "B"), int(blk), int(r),
                                            _dev_ptr(Y, (rows, r), "Y"), _stream_handle(stream)),
            None)
+    return Y
+
+
+def bf16x3_workspace_floats(blk, r) -> int:
+    """Floats of workspace rectified_contraction_bf16x3 needs (-1 for an unsupported r)."""
+    return int(lib().nmd_bf16x3_workspace_floats(int(blk), int(r)))
+
+
+def rectified_contraction_bf16x3(A, B, Y=None, work=None, stream=None):
+    """Y = max(0, A B^T) B with both products on split bf16 MFMA (A: rows x r, B: blk x r,
+    float32 CUDA tensors, r in {32, 64, 128, 256}; work: float32 workspace of at least
+    bf16x3_workspace_floats(blk, r) elements)."""
+    import torch
+    rows, r = A.shape
+    blk = B.shape[0]
+    need = bf16x3_workspace_floats(blk, r)
+    if need < 0:
+        raise NmdError(EINVAL, f"the bf16x3 contraction needs r in (32, 64, 128, 256), got {r}")
+    if Y is None:
+        Y = torch.empty((rows, r), dtype=torch.float32, device=A.device)
+    if work is None:
+        work = torch.empty((need,), dtype=torch.float32, device=A.device)
+    if not work.is_cuda or work.dtype != torch.float32 or not work.is_contiguous() or work.numel() < need:
+        raise ValueError(f"work must be a contiguous float32 CUDA tensor of at least {need} elements")
+    _check(lib().nmd_rectified_contraction_bf16x3(
+        _dev_ptr(A, (rows, r), "A"), int(rows), _dev_ptr(B, (blk, r), "B"), int(blk), int(r),
+        C.c_void_p(work.data_ptr()), _dev_ptr(Y, (rows, r), "Y"), _stream_handle(stream)), None)
     return Y
 
 

@@ -139,6 +139,20 @@ def test_rectified_contraction_argument_checks(L):
         assert split(fake, 10, fake, 10, r, fake, fake, None) == nmd.EINVAL
     assert split(fake, 10, fake, 10, 256, None, fake, None) == nmd.EINVAL
     assert split(fake, 0, fake, 10, 256, fake, fake, None) == nmd.EINVAL
+    bx = L.nmd_rectified_contraction_bf16x3
+    for r in (16, 48, 96, 192, 512):  # both-products bf16 contraction: r in 32, 64, 128, 256
+        assert bx(fake, 10, fake, 10, r, fake, fake, None) == nmd.EINVAL
+    assert bx(fake, 10, fake, 10, 64, None, fake, None) == nmd.EINVAL
+    assert bx(fake, 10, fake, 0, 64, fake, fake, None) == nmd.EINVAL
+
+
+def test_bf16x3_workspace_size(L):
+    """(blk + 32 ceil(blk / 32)) r floats: the row-major and the pair-padded transposed copy."""
+    for blk, r in ((1, 32), (31, 64), (32, 64), (33, 128), (2500, 128), (8192, 256)):
+        assert nmd.bf16x3_workspace_floats(blk, r) == (blk + 32 * ((blk + 31) // 32)) * r
+    assert nmd.bf16x3_workspace_floats(0, 64) == -1
+    assert nmd.bf16x3_workspace_floats(10, 16) == -1
+    assert nmd.bf16x3_workspace_floats(10, 512) == -1
 
 
 def test_dense_blocks_before_device_use(L):

@@ -223,6 +223,53 @@ def test_rectified_contraction_split_thin_slices():
     assert e < SPLIT_TOL
 
 
+@pytest.mark.parametrize("r,rows,blk", [(32, 300, 1000), (64, 257, 517), (128, 129, 33),
+                                         (128, 1000, 2500), (256, 340, 517), (64, 5, 7)])
+def test_rectified_contraction_bf16x3(r, rows, blk):
+    """Both products on split bf16: N(0,1) factors (about half of L positive, every 16 x 32
+    tile live), ragged rows and panel sizes (a panel shorter than one 32-row pair included)."""
+    _say("rectified_contraction_bf16x3", rows, blk, r)
+    g = np.random.default_rng(1000 * r + blk)
+    A = g.standard_normal((rows, r)).astype(np.float32)
+    B = g.standard_normal((blk, r)).astype(np.float32)
+    Y = nmd.rectified_contraction_bf16x3(dev(A), dev(B))
+    torch.cuda.synchronize()
+    e = rel(Y.cpu().numpy(), salsa.rectified_contraction(A, B))
+    print(f"bf16x3 r = {r}: rel err {e:.2e}")
+    assert e < SPLIT_TOL
+
+
+@pytest.mark.parametrize("r", [32, 128, 256])
+def test_rectified_contraction_bf16x3_sparse_and_zero(r):
+    """Thin positive slices (most 16 x 32 tiles skipped) and an all-negative L (exact zero)."""
+    rows, blk = 300 + 4, 1000 + 9
+    _say("rectified_contraction_bf16x3 sparse", rows, blk, r)
+    A, B = _thin_positive_case(rows, blk, r, 11 * r + 3)
+    Y = nmd.rectified_contraction_bf16x3(dev(A), dev(B))
+    torch.cuda.synchronize()
+    e = rel(Y.cpu().numpy(), salsa.rectified_contraction(A, B))
+    print(f"bf16x3 thin slices r = {r}: rel err {e:.2e}")
+    assert e < SPLIT_TOL
+    Y0 = nmd.rectified_contraction_bf16x3(dev(np.abs(A)), dev(-np.abs(B)))
+    torch.cuda.synchronize()
+    assert not torch.any(Y0 != 0).item()
+
+
+def test_rectified_contraction_bf16x3_workspace_reuse():
+    """Two calls in a row on one workspace, the second with a shorter panel: the second result
+    depends only on its own inputs."""
+    g = np.random.default_rng(77)
+    r = 64
+    A = g.standard_normal((200, r)).astype(np.float32)
+    B1 = g.standard_normal((700, r)).astype(np.float32)
+    B2 = g.standard_normal((45, r)).astype(np.float32)
+    work = torch.empty((nmd.bf16x3_workspace_floats(700, r),), device="cuda")
+    nmd.rectified_contraction_bf16x3(dev(A), dev(B1), work=work)
+    Y = nmd.rectified_contraction_bf16x3(dev(A), dev(B2), work=work)
+    torch.cuda.synchronize()
+    assert rel(Y.cpu().numpy(), salsa.rectified_contraction(A, B2)) < SPLIT_TOL
+
+
 def test_graph_tenth_two_sweeps_split_bf16():
     """The graph workload at a tenth of its size, two stochastic sweeps with the split-bf16
     first product: W, H and the objective within the 1e-4 bar of the fp64 oracle."""
