@@ -36,13 +36,13 @@ METRIC = "ALS sweeps/sec and dense-equiv TFLOP/s (4mnr/sweep), % of fp32 MFMA pe
 # kernel sources it was taken on.
 TRAFFIC_FILES = {
     "fp32": os.path.join(ROOT, "profiles", "dense_r256_graph139255_traffic.json"),
-    "split_bf16": os.path.join(ROOT, "profiles", "dense_split_r256_graph139255_traffic.json"),
+    "split_bf16": os.path.join(ROOT, "profiles", "bf16x3_r256_graph139255_traffic.json"),
 }
 KERNEL_SOURCES = {
     "fp32": [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f)
              for f in ("tile.h", "dense_kernel.h", "dense.hip")],
     "split_bf16": [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f)
-                   for f in ("tile.h", "dense_kernel.h", "dense_split.h", "dense_split.hip")],
+                   for f in ("tile.h", "dense_kernel.h", "dense_bf16.h", "dense_bf16.hip")],
 }
 
 
@@ -84,7 +84,8 @@ PAPER_FUSED_TF32 = {16: (215.30, 191.72), 32: (283.73, 203.06), 64: (285.10, 206
 def kernel_mb(steps, warmup):
     """The fused rectified contraction Y = max(0, A B^T) B alone at the shape of the paper's
     kernel table: A 250000 x r, B 2500 x r, N(0,1) entries.  About half of L is positive, so
-    every 16 x 4 slice of the second product runs and the work is 4 rows blk r flops."""
+    every slice of the second product runs and the work is 4 rows blk r flops.  Timed for the
+    fp32 kernel and, from r = 32, for the kernel with both products on split bf16 (bf16x3)."""
     import torch
 
     import paper_2608_21607_amd as nmd
@@ -96,25 +97,37 @@ def kernel_mb(steps, warmup):
         A = torch.randn((rows, r), generator=g, device="cuda")
         B = torch.randn((blk, r), generator=g, device="cuda")
         Y = torch.empty((rows, r), device="cuda")
-        for _ in range(warmup):
-            nmd.rectified_contraction(A, B, Y)
-        start = torch.cuda.Event(enable_timing=True)
-        stop = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        start.record()
-        for _ in range(steps):
-            nmd.rectified_contraction(A, B, Y)
-        stop.record()
-        torch.cuda.synchronize()
-        ms = start.elapsed_time(stop) / steps
-        tflops = 4.0 * rows * blk * r / (ms / 1e3) / 1e12
+        runs = [("fp32", lambda: nmd.rectified_contraction(A, B, Y))]
+        if nmd.bf16x3_workspace_floats(blk, r) > 0:
+            work = torch.empty((nmd.bf16x3_workspace_floats(blk, r),), device="cuda")
+            runs.append(("bf16x3", lambda: nmd.rectified_contraction_bf16x3(A, B, Y, work=work)))
+        row = {"r": r}
+        for tag, f in runs:
+            for _ in range(warmup):
+                f()
+            start = torch.cuda.Event(enable_timing=True)
+            stop = torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            start.record()
+            for _ in range(steps):
+                f()
+            stop.record()
+            torch.cuda.synchronize()
+            ms = start.elapsed_time(stop) / steps
+            tflops = 4.0 * rows * blk * r / (ms / 1e3) / 1e12
+            if tag == "fp32":
+                row.update({"ms_per_launch": ms, "tflops": tflops,
+                            "frac_of_fp32_peak": tflops / PEAK_FP32_MFMA})
+            else:
+                row.update({"bf16x3_ms_per_launch": ms, "bf16x3_tflops": tflops,
+                            "bf16x3_frac_of_peak": tflops / (PEAK_BF16_MFMA / 3.0)})
+            log(f"r = {r} {tag}: {ms:.3f} ms per launch, {tflops:.1f} TFLOP/s")
         h100, rtx = PAPER_FUSED_TF32[r]
-        res.append({"r": r, "ms_per_launch": ms, "tflops": tflops,
-                    "frac_of_fp32_peak": tflops / PEAK_FP32_MFMA,
-                    "paper_tf32_h100_pcie": h100, "paper_tf32_rtx_pro_6000": rtx})
-        log(f"r = {r}: {ms:.3f} ms per launch, {tflops:.1f} TFLOP/s")
+        row.update({"paper_tf32_h100_pcie": h100, "paper_tf32_rtx_pro_6000": rtx})
+        res.append(row)
     return {"metric": "fused rectified contraction TFLOP/s (4 rows blk r per launch)",
-            "unit": "TFLOP/s", "dtype": "f32", "data": "synthetic",
+            "unit": "TFLOP/s", "dtype": "f32; bf16x3 split for the bf16x3 columns",
+            "data": "synthetic",
             "config": {"workload": "kernel alone, A 250000 x r, B 2500 x r, N(0,1)"},
             "steps": steps, "warmup": warmup, "results": res}
 
@@ -176,8 +189,8 @@ def main():
     ap.add_argument("--kernel-mb", action="store_true",
                     help="time the fused kernel alone at the shape of the paper's kernel table")
     ap.add_argument("--split-bf16", action="store_true",
-                    help="opt-in r = 256 variant: first product of the dense kernel as three "
-                         "bf16 MFMA products of a two-term split (fp32 stays the default)")
+                    help="opt-in variant at r_p = 256: both products of the dense kernel as "
+                         "three bf16 MFMA products of two-term splits (fp32 stays the default)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first run one plain 1 GiB copy kernel (calibrates rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -260,15 +273,9 @@ def main():
     dense_equiv_kernel = dense["flops"] / dense_s / 1e12 if dense_s > 0 else 0.0
     sparse_gbs = sparse["bytes"] / (sparse["ms"] / 1e3) / 1e9 if sparse["ms"] > 0 else 0.0
     split = args.split_bf16 and rp == 256
-    if split:
-        # The split variant runs the first product as three bf16 products at the bf16 peak and
-        # the second on fp32 MFMA: the roofline is the time those would take at their peaks,
-        # stated as the equivalent rate for the kernel's algorithmic flops.
-        f1 = 0.5 * dense["flops"]
-        f2 = dense_alg_flops - f1
-        peak = dense_alg_flops / (3.0 * f1 / PEAK_BF16_MFMA + f2 / PEAK_FP32_MFMA)
-    else:
-        peak = PEAK_FP32_MFMA
+    # The split option runs both products as three bf16 products each: every algorithmic flop
+    # costs three bf16 flops, so its roofline peak is a third of the bf16 MFMA peak.
+    peak = PEAK_BF16_MFMA / 3.0 if split else PEAK_FP32_MFMA
 
     out = {
         "metric": METRIC,
@@ -311,7 +318,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": dense_tflops / peak,
             "traffic": measured_traffic(args.config, "split_bf16" if split else "fp32"),
-            "kernel": "dense_split_kernel" if split else f"dense_kernel<{rp}>",
+            "kernel": "bx_kernel<256>" if split else f"dense_kernel<{rp}>",
             "launches": dense["launches"],
             "avg_launch_ms": dense["ms"] / max(1, dense["launches"]),
             "flops_per_launch": dense_alg_flops / max(1, dense["launches"]),

@@ -49,13 +49,15 @@ enum {
   NMD_FLAG_TIMING = 2u, /* record HIP events around every kernel class (see
                           nmd_get_kernel_timing); adds a few microseconds per step        */
   NMD_FLAG_SPLIT_BF16 = 4u /* padded rank r_p = 256, i.e. r in 193..256 (other ranks
-                          ignore it): the first product of
-                          the dense contraction, L = A B_J^T, runs on bf16 MFMA with every
+                          ignore it): both products of the dense contraction,
+                          L = A B_J^T and max(0, L) B_J, run on bf16 MFMA with every
                           operand split in two (x = bf16(x) + bf16(x - bf16(x)), three
-                          products, fp32 accumulation; relative error of L about 2^-16 of
-                          sum |a_k b_k|) instead of fp32 MFMA, the counterpart of the
-                          paper's TF32 kernels (Sec. 4.2).  Everything else stays fp32.
-                          Needs (max(m, n) x 256) floats more device memory                */
+                          products each, fp32 accumulation; relative error about 2^-16 of
+                          the sum of the magnitudes of the terms) instead of fp32 MFMA, the
+                          counterpart of the paper's TF32 kernels (Sec. 4.2); the kernel of
+                          nmd_rectified_contraction_bf16x3.  Everything else stays fp32.
+                          Needs nmd_bf16x3_workspace_floats(max(m, n), 256) floats more
+                          device memory                                                     */
 };
 
 typedef struct {
@@ -190,16 +192,6 @@ int nmd_run_steps(nmd_ctx* ctx, float* W, float* H, const int32_t* steps, int32_
  */
 int nmd_rectified_contraction(const float* A, int64_t rows, const float* B, int64_t blk,
                               int32_t r, float* Y, void* hip_stream);
-
-/*
- * nmd_rectified_contraction_split - the same product Y = max(0, A B^T) B at r = 256 with the
- * first product on split bf16 MFMA (see NMD_FLAG_SPLIT_BF16).  Bsplit: device workspace of
- * blk x 256 floats that receives the split panel (caller-owned, overwritten).  Asynchronous on
- * hip_stream; allocates nothing.  NMD_EINVAL on NULL pointers, r other than 256 or bad sizes,
- * NMD_EDEVICE if a launch fails.
- */
-int nmd_rectified_contraction_split(const float* A, int64_t rows, const float* B, int64_t blk,
-                                    int32_t r, float* Bsplit, float* Y, void* hip_stream);
 
 /*
  * nmd_rectified_contraction_bf16x3 - the same product Y = max(0, A B^T) B with BOTH products on

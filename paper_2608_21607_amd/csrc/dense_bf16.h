@@ -164,14 +164,15 @@ __device__ __forceinline__ void stage(float* dst, const float* __restrict__ rowm
                                      (lds_void*)(tdst + 256 * i), 16, 0, 0);
 }
 
-// Both products over the pairs of one staged tile.
+// Both products over the pairs of one staged tile; returns the pairs whose second product ran.
 template <int RP>
-__device__ __forceinline__ void consume(const float* tile, int np, const u32x4 (&xh)[RP / 32],
-                                        const u32x4 (&xl)[RP / 32], floatx4 (&y)[RP / 16], int q,
-                                        int l16) {
+__device__ __forceinline__ unsigned consume(const float* tile, int np, const u32x4 (&xh)[RP / 32],
+                                            const u32x4 (&xl)[RP / 32], floatx4 (&y)[RP / 16],
+                                            int q, int l16) {
   using C = Cfg<RP>;
   constexpr int KC = RP / 32, CB = RP / 16, G = C::G;
   const float* trans = tile + C::NT * C::LS;
+  unsigned ran = 0;
   for (int jp = 0; jp < np; ++jp) {
     const u32x4* r0 = reinterpret_cast<const u32x4*>(tile + (32 * jp + l16) * C::LS);
     const u32x4* r1 = reinterpret_cast<const u32x4*>(tile + (32 * jp + 16 + l16) * C::LS);
@@ -211,6 +212,7 @@ __device__ __forceinline__ void consume(const float* tile, int np, const u32x4 (
                         l1[2] > 0.f ? l1[2] : 0.f, l1[3] > 0.f ? l1[3] : 0.f};
     const bool pos = z[0] + z[1] + z[2] + z[3] + z[4] + z[5] + z[6] + z[7] > 0.f;
     if (!__ballot(pos)) continue;  // max(0, L) is zero on the whole 16 x 32 tile
+    ++ran;
     u32x4 zh, zl;
     split8(z, zh, zl);
     const u32x4* bh = reinterpret_cast<const u32x4*>(trans + jp * C::TB) + (2 * q) * RP + l16;
@@ -245,13 +247,14 @@ __device__ __forceinline__ void consume(const float* tile, int np, const u32x4 (
       __builtin_amdgcn_sched_barrier(0);
     }
   }
+  return ran;
 }
 
 // One pipeline step: start the loads of the next tile into `nxt` (when not null) and consume
 // `cur`.  The restrict qualifiers let the compiler keep the reads of `cur` from waiting on the
 // direct loads into `nxt`.
 template <int RP>
-__device__ __forceinline__ void step(const float* __restrict__ cur, float* __restrict__ nxt,
+__device__ __forceinline__ unsigned step(const float* __restrict__ cur, float* __restrict__ nxt,
                                      const float* __restrict__ rowm,
                                      const float* __restrict__ trans, int64_t j0, int64_t jb1,
                                      const u32x4 (&xh)[RP / 32], const u32x4 (&xl)[RP / 32],
@@ -259,11 +262,11 @@ __device__ __forceinline__ void step(const float* __restrict__ cur, float* __res
   constexpr int NT = Cfg<RP>::NT;
   if (nxt) stage<RP>(nxt, rowm, trans, j0 + NT, jb1, wave, lane);
   const int64_t left = (jb1 - j0 + 31) / 32;
-  consume<RP>(cur, left < NT / 32 ? (int)left : NT / 32, xh, xl, y, q, l16);
+  return consume<RP>(cur, left < NT / 32 ? (int)left : NT / 32, xh, xl, y, q, l16);
 }
 
 // Panel rows of split s: [start(s), start(s + 1)), starts rounded down to whole pairs.
-__device__ __forceinline__ int64_t pair_start(int s, int nsplit, int64_t blk) {
+__host__ __device__ __forceinline__ int64_t pair_start(int s, int nsplit, int64_t blk) {
   return s >= nsplit ? blk : ((int64_t)s * blk / nsplit) / 32 * 32;
 }
 
@@ -271,7 +274,7 @@ template <int RP>
 __global__ __launch_bounds__(64 * Cfg<RP>::WAVES) void bx_kernel(
     const float* __restrict__ X, int64_t rows, const float* __restrict__ rowm,
     const float* __restrict__ trans, int64_t blk, float* __restrict__ Ypart, int64_t y_stride,
-    int nsplit, int64_t row_tiles, float sgn) {
+    int nsplit, int64_t row_tiles, float sgn, unsigned long long* __restrict__ live_slices) {
   using C = Cfg<RP>;
   constexpr int CB = RP / 16;
   __shared__ __attribute__((aligned(16))) float smem[2 * C::TILE];
@@ -295,10 +298,11 @@ __global__ __launch_bounds__(64 * Cfg<RP>::WAVES) void bx_kernel(
 
   if (jb0 < jb1) stage<RP>(smem, rowm, trans, jb0, jb1, wave, lane);
   int cur = 0;
+  unsigned ran = 0;
   for (int64_t j0 = jb0; j0 < jb1; j0 += C::NT, cur ^= 1) {
     __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the tile have landed
     __syncthreads();                // every wave's have; the other buffer is free again
-    step<RP>(smem + cur * C::TILE, j0 + C::NT < jb1 ? smem + (cur ^ 1) * C::TILE : nullptr, rowm,
+    ran += step<RP>(smem + cur * C::TILE, j0 + C::NT < jb1 ? smem + (cur ^ 1) * C::TILE : nullptr, rowm,
              trans, j0, jb1, xh, xl, y, wave, lane, q, l16);
   }
 
@@ -311,6 +315,8 @@ __global__ __launch_bounds__(64 * Cfg<RP>::WAVES) void bx_kernel(
       for (int cb = 0; cb < CB; ++cb) Y[row * RP + 16 * cb + l16] = sgn * y[cb][v];
     }
   }
+  // a live 16 x 32 tile counts as its eight 16 x 4 slices of max(0, L)
+  if (live_slices && lane == 0 && ran) atomicAdd(live_slices, 8ull * ran);
 }
 
 }  // namespace bx

@@ -11,7 +11,7 @@ int64_t bf16x3_work_floats(int64_t blk, int rp) { return (blk + (blk + 31) / 32 
 template <int RP>
 static hipError_t bx_launch_t(const float* X, int64_t rows, const float* P, int64_t blk,
                               float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
-                              hipStream_t st) {
+                              unsigned long long* live, hipStream_t st) {
   using C = bx::Cfg<RP>;
   const int64_t npair = (blk + 31) / 32;
   float* rowm = work;
@@ -27,20 +27,24 @@ static hipError_t bx_launch_t(const float* X, int64_t rows, const float* P, int6
   if (total <= 0) return hipSuccess;
   if (total > 0x7fffffffLL) return hipErrorInvalidValue;
   hipLaunchKernelGGL(bx::bx_kernel<RP>, dim3((unsigned)total), dim3(64 * C::WAVES), 0, st, X, rows,
-                     rowm, trans, blk, Ypart, y_stride, nsplit, row_tiles, sgn);
+                     rowm, trans, blk, Ypart, y_stride, nsplit, row_tiles, sgn, live);
   return hipGetLastError();
 }
 
 hipError_t launch_bf16x3(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
                          float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
-                         hipStream_t st) {
+                         unsigned long long* live, hipStream_t st) {
+#define BX(R) bx_launch_t<R>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, live, st)
   switch (rp) {
-    case 32: return bx_launch_t<32>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, st);
-    case 64: return bx_launch_t<64>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, st);
-    case 128: return bx_launch_t<128>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, st);
-    case 256: return bx_launch_t<256>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, st);
+    case 32: return BX(32);
+    case 64: return BX(64);
+    case 128: return BX(128);
+    case 256: return BX(256);
   }
+#undef BX
   return hipErrorInvalidValue;
 }
+
+int64_t bf16x3_pair_start(int s, int nsplit, int64_t blk) { return bx::pair_start(s, nsplit, blk); }
 
 }  // namespace nmd

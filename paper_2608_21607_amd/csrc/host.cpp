@@ -20,6 +20,7 @@
 #include "../../include/nmd.h"
 #include "nmd_internal.h"
 
+
 using nmd::Item;
 using nmd::Split;
 
@@ -232,7 +233,7 @@ struct nmd_ctx {
   float *A2 = nullptr, *B2 = nullptr, *VA2 = nullptr, *VB2 = nullptr;
   std::vector<std::pair<int, bool>> enqueued;  // (step id, W-step) of the call's steps, in order
   float* Ypart = nullptr;
-  float* Psplit = nullptr;  // split-bf16 panel (NMD_FLAG_SPLIT_BF16 at r_p = 256), max(m, n) x 256
+  float* Pbx = nullptr;  // split-bf16 panel copies (NMD_FLAG_SPLIT_BF16 at r_p = 256)
   int64_t ypart_floats = 0;
   float* scratch = nullptr;
   int64_t scratch_floats = 0;
@@ -322,7 +323,7 @@ void free_device(nmd_ctx* c) {
   dfree(c->VA2);
   dfree(c->VB2);
   dfree(c->Ypart);
-  dfree(c->Psplit);
+  dfree(c->Pbx);
   dfree(c->G);
   dfree(c->Gtmp);
   dfree(c->Gpart);
@@ -416,9 +417,11 @@ int ensure_device(nmd_ctx* c) {
     need = std::max(need, nsplit_for(c->m, c->n, c->rp, c->dense_slots) * c->m);
     need = std::max(need, nsplit_for(c->n, c->m, c->rp, c->dense_slots) * c->n);
     c->ypart_floats = need * rp;
+    // the split-bf16 option runs at r_p = 256 (at the smaller ranks of the workloads here the
+    // steps are too small for it to pay; the standalone contraction offers it from r_p = 32)
+    const bool bx = (c->opt.flags & NMD_FLAG_SPLIT_BF16) && rp == 256;
     if (dalloc(&c->Ypart, c->ypart_floats) != hipSuccess ||
-        ((c->opt.flags & NMD_FLAG_SPLIT_BF16) && rp == 256 &&
-         dalloc(&c->Psplit, std::max(c->m, c->n) * 256) != hipSuccess)) {
+        (bx && dalloc(&c->Pbx, nmd::bf16x3_work_floats(std::max(c->m, c->n), rp)) != hipSuccess)) {
       free_device(c);
       return fail(c, NMD_ENOMEM, "device allocation of %lld partial-output floats failed",
                   (long long)c->ypart_floats);
@@ -584,17 +587,19 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
     // U = Delta_{:J} P_J starts as -max(0, X P_J^T) P_J (eq. updateD off the nonzeros); the
     // second contraction is skipped on the 16 x 4 slices where that rectified tile is zero
     Scope sc(c, st, K_DENSE, 4.0 * rows * (double)blk * c->r, 4.0 * (2.0 * rows + blk) * c->r);
-    if (c->Psplit) {  // split-bf16 first product: the panel is split once per step
-      HIP_TRY(c, nmd::launch_split_panel(PJ, blk, c->Psplit, st));
-      HIP_TRY(c, nmd::launch_dense_split(X, rows, c->Psplit, blk, c->Ypart, y_stride, (int)ns,
-                                         -1.0f, c->g2, st));
+    int64_t jblocks = 0;  // 16-row panel blocks the launch examines
+    if (c->Pbx) {  // both products on split bf16: the panel is split once per step
+      HIP_TRY(c, nmd::launch_bf16x3(X, rows, PJ, blk, rp, c->Pbx, c->Ypart, y_stride, (int)ns,
+                                    -1.0f, c->g2, st));
+      for (int s = 0; s < (int)ns; ++s)
+        jblocks += 2 * ((nmd::bf16x3_pair_start(s + 1, (int)ns, blk) -
+                         nmd::bf16x3_pair_start(s, (int)ns, blk) + 31) / 32);
     } else {
       HIP_TRY(c, nmd::launch_dense(X, rows, PJ, blk, rp, c->Ypart, y_stride, (int)ns, -1.0f,
                                    c->g2, st));
+      for (int64_t s = 0; s < ns; ++s) jblocks += ((s + 1) * blk / ns - s * blk / ns + 15) / 16;
     }
     // slices of 16 rows x 4 panel rows examined (those entirely past the last row never run)
-    int64_t jblocks = 0;
-    for (int64_t s = 0; s < ns; ++s) jblocks += ((s + 1) * blk / ns - s * blk / ns + 15) / 16;
     c->g2_total += (rows + 15) / 16 * jblocks * 4;
   }
   // Sparse correction at the nonzeros (eq. updateD there: s - l = (s - min(0, l)) - max(0, l)),
@@ -1015,21 +1020,6 @@ int nmd_rectified_contraction(const float* A, int64_t rows, const float* B, int6
   return NMD_OK;
 }
 
-int nmd_rectified_contraction_split(const float* A, int64_t rows, const float* B, int64_t blk,
-                                    int32_t r, float* Bsplit, float* Y, void* hip_stream) {
-  g_create_error.clear();
-  if (!A || !B || !Bsplit || !Y)
-    return fail(nullptr, NMD_EINVAL, "A, B, Bsplit and Y must be non-NULL");
-  if (rows < 1 || blk < 1 || rows > INT32_MAX)
-    return fail(nullptr, NMD_EINVAL, "rows and blk must be >= 1");
-  if (r != 256) return fail(nullptr, NMD_EINVAL, "the split-bf16 contraction needs r = 256 (got %d)", r);
-  hipStream_t st = (hipStream_t)hip_stream;
-  hipError_t e = nmd::launch_split_panel(B, blk, Bsplit, st);
-  if (e == hipSuccess) e = nmd::launch_dense_split(A, rows, Bsplit, blk, Y, 0, 1, 1.0f, nullptr, st);
-  if (e != hipSuccess) return fail(nullptr, NMD_EDEVICE, "launch failed: %s", hipGetErrorString(e));
-  return NMD_OK;
-}
-
 int64_t nmd_bf16x3_workspace_floats(int64_t blk, int32_t r) {
   if (blk < 1 || (r != 32 && r != 64 && r != 128 && r != 256)) return -1;
   return nmd::bf16x3_work_floats(blk, r);
@@ -1044,7 +1034,8 @@ int nmd_rectified_contraction_bf16x3(const float* A, int64_t rows, const float* 
     return fail(nullptr, NMD_EINVAL, "rows and blk must be >= 1");
   if (r != 32 && r != 64 && r != 128 && r != 256)
     return fail(nullptr, NMD_EINVAL, "the bf16x3 contraction needs r in {32, 64, 128, 256} (got %d)", r);
-  hipError_t e = nmd::launch_bf16x3(A, rows, B, blk, r, work, Y, 0, 1, 1.0f, (hipStream_t)hip_stream);
+  hipError_t e = nmd::launch_bf16x3(A, rows, B, blk, r, work, Y, 0, 1, 1.0f, nullptr,
+                                    (hipStream_t)hip_stream);
   if (e != hipSuccess) return fail(nullptr, NMD_EDEVICE, "launch failed: %s", hipGetErrorString(e));
   return NMD_OK;
 }

@@ -46,22 +46,16 @@ hipError_t launch_dense(const float* X, int64_t rows, const float* P, int64_t bl
                         float* Ypart, int64_t y_stride, int nsplit, float sgn,
                         unsigned long long* gemm2_blocks, hipStream_t st);
 
-// Split-bf16 first product (r_p = 256 only): launch_split_panel writes the rows x 256 panel
-// P as rows of 1 KB (32 groups of 8 bf16 hi then 8 bf16 lo, x = hi + lo + O(2^-17 x)) to out
-// (rows x 256 floats of space); launch_dense_split is launch_dense at r_p = 256 with the first
-// product on bf16 MFMA from that split panel.
-hipError_t launch_split_panel(const float* P, int64_t rows, float* out, hipStream_t st);
-
 // Both products on split bf16 MFMA (dense_bf16.h), rp in {32, 64, 128, 256}: splits the blk x rp
 // panel P into `work` (bf16x3_work_floats(blk, rp) floats: row-major and transposed split
-// copies), then Y_s = sgn * max(0, X P_s^T) P_s for each of nsplit pair-aligned panel ranges.
+// copies), then Y_s = sgn * max(0, X P_s^T) P_s for each of nsplit panel ranges starting at
+// bf16x3_pair_start(s, nsplit, blk) (whole 32-row pairs).  When `live` is not NULL, 8 per
+// 16 x 32 tile of max(0, L) with a positive entry is added to it (its 16 x 4 slices).
 int64_t bf16x3_work_floats(int64_t blk, int rp);
+int64_t bf16x3_pair_start(int s, int nsplit, int64_t blk);
 hipError_t launch_bf16x3(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
                          float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
-                         hipStream_t st);
-hipError_t launch_dense_split(const float* X, int64_t rows, const float* Psplit, int64_t blk,
-                              float* Ypart, int64_t y_stride, int nsplit, float sgn,
-                              unsigned long long* gemm2_blocks, hipStream_t st);
+                         unsigned long long* live, hipStream_t st);
 
 // Sparse correction: for every item, c = sum over its entries of (s - min(0, x_row . p_j)) p_j;
 // a row with a single item gets Y[row] = c (accumulate = 0) or Y[row] += c (accumulate = 1);

@@ -66,7 +66,6 @@ def lib() -> C.CDLL:
         "nmd_get_sweep_count": (I32, [P, C.POINTER(I64)]),
         "nmd_run_steps": (I32, [P, P, P, P, I32, P]),
         "nmd_rectified_contraction": (I32, [P, I64, P, I64, I32, P, P]),
-        "nmd_rectified_contraction_split": (I32, [P, I64, P, I64, I32, P, P, P]),
         "nmd_rectified_contraction_bf16x3": (I32, [P, I64, P, I64, I32, P, P, P]),
         "nmd_bf16x3_workspace_floats": (I64, [I64, I32]),
         "nmd_get_dense_blocks": (I32, [P, P, P, P, I32]),
@@ -259,21 +258,4 @@ def rectified_contraction_bf16x3(A, B, Y=None, work=None, stream=None):
     _check(lib().nmd_rectified_contraction_bf16x3(
         _dev_ptr(A, (rows, r), "A"), int(rows), _dev_ptr(B, (blk, r), "B"), int(blk), int(r),
         C.c_void_p(work.data_ptr()), _dev_ptr(Y, (rows, r), "Y"), _stream_handle(stream)), None)
-    return Y
-
-
-def rectified_contraction_split(A, B, Y=None, work=None, stream=None):
-    """Y = max(0, A B^T) B at r = 256 with the first product on split bf16 MFMA (A: rows x 256,
-    B: blk x 256, float32 CUDA tensors; work: blk x 256 float32 workspace for the split panel)."""
-    import torch
-    rows, r = A.shape
-    blk = B.shape[0]
-    if Y is None:
-        Y = torch.empty((rows, r), dtype=torch.float32, device=A.device)
-    if work is None:
-        work = torch.empty((blk, r), dtype=torch.float32, device=A.device)
-    _check(lib().nmd_rectified_contraction_split(
-        _dev_ptr(A, (rows, r), "A"), int(rows), _dev_ptr(B, (blk, r), "B"), int(blk), int(r),
-        _dev_ptr(work, (blk, r), "work"), _dev_ptr(Y, (rows, r), "Y"), _stream_handle(stream)),
-        None)
     return Y

@@ -134,11 +134,6 @@ def test_rectified_contraction_argument_checks(L):
     assert L.nmd_rectified_contraction(fake, 0, fake, 10, 16, fake, None) == nmd.EINVAL
     assert L.nmd_rectified_contraction(fake, 10, fake, 0, 16, fake, None) == nmd.EINVAL
     assert L.nmd_rectified_contraction(None, 10, fake, 10, 16, fake, None) == nmd.EINVAL
-    split = L.nmd_rectified_contraction_split
-    for r in (16, 128, 255, 512):  # the split-bf16 contraction is for r = 256 only
-        assert split(fake, 10, fake, 10, r, fake, fake, None) == nmd.EINVAL
-    assert split(fake, 10, fake, 10, 256, None, fake, None) == nmd.EINVAL
-    assert split(fake, 0, fake, 10, 256, fake, fake, None) == nmd.EINVAL
     bx = L.nmd_rectified_contraction_bf16x3
     for r in (16, 48, 96, 192, 512):  # both-products bf16 contraction: r in 32, 64, 128, 256
         assert bx(fake, 10, fake, 10, r, fake, fake, None) == nmd.EINVAL

@@ -146,8 +146,8 @@ def test_config4_full_sweep_stepwise_sampled(config4):
 
 
 def test_config4_split_bf16_first_steps_sampled(config4):
-    """The split-bf16 first product on the full graph workload: the first six steps of sweep 0,
-    each checked on sampled rows against the oracle."""
+    """The split-bf16 option (both products of the dense term on split bf16) on the full graph
+    workload: the first six steps of sweep 0, each checked on sampled rows against the oracle."""
     p, S, ST = config4
     _say("config 4 split bf16, first steps checked on sampled rows")
     stepwise_sampled(p, S, ST, n_steps=6, flags=nmd.FLAG_SPLIT_BF16)
