@@ -44,21 +44,23 @@ struct Cfg {
   static_assert(RP % 32 == 0 && NT % 32 == 0 && NT % WAVES == 0, "shape");
 };
 
-__device__ __forceinline__ unsigned bf16_rne(float x) {
-  const unsigned u = __float_as_uint(x);
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(2))) float floatx2;
+
+// Two values rounded to bf16 (nearest even), packed: element 0 in the low half.
+__device__ __forceinline__ unsigned bf16_pair(floatx2 x) {
+  return __builtin_bit_cast(unsigned, __builtin_convertvector(x, bf16x2));
 }
-__device__ __forceinline__ float bf16_float(unsigned h) { return __uint_as_float(h << 16); }
 
 // Eight values as packed hi and lo operands (element e in bits 16 (e % 2) of word e / 2).
 __device__ __forceinline__ void split8(const float (&x)[8], u32x4& hi, u32x4& lo) {
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
-    const unsigned h0 = bf16_rne(x[2 * w]), h1 = bf16_rne(x[2 * w + 1]);
-    const unsigned l0 = bf16_rne(x[2 * w] - bf16_float(h0));
-    const unsigned l1 = bf16_rne(x[2 * w + 1] - bf16_float(h1));
-    hi[w] = h0 | (h1 << 16);
-    lo[w] = l0 | (l1 << 16);
+    const floatx2 v = {x[2 * w], x[2 * w + 1]};
+    const unsigned h = bf16_pair(v);
+    const floatx2 hv = {__uint_as_float(h << 16), __uint_as_float(h & 0xffff0000u)};
+    hi[w] = h;
+    lo[w] = bf16_pair(v - hv);
   }
 }
 
@@ -130,11 +132,10 @@ __device__ __forceinline__ void load_x(u32x4 (&xh)[RP / 32], u32x4 (&xl)[RP / 32
 
 // Load panel rows j0 .. j0 + NT - 1 into one buffer: the row-major rows (padded stride, rows at
 // or past jb1 zero-filled) and the transposed blocks of the pairs that hold rows below jb1.
-template <int RP>
-__device__ __forceinline__ void stage(float* dst, const float* __restrict__ rowm,
-                                      const float* __restrict__ trans, int64_t j0, int64_t jb1,
-                                      int wave, int lane) {
-  using C = Cfg<RP>;
+template <int RP, class C>
+__device__ __forceinline__ void stage_t(float* dst, const float* __restrict__ rowm,
+                                        const float* __restrict__ trans, int64_t j0, int64_t jb1,
+                                        int wave, int lane) {
   constexpr int CPR = RP / 4;              // 16-byte chunks per row
   constexpr int IPR = (CPR + 63) / 64;     // instructions per row
 #pragma unroll
@@ -164,88 +165,149 @@ __device__ __forceinline__ void stage(float* dst, const float* __restrict__ rowm
                                      (lds_void*)(tdst + 256 * i), 16, 0, 0);
 }
 
-// Both products over the pairs of one staged tile; returns the pairs whose second product ran.
+template <int RP>
+__device__ __forceinline__ void stage(float* dst, const float* __restrict__ rowm,
+                                      const float* __restrict__ trans, int64_t j0, int64_t jb1,
+                                      int wave, int lane) {
+  stage_t<RP, Cfg<RP>>(dst, rowm, trans, j0, jb1, wave, lane);
+}
+
+template <int RP>
+struct Cfg32;
+
+template <int RP>
+__device__ __forceinline__ void stage32(float* dst, const float* __restrict__ rowm,
+                                        const float* __restrict__ trans, int64_t j0, int64_t jb1,
+                                        int wave, int lane) {
+  stage_t<RP, Cfg32<RP>>(dst, rowm, trans, j0, jb1, wave, lane);
+}
+
+// First product of pair jp: the two 16 x 16 L^T tiles (six accumulator chains, panel reads two
+// chunks ahead).
+template <int RP>
+__device__ __forceinline__ void gemm1_pair(floatx4& l0, floatx4& l1, const float* tile, int jp,
+                                           const u32x4 (&xh)[RP / 32],
+                                           const u32x4 (&xl)[RP / 32], int q, int l16) {
+  using C = Cfg<RP>;
+  constexpr int KC = RP / 32;
+  constexpr int LA = KC < 2 ? KC : 2;
+  const u32x4* r0 = reinterpret_cast<const u32x4*>(tile + (32 * jp + l16) * C::LS);
+  const u32x4* r1 = reinterpret_cast<const u32x4*>(tile + (32 * jp + 16 + l16) * C::LS);
+  floatx4 a0[3], a1[3];
+#pragma unroll
+  for (int h = 0; h < 3; ++h) a0[h] = a1[h] = floatx4{0.f, 0.f, 0.f, 0.f};
+  u32x4 h0[KC], o0[KC], h1[KC], o1[KC];
+#pragma unroll
+  for (int t = 0; t < LA; ++t) {
+    h0[t] = r0[2 * (4 * t + q)];
+    o0[t] = r0[2 * (4 * t + q) + 1];
+    h1[t] = r1[2 * (4 * t + q)];
+    o1[t] = r1[2 * (4 * t + q) + 1];
+  }
+#pragma unroll
+  for (int t = 0; t < KC; ++t) {
+    if (t + LA < KC) {
+      h0[t + LA] = r0[2 * (4 * (t + LA) + q)];
+      o0[t + LA] = r0[2 * (4 * (t + LA) + q) + 1];
+      h1[t + LA] = r1[2 * (4 * (t + LA) + q)];
+      o1[t + LA] = r1[2 * (4 * (t + LA) + q) + 1];
+    }
+    a0[0] = mfma(h0[t], xh[t], a0[0]);
+    a1[0] = mfma(h1[t], xh[t], a1[0]);
+    a0[1] = mfma(h0[t], xl[t], a0[1]);
+    a1[1] = mfma(h1[t], xl[t], a1[1]);
+    a0[2] = mfma(o0[t], xh[t], a0[2]);
+    a1[2] = mfma(o1[t], xh[t], a1[2]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  l0 = a0[0] + (a0[1] + a0[2]);
+  l1 = a1[0] + (a1[1] + a1[2]);
+}
+
+// The rectified pair tile as the second product's split srcA operands; whether any of it is
+// positive (wave-uniform).
+__device__ __forceinline__ bool zsplit(floatx4 l0, floatx4 l1, u32x4& zh, u32x4& zl) {
+  const float z[8] = {l0[0] > 0.f ? l0[0] : 0.f, l0[1] > 0.f ? l0[1] : 0.f,
+                      l0[2] > 0.f ? l0[2] : 0.f, l0[3] > 0.f ? l0[3] : 0.f,
+                      l1[0] > 0.f ? l1[0] : 0.f, l1[1] > 0.f ? l1[1] : 0.f,
+                      l1[2] > 0.f ? l1[2] : 0.f, l1[3] > 0.f ? l1[3] : 0.f};
+  split8(z, zh, zl);
+  const bool pos = z[0] + z[1] + z[2] + z[3] + z[4] + z[5] + z[6] + z[7] > 0.f;
+  return __ballot(pos) != 0;
+}
+
+// Second product of pair jp with operands (zh, zl); the rectify and split of the next pair's
+// tile (m0, m1) is placed after the first group of MFMAs, so that its vector work issues while
+// they run.
+template <int RP>
+__device__ __forceinline__ bool gemm2_pair(floatx4 (&y)[RP / 16], const float* trans, int jp,
+                                           u32x4 zh, u32x4 zl, floatx4 m0, floatx4 m1,
+                                           u32x4& nzh, u32x4& nzl, int q, int l16) {
+  using C = Cfg<RP>;
+  constexpr int CB = RP / 16, G = C::G;
+  const u32x4* bh = reinterpret_cast<const u32x4*>(trans + jp * C::TB) + (2 * q) * RP + l16;
+  const u32x4* bl = bh + RP;
+  u32x4 nh[G], nl[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    nh[g] = bh[16 * g];
+    nl[g] = bl[16 * g];
+  }
+  bool live = false;
+#pragma unroll
+  for (int cb0 = 0; cb0 < CB; cb0 += G) {
+    u32x4 ch[G], cl[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      ch[g] = nh[g];
+      cl[g] = nl[g];
+    }
+    if (cb0 + G < CB) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        nh[g] = bh[16 * (cb0 + G + g)];
+        nl[g] = bl[16 * (cb0 + G + g)];
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) y[cb0 + g] = mfma(zh, ch[g], y[cb0 + g]);
+#pragma unroll
+    for (int g = 0; g < G; ++g) y[cb0 + g] = mfma(zh, cl[g], y[cb0 + g]);
+#pragma unroll
+    for (int g = 0; g < G; ++g) y[cb0 + g] = mfma(zl, ch[g], y[cb0 + g]);
+    if (cb0 == 0) live = zsplit(m0, m1, nzh, nzl);
+  }
+  return live;
+}
+
+// Both products over the pairs of one staged tile, software-pipelined: the first product of pair
+// jp + 1 is issued before the second product of pair jp, whose MFMAs then cover the rectify and
+// split of pair jp + 1.  Returns the pairs whose second product ran.
 template <int RP>
 __device__ __forceinline__ unsigned consume(const float* tile, int np, const u32x4 (&xh)[RP / 32],
                                             const u32x4 (&xl)[RP / 32], floatx4 (&y)[RP / 16],
                                             int q, int l16) {
   using C = Cfg<RP>;
-  constexpr int KC = RP / 32, CB = RP / 16, G = C::G;
   const float* trans = tile + C::NT * C::LS;
   unsigned ran = 0;
+  floatx4 l0, l1;
+  gemm1_pair<RP>(l0, l1, tile, 0, xh, xl, q, l16);
+  u32x4 zh, zl;
+  bool live = zsplit(l0, l1, zh, zl);
   for (int jp = 0; jp < np; ++jp) {
-    const u32x4* r0 = reinterpret_cast<const u32x4*>(tile + (32 * jp + l16) * C::LS);
-    const u32x4* r1 = reinterpret_cast<const u32x4*>(tile + (32 * jp + 16 + l16) * C::LS);
-    floatx4 a0[3], a1[3];
-#pragma unroll
-    for (int h = 0; h < 3; ++h) a0[h] = a1[h] = floatx4{0.f, 0.f, 0.f, 0.f};
-    u32x4 h0[KC], o0[KC], h1[KC], o1[KC];
-    constexpr int LA = KC < 2 ? KC : 2;
-#pragma unroll
-    for (int t = 0; t < LA; ++t) {
-      h0[t] = r0[2 * (4 * t + q)];
-      o0[t] = r0[2 * (4 * t + q) + 1];
-      h1[t] = r1[2 * (4 * t + q)];
-      o1[t] = r1[2 * (4 * t + q) + 1];
+    floatx4 m0 = floatx4{0.f, 0.f, 0.f, 0.f}, m1 = floatx4{0.f, 0.f, 0.f, 0.f};
+    if (jp + 1 < np) gemm1_pair<RP>(m0, m1, tile, jp + 1, xh, xl, q, l16);
+    u32x4 nzh, nzl;
+    bool nlive;
+    if (live) {
+      nlive = gemm2_pair<RP>(y, trans, jp, zh, zl, m0, m1, nzh, nzl, q, l16);
+      ++ran;
+    } else {
+      nlive = zsplit(m0, m1, nzh, nzl);
     }
-#pragma unroll
-    for (int t = 0; t < KC; ++t) {
-      if (t + LA < KC) {
-        h0[t + LA] = r0[2 * (4 * (t + LA) + q)];
-        o0[t + LA] = r0[2 * (4 * (t + LA) + q) + 1];
-        h1[t + LA] = r1[2 * (4 * (t + LA) + q)];
-        o1[t + LA] = r1[2 * (4 * (t + LA) + q) + 1];
-      }
-      a0[0] = mfma(h0[t], xh[t], a0[0]);
-      a1[0] = mfma(h1[t], xh[t], a1[0]);
-      a0[1] = mfma(h0[t], xl[t], a0[1]);
-      a1[1] = mfma(h1[t], xl[t], a1[1]);
-      a0[2] = mfma(o0[t], xh[t], a0[2]);
-      a1[2] = mfma(o1[t], xh[t], a1[2]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    const floatx4 l0 = a0[0] + (a0[1] + a0[2]);
-    const floatx4 l1 = a1[0] + (a1[1] + a1[2]);
-    const float z[8] = {l0[0] > 0.f ? l0[0] : 0.f, l0[1] > 0.f ? l0[1] : 0.f,
-                        l0[2] > 0.f ? l0[2] : 0.f, l0[3] > 0.f ? l0[3] : 0.f,
-                        l1[0] > 0.f ? l1[0] : 0.f, l1[1] > 0.f ? l1[1] : 0.f,
-                        l1[2] > 0.f ? l1[2] : 0.f, l1[3] > 0.f ? l1[3] : 0.f};
-    const bool pos = z[0] + z[1] + z[2] + z[3] + z[4] + z[5] + z[6] + z[7] > 0.f;
-    if (!__ballot(pos)) continue;  // max(0, L) is zero on the whole 16 x 32 tile
-    ++ran;
-    u32x4 zh, zl;
-    split8(z, zh, zl);
-    const u32x4* bh = reinterpret_cast<const u32x4*>(trans + jp * C::TB) + (2 * q) * RP + l16;
-    const u32x4* bl = bh + RP;
-    u32x4 nh[G], nl[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      nh[g] = bh[16 * g];
-      nl[g] = bl[16 * g];
-    }
-#pragma unroll
-    for (int cb0 = 0; cb0 < CB; cb0 += G) {
-      u32x4 ch[G], cl[G];
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        ch[g] = nh[g];
-        cl[g] = nl[g];
-      }
-      if (cb0 + G < CB) {
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          nh[g] = bh[16 * (cb0 + G + g)];
-          nl[g] = bl[16 * (cb0 + G + g)];
-        }
-      }
-#pragma unroll
-      for (int g = 0; g < G; ++g) y[cb0 + g] = mfma(zh, ch[g], y[cb0 + g]);
-#pragma unroll
-      for (int g = 0; g < G; ++g) y[cb0 + g] = mfma(zh, cl[g], y[cb0 + g]);
-#pragma unroll
-      for (int g = 0; g < G; ++g) y[cb0 + g] = mfma(zl, ch[g], y[cb0 + g]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    zh = nzh;
+    zl = nzl;
+    live = nlive;
   }
   return ran;
 }
@@ -317,6 +379,288 @@ __global__ __launch_bounds__(64 * Cfg<RP>::WAVES) void bx_kernel(
   }
   // a live 16 x 32 tile counts as its eight 16 x 4 slices of max(0, L)
   if (live_slices && lane == 0 && ran) atomicAdd(live_slices, 8ull * ran);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Ranks 32 to 128: 32 rows of X per wave on v_mfma_f32_32x32x16_bf16 (srcA lane l:
+// A[l%32][8(l/32) + e], srcB lane l: B[8(l/32) + e][l%32], accumulator register v of lane l:
+// D[8(v/4) + 4(l/32) + v%4][l%32]), which streams about 1.6 times the flops of the 16 x 16 x 32
+// form.  Per 32-row panel block: the first product gives lane l the L^T values of X row l%32
+// and panel rows j = 8(v/4) + 4(l/32) + v%4; rectified and split they are the srcA operands of
+// two K = 16 MFMAs of the second product (a = 0, 1), k-slot (h, e) <-> panel row
+// jrow32(a, h, e) = 16a + 8(e/4) + 4h + e%4.  The transposed panel copy holds, per block,
+// [a][h][hi, lo][column] groups of those eight rows.
+
+template <int RP>
+struct Cfg32 {
+  static constexpr int WAVES = 8;                     // two per SIMD
+  static constexpr int ROWS = 32 * WAVES;             // rows of X per workgroup
+  static constexpr int NT = RP >= 128 ? 64 : (RP >= 64 ? 128 : 256);
+  static constexpr int LS = RP + 4;
+  static constexpr int TB = 32 * RP;
+  static constexpr int TILE = NT * LS + (NT / 32) * TB;
+  static constexpr int CB = RP / 32;                  // 32-column blocks of Y
+  static_assert(RP % 32 == 0 && RP <= 128 && NT % WAVES == 0, "shape");
+};
+
+typedef __attribute__((ext_vector_type(16))) float floatx16;
+
+__device__ __forceinline__ floatx16 mfma32(u32x4 a, u32x4 b, floatx16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16(a), as_bf16(b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ int jrow32(int a, int h, int e) {
+  return 16 * a + 8 * (e >> 2) + 4 * h + (e & 3);
+}
+
+// Row-major and transposed split copies for the 32-row form (row-major as bx_split_kernel).
+template <int RP>
+__global__ __launch_bounds__(256) void bx32_split_kernel(const float* __restrict__ P, int64_t blk,
+                                                         int64_t npair, u32x4* __restrict__ rowm,
+                                                         u32x4* __restrict__ trans) {
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t na = blk * (RP / 8);
+  if (gid < na) {
+    const int64_t row = gid / (RP / 8);
+    const int g = (int)(gid - row * (RP / 8));
+    const float4 a = *reinterpret_cast<const float4*>(P + row * RP + 8 * g);
+    const float4 b = *reinterpret_cast<const float4*>(P + row * RP + 8 * g + 4);
+    const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    u32x4 hi, lo;
+    split8(x, hi, lo);
+    rowm[row * (RP / 4) + 2 * g] = hi;
+    rowm[row * (RP / 4) + 2 * g + 1] = lo;
+    return;
+  }
+  const int64_t t = gid - na;
+  if (t >= npair * 4 * RP) return;
+  const int64_t p = t / (4 * RP);
+  const int rem = (int)(t - p * 4 * RP);
+  const int ah = rem / RP, c = rem - ah * RP;  // ah = 2a + h
+  float x[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int64_t j = 32 * p + jrow32(ah >> 1, ah & 1, e);
+    x[e] = j < blk ? P[j * RP + c] : 0.f;
+  }
+  u32x4 hi, lo;
+  split8(x, hi, lo);
+  u32x4* blkp = trans + p * (8 * RP);
+  blkp[(2 * ah) * RP + c] = hi;
+  blkp[(2 * ah + 1) * RP + c] = lo;
+}
+
+// X rows of one wave as split srcB operands: xh[t], xl[t] = X[row0 + l%32][16t + 8h .. + 7].
+template <int RP>
+__device__ __forceinline__ void load_x32(u32x4 (&xh)[RP / 16], u32x4 (&xl)[RP / 16],
+                                         const float* __restrict__ X, int64_t rows, int64_t row0,
+                                         int h, int l32) {
+  const int64_t row = row0 + l32;
+#pragma unroll
+  for (int t = 0; t < RP / 16; ++t) {
+    float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (row < rows) {
+      const float4 a = *reinterpret_cast<const float4*>(X + row * RP + 16 * t + 8 * h);
+      const float4 b = *reinterpret_cast<const float4*>(X + row * RP + 16 * t + 8 * h + 4);
+      x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+      x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+    }
+    split8(x, xh[t], xl[t]);
+  }
+}
+
+// First product of panel block jp: L^T (32 panel rows x 32 X rows) in two accumulator chains.
+template <int RP>
+__device__ __forceinline__ floatx16 gemm1_blk32(const float* tile, int jp,
+                                                const u32x4 (&xh)[RP / 16],
+                                                const u32x4 (&xl)[RP / 16], int h, int l32) {
+  using C = Cfg32<RP>;
+  constexpr int KC = RP / 16;
+  constexpr int LA = RP >= 128 ? 1 : (KC < 2 ? KC : 2);  // one chunk ahead where registers are short
+  const u32x4* pr = reinterpret_cast<const u32x4*>(tile + (32 * jp + l32) * C::LS);
+  floatx16 a0, a1;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) a0[v] = a1[v] = 0.f;
+  u32x4 ph[KC], pl[KC];
+#pragma unroll
+  for (int t = 0; t < LA; ++t) {
+    ph[t] = pr[2 * (2 * t + h)];
+    pl[t] = pr[2 * (2 * t + h) + 1];
+  }
+#pragma unroll
+  for (int t = 0; t < KC; ++t) {
+    if (t + LA < KC) {
+      ph[t + LA] = pr[2 * (2 * (t + LA) + h)];
+      pl[t + LA] = pr[2 * (2 * (t + LA) + h) + 1];
+    }
+    a0 = mfma32(ph[t], xh[t], a0);
+    a1 = mfma32(ph[t], xl[t], a1);
+    a0 = mfma32(pl[t], xh[t], a0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  return a0 + a1;
+}
+
+// Rectified block as the second product's split srcA operands (a = 0: registers 0..7,
+// a = 1: registers 8..15); whether any of it is positive (wave-uniform).
+__device__ __forceinline__ bool zsplit32(floatx16 l, u32x4 (&zh)[2], u32x4 (&zl)[2]) {
+  float z[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) z[v] = l[v] > 0.f ? l[v] : 0.f;
+  float s = 0.f;
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      x[e] = z[8 * a + e];
+      s += x[e];
+    }
+    split8(x, zh[a], zl[a]);
+  }
+  return __ballot(s > 0.f) != 0;
+}
+
+// Second product of block jp into the 32 x 32 tiles of Y; with NEXT the next block's rectify
+// and split (from ln) is placed after the first column block, so that its vector work issues
+// while the MFMAs run.
+template <int RP, bool NEXT>
+__device__ __forceinline__ bool gemm2_blk32(floatx16 (&y)[RP / 32], const float* trans, int jp,
+                                            const u32x4 (&zh)[2], const u32x4 (&zl)[2],
+                                            floatx16 ln, u32x4 (&nzh)[2], u32x4 (&nzl)[2], int h,
+                                            int l32) {
+  using C = Cfg32<RP>;
+  constexpr int CB = C::CB;
+  const u32x4* base = reinterpret_cast<const u32x4*>(trans + jp * C::TB) + l32;
+  bool live = false;
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    u32x4 bh[2], bl[2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      bh[a] = base[(2 * (2 * a + h)) * RP + 32 * cb];
+      bl[a] = base[(2 * (2 * a + h) + 1) * RP + 32 * cb];
+    }
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      y[cb] = mfma32(zh[a], bh[a], y[cb]);
+      y[cb] = mfma32(zh[a], bl[a], y[cb]);
+      y[cb] = mfma32(zl[a], bh[a], y[cb]);
+    }
+    if (NEXT && cb == 0) live = zsplit32(ln, nzh, nzl);
+  }
+  return live;
+}
+
+template <int RP>
+__device__ __forceinline__ unsigned consume32(const float* tile, int np,
+                                              const u32x4 (&xh)[RP / 16],
+                                              const u32x4 (&xl)[RP / 16],
+                                              floatx16 (&y)[RP / 32], int h, int l32) {
+  using C = Cfg32<RP>;
+  const float* trans = tile + C::NT * C::LS;
+  unsigned ran = 0;
+  u32x4 zh[2], zl[2];
+  if constexpr (RP >= 128) {
+    // registers do not allow the pipelined form: one block at a time
+    floatx16 zero;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) zero[v] = 0.f;
+    for (int jp = 0; jp < np; ++jp) {
+      if (zsplit32(gemm1_blk32<RP>(tile, jp, xh, xl, h, l32), zh, zl)) {
+        u32x4 dh[2], dl[2];
+        gemm2_blk32<RP, false>(y, trans, jp, zh, zl, zero, dh, dl, h, l32);
+        ++ran;
+      }
+    }
+    return ran;
+  }
+  bool live = zsplit32(gemm1_blk32<RP>(tile, 0, xh, xl, h, l32), zh, zl);
+  for (int jp = 0; jp < np; ++jp) {
+    floatx16 ln;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) ln[v] = 0.f;
+    if (jp + 1 < np) ln = gemm1_blk32<RP>(tile, jp + 1, xh, xl, h, l32);
+    u32x4 nzh[2], nzl[2];
+    bool nlive;
+    if (live) {
+      nlive = gemm2_blk32<RP, true>(y, trans, jp, zh, zl, ln, nzh, nzl, h, l32);
+      ++ran;
+    } else {
+      nlive = zsplit32(ln, nzh, nzl);
+    }
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      zh[a] = nzh[a];
+      zl[a] = nzl[a];
+    }
+    live = nlive;
+  }
+  return ran;
+}
+
+template <int RP>
+__device__ __forceinline__ unsigned step32(const float* __restrict__ cur, float* __restrict__ nxt,
+                                           const float* __restrict__ rowm,
+                                           const float* __restrict__ trans, int64_t j0,
+                                           int64_t jb1, const u32x4 (&xh)[RP / 16],
+                                           const u32x4 (&xl)[RP / 16], floatx16 (&y)[RP / 32],
+                                           int wave, int lane, int h, int l32) {
+  constexpr int NT = Cfg32<RP>::NT;
+  if (nxt) stage32<RP>(nxt, rowm, trans, j0 + NT, jb1, wave, lane);
+  const int64_t left = (jb1 - j0 + 31) / 32;
+  return consume32<RP>(cur, left < NT / 32 ? (int)left : NT / 32, xh, xl, y, h, l32);
+}
+
+template <int RP>
+__global__ __launch_bounds__(64 * Cfg32<RP>::WAVES) void bx32_kernel(
+    const float* __restrict__ X, int64_t rows, const float* __restrict__ rowm,
+    const float* __restrict__ trans, int64_t blk, float* __restrict__ Ypart, int64_t y_stride,
+    int nsplit, int64_t row_tiles, float sgn, unsigned long long* __restrict__ live_slices) {
+  using C = Cfg32<RP>;
+  constexpr int CB = C::CB;
+  __shared__ __attribute__((aligned(16))) float smem[2 * C::TILE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = lane >> 5, l32 = lane & 31;
+
+  const int64_t logical = xcd_logical(blockIdx.x, (int64_t)gridDim.x);
+  const int split = (int)(logical / row_tiles);
+  const int64_t rt = logical - (int64_t)split * row_tiles;
+  const int64_t jb0 = pair_start(split, nsplit, blk);
+  const int64_t jb1 = pair_start(split + 1, nsplit, blk);
+  const int64_t row0 = rt * C::ROWS + (int64_t)wave * 32;
+
+  u32x4 xh[RP / 16], xl[RP / 16];
+  load_x32<RP>(xh, xl, X, rows, row0, h, l32);
+  floatx16 y[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) y[cb][v] = 0.f;
+
+  if (jb0 < jb1) stage32<RP>(smem, rowm, trans, jb0, jb1, wave, lane);
+  int cur = 0;
+  unsigned ran = 0;
+  for (int64_t j0 = jb0; j0 < jb1; j0 += C::NT, cur ^= 1) {
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the tile have landed
+    __syncthreads();                // every wave's have; the other buffer is free again
+    ran += step32<RP>(smem + cur * C::TILE, j0 + C::NT < jb1 ? smem + (cur ^ 1) * C::TILE : nullptr,
+                      rowm, trans, j0, jb1, xh, xl, y, wave, lane, h, l32);
+  }
+
+  float* Y = Ypart + (int64_t)split * y_stride;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int64_t row = row0 + 8 * (v / 4) + 4 * h + (v % 4);
+    if (row < rows) {
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) Y[row * RP + 32 * cb + l32] = sgn * y[cb][v];
+    }
+  }
+  // a live 32 x 32 tile counts as its sixteen 16 x 4 slices of max(0, L)
+  if (live_slices && lane == 0 && ran) atomicAdd(live_slices, 16ull * ran);
 }
 
 }  // namespace bx
