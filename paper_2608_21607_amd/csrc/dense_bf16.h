@@ -397,10 +397,12 @@ struct Cfg32 {
   static constexpr int ROWS = 32 * WAVES;             // rows of X per workgroup
   static constexpr int NT = RP >= 128 ? 64 : (RP >= 64 ? 128 : 256);
   static constexpr int LS = RP + 4;
-  static constexpr int TB = 32 * RP;
+  static constexpr int RPC = RP < 32 ? 32 : RP;       // columns of the second product (r = 16
+                                                      // pads to one 32-column block)
+  static constexpr int TB = 32 * RPC;
   static constexpr int TILE = NT * LS + (NT / 32) * TB;
-  static constexpr int CB = RP / 32;                  // 32-column blocks of Y
-  static_assert(RP % 32 == 0 && RP <= 128 && NT % WAVES == 0, "shape");
+  static constexpr int CB = RPC / 32;                 // 32-column blocks of Y
+  static_assert(RP % 16 == 0 && RP <= 128 && NT % WAVES == 0, "shape");
 };
 
 typedef __attribute__((ext_vector_type(16))) float floatx16;
@@ -413,7 +415,8 @@ __device__ __forceinline__ int jrow32(int a, int h, int e) {
   return 16 * a + 8 * (e >> 2) + 4 * h + (e & 3);
 }
 
-// Row-major and transposed split copies for the 32-row form (row-major as bx_split_kernel).
+// Row-major and transposed split copies for the 32-row form (row-major as bx_split_kernel; the
+// transposed blocks are Cfg32<RP>::RPC columns wide, zero past RP).
 template <int RP>
 __global__ __launch_bounds__(256) void bx32_split_kernel(const float* __restrict__ P, int64_t blk,
                                                          int64_t npair, u32x4* __restrict__ rowm,
@@ -432,22 +435,23 @@ __global__ __launch_bounds__(256) void bx32_split_kernel(const float* __restrict
     rowm[row * (RP / 4) + 2 * g + 1] = lo;
     return;
   }
+  constexpr int RPC = Cfg32<RP>::RPC;
   const int64_t t = gid - na;
-  if (t >= npair * 4 * RP) return;
-  const int64_t p = t / (4 * RP);
-  const int rem = (int)(t - p * 4 * RP);
-  const int ah = rem / RP, c = rem - ah * RP;  // ah = 2a + h
+  if (t >= npair * 4 * RPC) return;
+  const int64_t p = t / (4 * RPC);
+  const int rem = (int)(t - p * 4 * RPC);
+  const int ah = rem / RPC, c = rem - ah * RPC;  // ah = 2a + h
   float x[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int64_t j = 32 * p + jrow32(ah >> 1, ah & 1, e);
-    x[e] = j < blk ? P[j * RP + c] : 0.f;
+    x[e] = j < blk && c < RP ? P[j * RP + c] : 0.f;
   }
   u32x4 hi, lo;
   split8(x, hi, lo);
-  u32x4* blkp = trans + p * (8 * RP);
-  blkp[(2 * ah) * RP + c] = hi;
-  blkp[(2 * ah + 1) * RP + c] = lo;
+  u32x4* blkp = trans + p * (8 * RPC);
+  blkp[(2 * ah) * RPC + c] = hi;
+  blkp[(2 * ah + 1) * RPC + c] = lo;
 }
 
 // X rows of one wave as split srcB operands: xh[t], xl[t] = X[row0 + l%32][16t + 8h .. + 7].
@@ -525,7 +529,7 @@ __device__ __forceinline__ bool zsplit32(floatx16 l, u32x4 (&zh)[2], u32x4 (&zl)
 // and split (from ln) is placed after the first column block, so that its vector work issues
 // while the MFMAs run.
 template <int RP, bool NEXT>
-__device__ __forceinline__ bool gemm2_blk32(floatx16 (&y)[RP / 32], const float* trans, int jp,
+__device__ __forceinline__ bool gemm2_blk32(floatx16 (&y)[Cfg32<RP>::CB], const float* trans, int jp,
                                             const u32x4 (&zh)[2], const u32x4 (&zl)[2],
                                             floatx16 ln, u32x4 (&nzh)[2], u32x4 (&nzl)[2], int h,
                                             int l32) {
@@ -538,8 +542,8 @@ __device__ __forceinline__ bool gemm2_blk32(floatx16 (&y)[RP / 32], const float*
     u32x4 bh[2], bl[2];
 #pragma unroll
     for (int a = 0; a < 2; ++a) {
-      bh[a] = base[(2 * (2 * a + h)) * RP + 32 * cb];
-      bl[a] = base[(2 * (2 * a + h) + 1) * RP + 32 * cb];
+      bh[a] = base[(2 * (2 * a + h)) * C::RPC + 32 * cb];
+      bl[a] = base[(2 * (2 * a + h) + 1) * C::RPC + 32 * cb];
     }
 #pragma unroll
     for (int a = 0; a < 2; ++a) {
@@ -556,7 +560,7 @@ template <int RP>
 __device__ __forceinline__ unsigned consume32(const float* tile, int np,
                                               const u32x4 (&xh)[RP / 16],
                                               const u32x4 (&xl)[RP / 16],
-                                              floatx16 (&y)[RP / 32], int h, int l32) {
+                                              floatx16 (&y)[Cfg32<RP>::CB], int h, int l32) {
   using C = Cfg32<RP>;
   const float* trans = tile + C::NT * C::LS;
   unsigned ran = 0;
@@ -604,7 +608,7 @@ __device__ __forceinline__ unsigned step32(const float* __restrict__ cur, float*
                                            const float* __restrict__ rowm,
                                            const float* __restrict__ trans, int64_t j0,
                                            int64_t jb1, const u32x4 (&xh)[RP / 16],
-                                           const u32x4 (&xl)[RP / 16], floatx16 (&y)[RP / 32],
+                                           const u32x4 (&xl)[RP / 16], floatx16 (&y)[Cfg32<RP>::CB],
                                            int wave, int lane, int h, int l32) {
   constexpr int NT = Cfg32<RP>::NT;
   if (nxt) stage32<RP>(nxt, rowm, trans, j0 + NT, jb1, wave, lane);
@@ -656,7 +660,8 @@ __global__ __launch_bounds__(64 * Cfg32<RP>::WAVES) void bx32_kernel(
     const int64_t row = row0 + 8 * (v / 4) + 4 * h + (v % 4);
     if (row < rows) {
 #pragma unroll
-      for (int cb = 0; cb < CB; ++cb) Y[row * RP + 32 * cb + l32] = sgn * y[cb][v];
+      for (int cb = 0; cb < CB; ++cb)
+        if (RP % 32 == 0 || 32 * cb + l32 < RP) Y[row * RP + 32 * cb + l32] = sgn * y[cb][v];
     }
   }
   // a live 32 x 32 tile counts as its sixteen 16 x 4 slices of max(0, L)
@@ -698,7 +703,7 @@ static hipError_t bx32_launch_t(const float* X, int64_t rows, const float* P, in
   const int64_t npair = (blk + 31) / 32;
   float* rowm = work;
   float* trans = work + blk * RP;
-  const int64_t threads = blk * (RP / 8) + npair * 4 * RP;
+  const int64_t threads = blk * (RP / 8) + npair * 4 * C::RPC;
   hipLaunchKernelGGL(bx::bx32_split_kernel<RP>, dim3((unsigned)((threads + 255) / 256)),
                      dim3(256), 0, st, P, blk, npair, reinterpret_cast<bx::u32x4*>(rowm),
                      reinterpret_cast<bx::u32x4*>(trans));

@@ -1,12 +1,14 @@
 // Launchers of the rectified contraction with both products on split bf16 MFMA (kernels in
-// dense_bf16.h): the 32 x 32 x 16 form at padded ranks 32, 64, 128, the 16 x 16 x 32 form at 256.
+// dense_bf16.h): the 32 x 32 x 16 form at padded ranks 16 to 128, the 16 x 16 x 32 form at 256.
 
 #include "dense_bf16.h"
 #include "nmd_internal.h"
 
 namespace nmd {
 
-int64_t bf16x3_work_floats(int64_t blk, int rp) { return (blk + (blk + 31) / 32 * 32) * rp; }
+int64_t bf16x3_work_floats(int64_t blk, int rp) {
+  return blk * rp + (blk + 31) / 32 * 32 * (rp < 32 ? 32 : rp);
+}
 
 hipError_t launch_bf16x3(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
                          float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
@@ -14,6 +16,7 @@ hipError_t launch_bf16x3(const float* X, int64_t rows, const float* P, int64_t b
 #define BX(R) bx_launch_t<R>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, live, st)
 #define BX32(R) bx32_launch_t<R>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, live, st)
   switch (rp) {
+    case 16: return BX32(16);
     case 32: return BX32(32);
     case 64: return BX32(64);
     case 128: return BX32(128);

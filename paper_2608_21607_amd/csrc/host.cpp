@@ -1021,7 +1021,7 @@ int nmd_rectified_contraction(const float* A, int64_t rows, const float* B, int6
 }
 
 int64_t nmd_bf16x3_workspace_floats(int64_t blk, int32_t r) {
-  if (blk < 1 || (r != 32 && r != 64 && r != 128 && r != 256)) return -1;
+  if (blk < 1 || (r != 16 && r != 32 && r != 64 && r != 128 && r != 256)) return -1;
   return nmd::bf16x3_work_floats(blk, r);
 }
 
@@ -1032,8 +1032,8 @@ int nmd_rectified_contraction_bf16x3(const float* A, int64_t rows, const float* 
     return fail(nullptr, NMD_EINVAL, "A, B, work and Y must be non-NULL");
   if (rows < 1 || blk < 1 || rows > INT32_MAX)
     return fail(nullptr, NMD_EINVAL, "rows and blk must be >= 1");
-  if (r != 32 && r != 64 && r != 128 && r != 256)
-    return fail(nullptr, NMD_EINVAL, "the bf16x3 contraction needs r in {32, 64, 128, 256} (got %d)", r);
+  if (r != 16 && r != 32 && r != 64 && r != 128 && r != 256)
+    return fail(nullptr, NMD_EINVAL, "the bf16x3 contraction needs r in {16, 32, 64, 128, 256} (got %d)", r);
   hipError_t e = nmd::launch_bf16x3(A, rows, B, blk, r, work, Y, 0, 1, 1.0f, nullptr,
                                     (hipStream_t)hip_stream);
   if (e != hipSuccess) return fail(nullptr, NMD_EDEVICE, "launch failed: %s", hipGetErrorString(e));

@@ -46,7 +46,7 @@ hipError_t launch_dense(const float* X, int64_t rows, const float* P, int64_t bl
                         float* Ypart, int64_t y_stride, int nsplit, float sgn,
                         unsigned long long* gemm2_blocks, hipStream_t st);
 
-// Both products on split bf16 MFMA (dense_bf16.h), rp in {32, 64, 128, 256}: splits the blk x rp
+// Both products on split bf16 MFMA (dense_bf16.h), rp in {16, 32, 64, 128, 256}: splits the blk x rp
 // panel P into `work` (bf16x3_work_floats(blk, rp) floats: row-major and transposed split
 // copies), then Y_s = sgn * max(0, X P_s^T) P_s for each of nsplit panel ranges starting at
 // bf16x3_pair_start(s, nsplit, blk) (whole 32-row pairs).  When `live` is not NULL, 8 per
