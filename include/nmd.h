@@ -48,16 +48,18 @@ enum {
                           nmd_reset                                                       */
   NMD_FLAG_TIMING = 2u, /* record HIP events around every kernel class (see
                           nmd_get_kernel_timing); adds a few microseconds per step        */
-  NMD_FLAG_SPLIT_BF16 = 4u /* padded rank r_p = 256, i.e. r in 193..256 (other ranks
-                          ignore it): both products of the dense contraction,
+  NMD_FLAG_SPLIT_BF16 = 4u /* padded rank r_p in {16, 32, 64, 128, 256}, i.e. r <= 32 or
+                          r in 49..64, 65..128, 193..256 (other ranks ignore it): both
+                          products of the dense contraction,
                           L = A B_J^T and max(0, L) B_J, run on bf16 MFMA with every
                           operand split in two (x = bf16(x) + bf16(x - bf16(x)), three
                           products each, fp32 accumulation; relative error about 2^-16 of
                           the sum of the magnitudes of the terms) instead of fp32 MFMA, the
                           counterpart of the paper's TF32 kernels (Sec. 4.2); the kernel of
                           nmd_rectified_contraction_bf16x3.  Everything else stays fp32.
-                          Needs nmd_bf16x3_workspace_floats(max(m, n), 256) floats more
-                          device memory                                                     */
+                          Needs nmd_bf16x3_workspace_floats(max(m, n), r_p) floats more
+                          device memory.  It adds one small kernel per step, so on steps
+                          too small to fill the GPU it can cost more than it saves         */
 };
 
 typedef struct {

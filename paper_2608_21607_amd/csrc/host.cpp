@@ -233,7 +233,7 @@ struct nmd_ctx {
   float *A2 = nullptr, *B2 = nullptr, *VA2 = nullptr, *VB2 = nullptr;
   std::vector<std::pair<int, bool>> enqueued;  // (step id, W-step) of the call's steps, in order
   float* Ypart = nullptr;
-  float* Pbx = nullptr;  // split-bf16 panel copies (NMD_FLAG_SPLIT_BF16 at r_p = 256)
+  float* Pbx = nullptr;  // split-bf16 panel copies (NMD_FLAG_SPLIT_BF16 at r_p = 16..256)
   int64_t ypart_floats = 0;
   float* scratch = nullptr;
   int64_t scratch_floats = 0;
@@ -417,9 +417,9 @@ int ensure_device(nmd_ctx* c) {
     need = std::max(need, nsplit_for(c->m, c->n, c->rp, c->dense_slots) * c->m);
     need = std::max(need, nsplit_for(c->n, c->m, c->rp, c->dense_slots) * c->n);
     c->ypart_floats = need * rp;
-    // the split-bf16 option runs at r_p = 256 (at the smaller ranks of the workloads here the
-    // steps are too small for it to pay; the standalone contraction offers it from r_p = 32)
-    const bool bx = (c->opt.flags & NMD_FLAG_SPLIT_BF16) && rp == 256;
+    // the split-bf16 option covers the padded ranks the bf16x3 kernels support
+    const bool bx = (c->opt.flags & NMD_FLAG_SPLIT_BF16) &&
+                    (rp == 16 || rp == 32 || rp == 64 || rp == 128 || rp == 256);
     if (dalloc(&c->Ypart, c->ypart_floats) != hipSuccess ||
         (bx && dalloc(&c->Pbx, nmd::bf16x3_work_floats(std::max(c->m, c->n), rp)) != hipSuccess)) {
       free_device(c);

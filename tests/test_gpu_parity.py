@@ -348,6 +348,23 @@ def test_stochastic_planted_reduced(eta, mom):
     assert ctx.schedule(0) == schedule.sweep_schedule(p.seed, 0, R, C, True)
 
 
+def test_stochastic_planted_reduced_split_bf16():
+    """The split-bf16 flag at r_p = 64 (the 32 x 32 x 16 form of both products) on the 4096 x 4096
+    planted workload, momentum 0.9, one sweep: W, H within the 1e-4 bar."""
+    p = gen.config(3, scale=0.125)
+    p.block_m = p.block_n = 512
+    _say("config 3 reduced, stochastic, split bf16")
+    ctx = make_ctx(p, eta=1.0, mom=0.9, flags=nmd.FLAG_SPLIT_BF16)
+    W, H = dev(p.W0), dev(p.H0)
+    ctx.sweep(W, H, 1)
+    run, total, entries = ctx.dense_blocks()
+    assert total > 0 and run % 16 == 0 and entries == 0  # live 32 x 32 tiles count 16 slices
+    Wo, Ho, _ = oracle_run(p, 1, eta=1.0, mom=0.9)
+    ew, eh = rel(W.cpu().numpy(), Wo), rel(H.cpu().numpy(), Ho)
+    print(f"split bf16 sweep r = 64: rel err W {ew:.2e} H {eh:.2e}")
+    assert ew < TOL and eh < TOL
+
+
 def test_stochastic_three_sweeps_and_persistent_state():
     """Sweeps run in one call equal the same sweeps run one call at a time (the sweep counter
     and the momentum persist); after reset the first sweep repeats bit for bit."""
