@@ -175,11 +175,44 @@ __device__ __forceinline__ void stage(float* dst, const float* __restrict__ rowm
 template <int RP>
 struct Cfg32;
 
+// Row-major tile of the 32-row form: rows unpadded, 16-byte chunk c of row j stored at
+// c ^ swz32(j), which spreads 16 consecutive rows over 16 distinct bank groups for the first
+// product's reads while letting one direct load cover 64 consecutive chunks (several rows).
+template <int RP>
+__device__ __forceinline__ int swz32(int row) {
+  constexpr int C = RP / 4;  // chunks per row
+  return C >= 16 ? (row & 15) : (C == 8 ? ((row >> 1) & 7) : ((row >> 2) & 3));
+}
+
 template <int RP>
 __device__ __forceinline__ void stage32(float* dst, const float* __restrict__ rowm,
                                         const float* __restrict__ trans, int64_t j0, int64_t jb1,
                                         int wave, int lane) {
-  stage_t<RP, Cfg32<RP>>(dst, rowm, trans, j0, jb1, wave, lane);
+  using C = Cfg32<RP>;
+  constexpr int CPR = RP / 4;
+  constexpr int NI = C::NT * CPR / 64;  // direct loads of 64 chunks for the row-major tile
+#pragma unroll
+  for (int u = 0; u < NI / C::WAVES; ++u) {
+    const int i = wave + C::WAVES * u;
+    const int q = 64 * i + lane;           // chunk of the tile this lane fills
+    const int r = q / CPR, ph = q - r * CPR;
+    const int c = ph ^ swz32<RP>(r);       // logical chunk stored there
+    const int64_t j = j0 + r;
+    if (j < jb1)
+      __builtin_amdgcn_global_load_lds((glb_void*)(rowm + j * RP + 4 * c),
+                                       (lds_void*)(dst + 256 * i), 16, 0, 0);
+    else
+      *reinterpret_cast<float4*>(dst + 4 * q) = float4{0.f, 0.f, 0.f, 0.f};
+  }
+  const int64_t p0 = j0 / 32;
+  const int64_t left = (jb1 - j0 + 31) / 32;
+  const int np = left < C::NT / 32 ? (int)left : C::NT / 32;
+  const int ninst = np * (C::TB / 256);
+  float* tdst = dst + C::NT * C::LS;
+  const float* tsrc = trans + p0 * C::TB;
+  for (int i = wave; i < ninst; i += C::WAVES)
+    __builtin_amdgcn_global_load_lds((glb_void*)(tsrc + 256 * i + 4 * lane),
+                                     (lds_void*)(tdst + 256 * i), 16, 0, 0);
 }
 
 // First product of pair jp: the two 16 x 16 L^T tiles (six accumulator chains, panel reads two
@@ -396,7 +429,7 @@ struct Cfg32 {
   static constexpr int WAVES = 8;                     // two per SIMD
   static constexpr int ROWS = 32 * WAVES;             // rows of X per workgroup
   static constexpr int NT = RP >= 128 ? 64 : (RP >= 64 ? 128 : 256);
-  static constexpr int LS = RP + 4;
+  static constexpr int LS = RP;                       // row-major rows unpadded, chunks swizzled
   static constexpr int RPC = RP < 32 ? 32 : RP;       // columns of the second product (r = 16
                                                       // pads to one 32-column block)
   static constexpr int TB = 32 * RPC;
@@ -481,26 +514,63 @@ __device__ __forceinline__ floatx16 gemm1_blk32(const float* tile, int jp,
   using C = Cfg32<RP>;
   constexpr int KC = RP / 16;
   constexpr int LA = RP >= 128 ? 1 : (KC < 2 ? KC : 2);  // one chunk ahead where registers are short
-  const u32x4* pr = reinterpret_cast<const u32x4*>(tile + (32 * jp + l32) * C::LS);
+  const int row = 32 * jp + l32;
+  const u32x4* pr = reinterpret_cast<const u32x4*>(tile + row * C::LS);
+  const int sw = swz32<RP>(row);
   floatx16 a0, a1;
 #pragma unroll
   for (int v = 0; v < 16; ++v) a0[v] = a1[v] = 0.f;
   u32x4 ph[KC], pl[KC];
 #pragma unroll
   for (int t = 0; t < LA; ++t) {
-    ph[t] = pr[2 * (2 * t + h)];
-    pl[t] = pr[2 * (2 * t + h) + 1];
+    ph[t] = pr[(2 * (2 * t + h)) ^ sw];
+    pl[t] = pr[(2 * (2 * t + h) + 1) ^ sw];
   }
 #pragma unroll
   for (int t = 0; t < KC; ++t) {
     if (t + LA < KC) {
-      ph[t + LA] = pr[2 * (2 * (t + LA) + h)];
-      pl[t + LA] = pr[2 * (2 * (t + LA) + h) + 1];
+      ph[t + LA] = pr[(2 * (2 * (t + LA) + h)) ^ sw];
+      pl[t + LA] = pr[(2 * (2 * (t + LA) + h) + 1) ^ sw];
     }
     a0 = mfma32(ph[t], xh[t], a0);
     a1 = mfma32(ph[t], xl[t], a1);
     a0 = mfma32(pl[t], xh[t], a0);
     __builtin_amdgcn_sched_barrier(0);
+  }
+  return a0 + a1;
+}
+
+// Ranks up to 32 (at most two k chunks): a block's panel operands as registers, read a block
+// ahead of its MFMAs, so that the LDS latency hides behind the previous block's work.
+template <int RP>
+struct Ops32 {
+  u32x4 h[RP / 16], l[RP / 16];
+};
+
+template <int RP>
+__device__ __forceinline__ void load_blk32(Ops32<RP>& o, const float* tile, int jp, int h,
+                                           int l32) {
+  const int row = 32 * jp + l32;
+  const u32x4* pr = reinterpret_cast<const u32x4*>(tile + row * Cfg32<RP>::LS);
+  const int sw = swz32<RP>(row);
+#pragma unroll
+  for (int t = 0; t < RP / 16; ++t) {
+    o.h[t] = pr[(2 * (2 * t + h)) ^ sw];
+    o.l[t] = pr[(2 * (2 * t + h) + 1) ^ sw];
+  }
+}
+
+template <int RP>
+__device__ __forceinline__ floatx16 mma_blk32(const Ops32<RP>& o, const u32x4 (&xh)[RP / 16],
+                                              const u32x4 (&xl)[RP / 16]) {
+  floatx16 a0, a1;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) a0[v] = a1[v] = 0.f;
+#pragma unroll
+  for (int t = 0; t < RP / 16; ++t) {
+    a0 = mfma32(o.h[t], xh[t], a0);
+    a1 = mfma32(o.h[t], xl[t], a1);
+    a0 = mfma32(o.l[t], xh[t], a0);
   }
   return a0 + a1;
 }
@@ -576,6 +646,42 @@ __device__ __forceinline__ unsigned consume32(const float* tile, int np,
         gemm2_blk32<RP, false>(y, trans, jp, zh, zl, zero, dh, dl, h, l32);
         ++ran;
       }
+    }
+    return ran;
+  }
+  if constexpr (RP <= 32) {
+    // operands a block ahead in ping-pong registers: the reads of block jp + 2 are in flight
+    // during the second product of block jp
+    Ops32<RP> o0, o1;  // block jp's operands alternate between o0 (even) and o1 (odd)
+    load_blk32<RP>(o0, tile, 0, h, l32);
+    if (np > 1) load_blk32<RP>(o1, tile, 1, h, l32);
+    bool live = zsplit32(mma_blk32<RP>(o0, xh, xl), zh, zl);
+    // one block: the first product of jp + 1 (operands in nxt), the reads of jp + 2 (into
+    // reload, whose block jp is done), the second product of jp with the split of jp + 1
+    auto block = [&](int jp, const Ops32<RP>& nxt, Ops32<RP>& reload) {
+      floatx16 ln;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) ln[v] = 0.f;
+      if (jp + 1 < np) ln = mma_blk32<RP>(nxt, xh, xl);
+      if (jp + 2 < np) load_blk32<RP>(reload, tile, jp + 2, h, l32);
+      u32x4 nzh[2], nzl[2];
+      bool nlive;
+      if (live) {
+        nlive = gemm2_blk32<RP, true>(y, trans, jp, zh, zl, ln, nzh, nzl, h, l32);
+        ++ran;
+      } else {
+        nlive = zsplit32(ln, nzh, nzl);
+      }
+#pragma unroll
+      for (int a = 0; a < 2; ++a) {
+        zh[a] = nzh[a];
+        zl[a] = nzl[a];
+      }
+      live = nlive;
+    };
+    for (int jp = 0; jp < np; jp += 2) {
+      block(jp, o1, o0);
+      if (jp + 1 < np) block(jp + 1, o0, o1);
     }
     return ran;
   }
