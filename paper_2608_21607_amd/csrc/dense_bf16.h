@@ -599,14 +599,31 @@ __device__ __forceinline__ bool zsplit32(floatx16 l, u32x4 (&zh)[2], u32x4 (&zl)
 // and split (from ln) is placed after the first column block, so that its vector work issues
 // while the MFMAs run.
 template <int RP, bool NEXT>
-__device__ __forceinline__ bool gemm2_blk32(floatx16 (&y)[Cfg32<RP>::CB], const float* trans, int jp,
-                                            const u32x4 (&zh)[2], const u32x4 (&zl)[2],
-                                            floatx16 ln, u32x4 (&nzh)[2], u32x4 (&nzl)[2], int h,
-                                            int l32) {
+__device__ __forceinline__ bool gemm2_blk32(floatx16 (&y)[Cfg32<RP>::CB], floatx16& y2,
+                                            const float* trans, int jp, const u32x4 (&zh)[2],
+                                            const u32x4 (&zl)[2], floatx16 ln, u32x4 (&nzh)[2],
+                                            u32x4 (&nzl)[2], int h, int l32) {
   using C = Cfg32<RP>;
   constexpr int CB = C::CB;
   const u32x4* base = reinterpret_cast<const u32x4*>(trans + jp * C::TB) + l32;
   bool live = false;
+  if constexpr (CB == 1) {
+    // one column block: the a = 1 half accumulates into y2 so that the two chains interleave
+    u32x4 bh[2], bl[2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      bh[a] = base[(2 * (2 * a + h)) * C::RPC];
+      bl[a] = base[(2 * (2 * a + h) + 1) * C::RPC];
+    }
+    y[0] = mfma32(zh[0], bh[0], y[0]);
+    y2 = mfma32(zh[1], bh[1], y2);
+    y[0] = mfma32(zh[0], bl[0], y[0]);
+    y2 = mfma32(zh[1], bl[1], y2);
+    y[0] = mfma32(zl[0], bh[0], y[0]);
+    y2 = mfma32(zl[1], bh[1], y2);
+    if (NEXT) live = zsplit32(ln, nzh, nzl);
+    return live;
+  }
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     u32x4 bh[2], bl[2];
@@ -630,7 +647,8 @@ template <int RP>
 __device__ __forceinline__ unsigned consume32(const float* tile, int np,
                                               const u32x4 (&xh)[RP / 16],
                                               const u32x4 (&xl)[RP / 16],
-                                              floatx16 (&y)[Cfg32<RP>::CB], int h, int l32) {
+                                              floatx16 (&y)[Cfg32<RP>::CB], floatx16& y2, int h,
+                                              int l32) {
   using C = Cfg32<RP>;
   const float* trans = tile + C::NT * C::LS;
   unsigned ran = 0;
@@ -643,7 +661,7 @@ __device__ __forceinline__ unsigned consume32(const float* tile, int np,
     for (int jp = 0; jp < np; ++jp) {
       if (zsplit32(gemm1_blk32<RP>(tile, jp, xh, xl, h, l32), zh, zl)) {
         u32x4 dh[2], dl[2];
-        gemm2_blk32<RP, false>(y, trans, jp, zh, zl, zero, dh, dl, h, l32);
+        gemm2_blk32<RP, false>(y, y2, trans, jp, zh, zl, zero, dh, dl, h, l32);
         ++ran;
       }
     }
@@ -667,7 +685,7 @@ __device__ __forceinline__ unsigned consume32(const float* tile, int np,
       u32x4 nzh[2], nzl[2];
       bool nlive;
       if (live) {
-        nlive = gemm2_blk32<RP, true>(y, trans, jp, zh, zl, ln, nzh, nzl, h, l32);
+        nlive = gemm2_blk32<RP, true>(y, y2, trans, jp, zh, zl, ln, nzh, nzl, h, l32);
         ++ran;
       } else {
         nlive = zsplit32(ln, nzh, nzl);
@@ -694,7 +712,7 @@ __device__ __forceinline__ unsigned consume32(const float* tile, int np,
     u32x4 nzh[2], nzl[2];
     bool nlive;
     if (live) {
-      nlive = gemm2_blk32<RP, true>(y, trans, jp, zh, zl, ln, nzh, nzl, h, l32);
+      nlive = gemm2_blk32<RP, true>(y, y2, trans, jp, zh, zl, ln, nzh, nzl, h, l32);
       ++ran;
     } else {
       nlive = zsplit32(ln, nzh, nzl);
@@ -715,11 +733,11 @@ __device__ __forceinline__ unsigned step32(const float* __restrict__ cur, float*
                                            const float* __restrict__ trans, int64_t j0,
                                            int64_t jb1, const u32x4 (&xh)[RP / 16],
                                            const u32x4 (&xl)[RP / 16], floatx16 (&y)[Cfg32<RP>::CB],
-                                           int wave, int lane, int h, int l32) {
+                                           floatx16& y2, int wave, int lane, int h, int l32) {
   constexpr int NT = Cfg32<RP>::NT;
   if (nxt) stage32<RP>(nxt, rowm, trans, j0 + NT, jb1, wave, lane);
   const int64_t left = (jb1 - j0 + 31) / 32;
-  return consume32<RP>(cur, left < NT / 32 ? (int)left : NT / 32, xh, xl, y, h, l32);
+  return consume32<RP>(cur, left < NT / 32 ? (int)left : NT / 32, xh, xl, y, y2, h, l32);
 }
 
 template <int RP>
@@ -744,7 +762,9 @@ __global__ __launch_bounds__(64 * Cfg32<RP>::WAVES) void bx32_kernel(
 
   u32x4 xh[RP / 16], xl[RP / 16];
   load_x32<RP>(xh, xl, X, rows, row0, h, l32);
-  floatx16 y[CB];
+  floatx16 y[CB], y2;  // y2: second accumulator of the one-column-block case
+#pragma unroll
+  for (int v = 0; v < 16; ++v) y2[v] = 0.f;
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
@@ -757,8 +777,9 @@ __global__ __launch_bounds__(64 * Cfg32<RP>::WAVES) void bx32_kernel(
     __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the tile have landed
     __syncthreads();                // every wave's have; the other buffer is free again
     ran += step32<RP>(smem + cur * C::TILE, j0 + C::NT < jb1 ? smem + (cur ^ 1) * C::TILE : nullptr,
-                      rowm, trans, j0, jb1, xh, xl, y, wave, lane, h, l32);
+                      rowm, trans, j0, jb1, xh, xl, y, y2, wave, lane, h, l32);
   }
+  if constexpr (CB == 1) y[0] += y2;
 
   float* Y = Ypart + (int64_t)split * y_stride;
 #pragma unroll
