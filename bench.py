@@ -189,7 +189,7 @@ def main():
     ap.add_argument("--kernel-mb", action="store_true",
                     help="time the fused kernel alone at the shape of the paper's kernel table")
     ap.add_argument("--split-bf16", action="store_true",
-                    help="opt-in variant at r_p = 16..256: both products of the dense kernel as "
+                    help="opt-in variant at r_p = 16..512: both products of the dense kernel as "
                          "three bf16 MFMA products of two-term splits (fp32 stays the default)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first run one plain 1 GiB copy kernel (calibrates rocprofv3 byte counters)")
@@ -272,7 +272,7 @@ def main():
     dense_tflops = dense_alg_flops / dense_s / 1e12 if dense_s > 0 else 0.0
     dense_equiv_kernel = dense["flops"] / dense_s / 1e12 if dense_s > 0 else 0.0
     sparse_gbs = sparse["bytes"] / (sparse["ms"] / 1e3) / 1e9 if sparse["ms"] > 0 else 0.0
-    split = args.split_bf16 and rp in (16, 32, 64, 128, 256)
+    split = args.split_bf16 and rp in (16, 32, 64, 128, 256, 512)
     # The split option runs both products as three bf16 products each: every algorithmic flop
     # costs three bf16 flops, so its roofline peak is a third of the bf16 MFMA peak.
     peak = PEAK_BF16_MFMA / 3.0 if split else PEAK_FP32_MFMA
@@ -318,8 +318,8 @@ def main():
             "unit": "TFLOP/s",
             "frac": dense_tflops / peak,
             "traffic": measured_traffic(args.config, "split_bf16" if split else "fp32"),
-            "kernel": (("bx_kernel<256>" if rp == 256 else f"bx32_kernel<{rp}>") if split
-                       else f"dense_kernel<{rp}>"),
+            "kernel": ({256: "bx_kernel<256>", 512: "bxl_kernel"}.get(rp, f"bx32_kernel<{rp}>")
+                       if split else f"dense_kernel<{rp}>"),
             "launches": dense["launches"],
             "avg_launch_ms": dense["ms"] / max(1, dense["launches"]),
             "flops_per_launch": dense_alg_flops / max(1, dense["launches"]),

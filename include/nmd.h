@@ -48,8 +48,9 @@ enum {
                           nmd_reset                                                       */
   NMD_FLAG_TIMING = 2u, /* record HIP events around every kernel class (see
                           nmd_get_kernel_timing); adds a few microseconds per step        */
-  NMD_FLAG_SPLIT_BF16 = 4u /* padded rank r_p in {16, 32, 64, 128, 256}, i.e. r <= 32 or
-                          r in 49..64, 65..128, 193..256 (other ranks ignore it): both
+  NMD_FLAG_SPLIT_BF16 = 4u /* padded rank r_p in {16, 32, 64, 128, 256, 512}, i.e. r <= 32
+                          or r in 49..64, 65..128, 193..256, 449..512 (other ranks ignore
+                          it): both
                           products of the dense contraction,
                           L = A B_J^T and max(0, L) B_J, run on bf16 MFMA with every
                           operand split in two (x = bf16(x) + bf16(x - bf16(x)), three
@@ -201,7 +202,7 @@ int nmd_rectified_contraction(const float* A, int64_t rows, const float* B, int6
  * fp32 accumulation): the counterpart, for a dense max(0, A B^T), of the paper's TF32 fused
  * kernels (Sec. 4.2, kernel throughput table).  Relative error of each output about 2^-16 of
  * the sum of the magnitudes of its terms.  A: device rows x r, B: device blk x r, Y: device
- * rows x r (all fp32 row-major), r in {16, 32, 64, 128, 256}.  work: caller-owned device workspace
+ * rows x r (all fp32 row-major), r in {16, 32, 64, 128, 256, 512}.  work: caller-owned device workspace
  * of nmd_bf16x3_workspace_floats(blk, r) floats, overwritten with the split panel (row-major
  * and transposed copies).  Asynchronous on hip_stream; allocates nothing.  NMD_EINVAL on NULL
  * pointers, another r or bad sizes, NMD_EDEVICE if a launch fails.
@@ -212,7 +213,7 @@ int nmd_rectified_contraction_bf16x3(const float* A, int64_t rows, const float* 
 /*
  * nmd_bf16x3_workspace_floats - floats of workspace nmd_rectified_contraction_bf16x3 needs for
  * a blk-row panel at rank r: blk r + 32 ceil(blk / 32) max(r, 32).  -1 if blk < 1 or r is not
- * one of 16, 32, 64, 128, 256.
+ * one of 16, 32, 64, 128, 256, 512.
  */
 int64_t nmd_bf16x3_workspace_floats(int64_t blk, int32_t r);
 

@@ -18,8 +18,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnmd.so")
-SOURCES = ["host.cpp", "dense.hip", "dense_bf16.hip", "dense_large.hip", "objective.hip",
-           "sparse.hip", "solve.hip", "layout.hip"]
+SOURCES = ["host.cpp", "dense.hip", "dense_bf16.hip", "dense_large.hip", "dense_bf16_large.hip",
+           "objective.hip", "sparse.hip", "solve.hip", "layout.hip"]
 ARCH = "gfx950"
 
 # Packed-fp32 instructions are kept out of the generated code on purpose.
@@ -36,7 +36,8 @@ HIPFLAGS = [
 # register files on every panel block at small ranks (measured: r = 16 at 53% of the fp32 MFMA
 # peak instead of 72%).  The r_p >= 320 instantiations (dense_large.hip) keep the default: at
 # one wave per SIMD the output tiles sit in accumulation registers and leave the VGPRs to the
-# operands (r = 512: 3-4% faster).  The split-bf16 kernels (dense_bf16.hip) follow the fp32 one.
+# operands (r = 512: 3-4% faster).  The split-bf16 kernels follow the fp32 ones: dense_bf16.hip
+# (r_p <= 256) with the VGPR form, dense_bf16_large.hip (r_p = 512) with the default.
 EXTRA_FLAGS = {"dense.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
                "dense_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 

@@ -1,10 +1,15 @@
 // Launchers of the rectified contraction with both products on split bf16 MFMA (kernels in
-// dense_bf16.h): the 32 x 32 x 16 form at padded ranks 16 to 128, the 16 x 16 x 32 form at 256.
+// dense_bf16.h): the 32 x 32 x 16 form at padded ranks 16 to 128, the 16 x 16 x 32 form at 256
+// (and, from dense_bf16_large.hip, at 512).
 
 #include "dense_bf16.h"
 #include "nmd_internal.h"
 
 namespace nmd {
+
+bool bf16x3_rank(int rp) {
+  return rp == 16 || rp == 32 || rp == 64 || rp == 128 || rp == 256 || rp == 512;
+}
 
 int64_t bf16x3_work_floats(int64_t blk, int rp) {
   return blk * rp + (blk + 31) / 32 * 32 * (rp < 32 ? 32 : rp);
@@ -21,6 +26,8 @@ hipError_t launch_bf16x3(const float* X, int64_t rows, const float* P, int64_t b
     case 64: return BX32(64);
     case 128: return BX32(128);
     case 256: return BX(256);
+    case 512: return launch_bf16x3_512(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, live,
+                                       st);
   }
 #undef BX
 #undef BX32

@@ -233,7 +233,7 @@ struct nmd_ctx {
   float *A2 = nullptr, *B2 = nullptr, *VA2 = nullptr, *VB2 = nullptr;
   std::vector<std::pair<int, bool>> enqueued;  // (step id, W-step) of the call's steps, in order
   float* Ypart = nullptr;
-  float* Pbx = nullptr;  // split-bf16 panel copies (NMD_FLAG_SPLIT_BF16 at r_p = 16..256)
+  float* Pbx = nullptr;  // split-bf16 panel copies (NMD_FLAG_SPLIT_BF16 at r_p = 16..512)
   int64_t ypart_floats = 0;
   float* scratch = nullptr;
   int64_t scratch_floats = 0;
@@ -418,8 +418,7 @@ int ensure_device(nmd_ctx* c) {
     need = std::max(need, nsplit_for(c->n, c->m, c->rp, c->dense_slots) * c->n);
     c->ypart_floats = need * rp;
     // the split-bf16 option covers the padded ranks the bf16x3 kernels support
-    const bool bx = (c->opt.flags & NMD_FLAG_SPLIT_BF16) &&
-                    (rp == 16 || rp == 32 || rp == 64 || rp == 128 || rp == 256);
+    const bool bx = (c->opt.flags & NMD_FLAG_SPLIT_BF16) && nmd::bf16x3_rank(rp);
     if (dalloc(&c->Ypart, c->ypart_floats) != hipSuccess ||
         (bx && dalloc(&c->Pbx, nmd::bf16x3_work_floats(std::max(c->m, c->n), rp)) != hipSuccess)) {
       free_device(c);
@@ -1021,7 +1020,7 @@ int nmd_rectified_contraction(const float* A, int64_t rows, const float* B, int6
 }
 
 int64_t nmd_bf16x3_workspace_floats(int64_t blk, int32_t r) {
-  if (blk < 1 || (r != 16 && r != 32 && r != 64 && r != 128 && r != 256)) return -1;
+  if (blk < 1 || !nmd::bf16x3_rank(r)) return -1;
   return nmd::bf16x3_work_floats(blk, r);
 }
 
@@ -1032,8 +1031,9 @@ int nmd_rectified_contraction_bf16x3(const float* A, int64_t rows, const float* 
     return fail(nullptr, NMD_EINVAL, "A, B, work and Y must be non-NULL");
   if (rows < 1 || blk < 1 || rows > INT32_MAX)
     return fail(nullptr, NMD_EINVAL, "rows and blk must be >= 1");
-  if (r != 16 && r != 32 && r != 64 && r != 128 && r != 256)
-    return fail(nullptr, NMD_EINVAL, "the bf16x3 contraction needs r in {16, 32, 64, 128, 256} (got %d)", r);
+  if (!nmd::bf16x3_rank(r))
+    return fail(nullptr, NMD_EINVAL,
+                "the bf16x3 contraction needs r in {16, 32, 64, 128, 256, 512} (got %d)", r);
   hipError_t e = nmd::launch_bf16x3(A, rows, B, blk, r, work, Y, 0, 1, 1.0f, nullptr,
                                     (hipStream_t)hip_stream);
   if (e != hipSuccess) return fail(nullptr, NMD_EDEVICE, "launch failed: %s", hipGetErrorString(e));

@@ -46,16 +46,22 @@ hipError_t launch_dense(const float* X, int64_t rows, const float* P, int64_t bl
                         float* Ypart, int64_t y_stride, int nsplit, float sgn,
                         unsigned long long* gemm2_blocks, hipStream_t st);
 
-// Both products on split bf16 MFMA (dense_bf16.h), rp in {16, 32, 64, 128, 256}: splits the blk x rp
+// Both products on split bf16 MFMA (dense_bf16.h), rp in {16, 32, 64, 128, 256, 512}
+// (bf16x3_rank): splits the blk x rp
 // panel P into `work` (bf16x3_work_floats(blk, rp) floats: row-major and transposed split
 // copies), then Y_s = sgn * max(0, X P_s^T) P_s for each of nsplit panel ranges starting at
 // bf16x3_pair_start(s, nsplit, blk) (whole 32-row pairs).  When `live` is not NULL, 8 per
 // 16 x 32 tile of max(0, L) with a positive entry is added to it (its 16 x 4 slices).
+bool bf16x3_rank(int rp);
 int64_t bf16x3_work_floats(int64_t blk, int rp);
 int64_t bf16x3_pair_start(int s, int nsplit, int64_t blk);
 hipError_t launch_bf16x3(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
                          float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
                          unsigned long long* live, hipStream_t st);
+// The rp = 512 form (dense_bf16_large.hip), same contract.
+hipError_t launch_bf16x3_512(const float* X, int64_t rows, const float* P, int64_t blk,
+                             float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
+                             unsigned long long* live, hipStream_t st);
 
 // Sparse correction: for every item, c = sum over its entries of (s - min(0, x_row . p_j)) p_j;
 // a row with a single item gets Y[row] = c (accumulate = 0) or Y[row] += c (accumulate = 1);

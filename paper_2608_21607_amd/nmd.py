@@ -248,7 +248,7 @@ def rectified_contraction_bf16x3(A, B, Y=None, work=None, stream=None):
     blk = B.shape[0]
     need = bf16x3_workspace_floats(blk, r)
     if need < 0:
-        raise NmdError(EINVAL, f"the bf16x3 contraction needs r in (16, 32, 64, 128, 256), got {r}")
+        raise NmdError(EINVAL, f"the bf16x3 contraction needs r in (16, 32, 64, 128, 256, 512), got {r}")
     if Y is None:
         Y = torch.empty((rows, r), dtype=torch.float32, device=A.device)
     if work is None:

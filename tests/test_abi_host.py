@@ -135,7 +135,7 @@ def test_rectified_contraction_argument_checks(L):
     assert L.nmd_rectified_contraction(fake, 10, fake, 0, 16, fake, None) == nmd.EINVAL
     assert L.nmd_rectified_contraction(None, 10, fake, 10, 16, fake, None) == nmd.EINVAL
     bx = L.nmd_rectified_contraction_bf16x3
-    for r in (8, 48, 96, 192, 512):  # both-products bf16 contraction: r in 16, 32, 64, 128, 256
+    for r in (8, 48, 96, 192, 384, 1024):  # both-products bf16: r in 16, 32, 64, 128, 256, 512
         assert bx(fake, 10, fake, 10, r, fake, fake, None) == nmd.EINVAL
     assert bx(fake, 10, fake, 10, 64, None, fake, None) == nmd.EINVAL
     assert bx(fake, 10, fake, 0, 64, fake, fake, None) == nmd.EINVAL
@@ -144,11 +144,12 @@ def test_rectified_contraction_argument_checks(L):
 def test_bf16x3_workspace_size(L):
     """blk r + 32 ceil(blk / 32) max(r, 32) floats: the row-major copy and the pair-padded,
     at least 32-column transposed copy."""
-    for blk, r in ((1, 16), (40, 16), (1, 32), (31, 64), (32, 64), (33, 128), (2500, 128), (8192, 256)):
+    for blk, r in ((1, 16), (40, 16), (1, 32), (31, 64), (32, 64), (33, 128), (2500, 128), (8192, 256),
+                   (1, 512), (33, 512)):
         assert nmd.bf16x3_workspace_floats(blk, r) == blk * r + 32 * ((blk + 31) // 32) * max(r, 32)
     assert nmd.bf16x3_workspace_floats(0, 64) == -1
     assert nmd.bf16x3_workspace_floats(10, 8) == -1
-    assert nmd.bf16x3_workspace_floats(10, 512) == -1
+    assert nmd.bf16x3_workspace_floats(10, 384) == -1
 
 
 def test_dense_blocks_before_device_use(L):
