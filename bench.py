@@ -42,7 +42,8 @@ KERNEL_SOURCES = {
     "fp32": [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f)
              for f in ("tile.h", "dense_kernel.h", "dense.hip")],
     "split_bf16": [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f)
-                   for f in ("tile.h", "dense_kernel.h", "dense_bf16.h", "dense_bf16.hip")],
+                   for f in ("tile.h", "dense_kernel.h", "dense_bf16.h", "dense_bf16.hip",
+                             "dense_bf16_large.hip")],
 }
 
 
@@ -318,7 +319,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": dense_tflops / peak,
             "traffic": measured_traffic(args.config, "split_bf16" if split else "fp32"),
-            "kernel": ({256: "bx_kernel<256>", 512: "bxl_kernel"}.get(rp, f"bx32_kernel<{rp}>")
+            "kernel": ((f"bxl_kernel<{rp}>" if rp >= 256 else f"bx32_kernel<{rp}>")
                        if split else f"dense_kernel<{rp}>"),
             "launches": dense["launches"],
             "avg_launch_ms": dense["ms"] / max(1, dense["launches"]),

@@ -202,9 +202,10 @@ int nmd_rectified_contraction(const float* A, int64_t rows, const float* B, int6
  * fp32 accumulation): the counterpart, for a dense max(0, A B^T), of the paper's TF32 fused
  * kernels (Sec. 4.2, kernel throughput table).  Relative error of each output about 2^-16 of
  * the sum of the magnitudes of its terms.  A: device rows x r, B: device blk x r, Y: device
- * rows x r (all fp32 row-major), r in {16, 32, 64, 128, 256, 512}.  work: caller-owned device workspace
- * of nmd_bf16x3_workspace_floats(blk, r) floats, overwritten with the split panel (row-major
- * and transposed copies).  Asynchronous on hip_stream; allocates nothing.  NMD_EINVAL on NULL
+ * rows x r (all fp32 row-major), r in {16, 32, 64, 128, 256, 512}.  work: caller-owned device
+ * workspace of nmd_bf16x3_workspace_floats(blk, r) floats, overwritten with the split panel
+ * (row-major and, at r <= 128, transposed copies).  Asynchronous on hip_stream; allocates
+ * nothing.  NMD_EINVAL on NULL
  * pointers, another r or bad sizes, NMD_EDEVICE if a launch fails.
  */
 int nmd_rectified_contraction_bf16x3(const float* A, int64_t rows, const float* B, int64_t blk,
@@ -212,8 +213,9 @@ int nmd_rectified_contraction_bf16x3(const float* A, int64_t rows, const float* 
 
 /*
  * nmd_bf16x3_workspace_floats - floats of workspace nmd_rectified_contraction_bf16x3 needs for
- * a blk-row panel at rank r: blk r + 32 ceil(blk / 32) max(r, 32).  -1 if blk < 1 or r is not
- * one of 16, 32, 64, 128, 256, 512.
+ * a blk-row panel at rank r: blk r + 32 ceil(blk / 32) max(r, 32) for r <= 128, blk r for
+ * r = 256 and 512 (whose kernels read the row-major copy transposed in LDS).  -1 if blk < 1 or
+ * r is not one of 16, 32, 64, 128, 256, 512.
  */
 int64_t nmd_bf16x3_workspace_floats(int64_t blk, int32_t r);
 

@@ -5,22 +5,12 @@
 // accumulated in fp32; the dropped lo lo terms and the split remainders are about 2^-16 of
 // sum |a_k b_k| per output.
 //
-// Work unit: a wave holds 16 rows of X and takes the panel 32 rows (a j-pair) at a time.
-//   * First product, v_mfma_f32_16x16x32_bf16 with srcA = panel rows, srcB = X rows: the two
-//     16 x 16 L^T tiles of the pair in six accumulator chains.  Lane (q, l16), register v holds
-//     L[i = l16][j = 4q + v] (first tile) and L[i = l16][j = 16 + 4q + v] (second tile).
-//   * Those eight values, rectified and split, are the srcA operand of one K = 32 MFMA of the
-//     second product: A[i = l16][k = 8q + e] with k <-> panel row jrow(q, e) = 4q + e (e < 4),
-//     16 + 4q + e - 4 (e >= 4).  Its srcB, B[k][16 cb + l16] = P[jrow(q, e)][16 cb + l16], comes
-//     from a transposed copy of the pair (eight panel rows of one column per 16 bytes), so one
-//     ds_read_b128 reads it.  The accumulator layout is the fp32 kernel's:
-//     Y[4q + v][16 cb + l16] in register v of y[cb].
-//   * A j-pair whose rectified tile is all zero skips the second product.
-// Panel layouts, written once per call by bx_split_kernel:
-//   * row-major: row j as RP/8 groups of (8 hi, 8 lo) bf16 (4 RP bytes per row);
-//   * transposed: pair p as 4 (q) x 2 (hi, lo) x RP (column) groups of the 8 values
-//     P[32p + jrow(q, e)][c], e = 0..7 (128 RP bytes per pair; rows past the panel are zero).
-// Both stream through LDS in double-buffered tiles of NT rows (direct global->LDS loads).
+// This header holds the helpers of both forms and the 32 x 32 x 16 form (padded ranks 16 to
+// 128); the 16 x 16 x 32 form (256 and 512) is in dense_bf16_large.hip.  In the 16 x 16 form a
+// wave holds 16 rows of X and takes the panel 32 rows at a time: its first product gives lane
+// (q, l16), register v, L[i = l16][j = 4q + v] and L[i = l16][j = 16 + 4q + v]; those eight
+// values, rectified and split (zsplit), are the srcA operand of one K = 32 MFMA of the second
+// product, A[i = l16][k = 8q + e] with k <-> panel row 4q + e (e < 4), 16 + 4q + e - 4 (e >= 4).
 
 #pragma once
 
@@ -31,18 +21,6 @@ namespace bx {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
-
-template <int RP>
-struct Cfg {
-  static constexpr int WAVES = 8;                     // two per SIMD
-  static constexpr int ROWS = 16 * WAVES;             // rows of X per workgroup
-  static constexpr int NT = RP >= 256 ? 32 : (RP >= 128 ? 64 : (RP >= 64 ? 128 : 256));
-  static constexpr int LS = RP + 4;                   // row-major tile stride, floats
-  static constexpr int TB = 32 * RP;                  // transposed pair block, floats
-  static constexpr int TILE = NT * LS + (NT / 32) * TB;  // one buffer, floats
-  static constexpr int G = RP >= 256 ? 2 : (RP / 16 >= 4 ? 4 : RP / 16);  // column blocks per group
-  static_assert(RP % 32 == 0 && NT % 32 == 0 && NT % WAVES == 0, "shape");
-};
 
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 typedef __attribute__((ext_vector_type(2))) float floatx2;
@@ -70,47 +48,6 @@ __device__ __forceinline__ floatx4 mfma(u32x4 a, u32x4 b, floatx4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16(a), as_bf16(b), c, 0, 0, 0);
 }
 
-// Panel row of the pair's k-slot e for lane group q.
-__device__ __forceinline__ int jrow(int q, int e) { return e < 4 ? 4 * q + e : 12 + 4 * q + e; }
-
-// Both split layouts of the blk x RP panel P: threads [0, blk RP/8) write the row-major groups,
-// the next npair * 4 * RP threads the transposed pair blocks.
-template <int RP>
-__global__ __launch_bounds__(256) void bx_split_kernel(const float* __restrict__ P, int64_t blk,
-                                                       int64_t npair, u32x4* __restrict__ rowm,
-                                                       u32x4* __restrict__ trans) {
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t na = blk * (RP / 8);
-  if (gid < na) {
-    const int64_t row = gid / (RP / 8);
-    const int g = (int)(gid - row * (RP / 8));
-    const float4 a = *reinterpret_cast<const float4*>(P + row * RP + 8 * g);
-    const float4 b = *reinterpret_cast<const float4*>(P + row * RP + 8 * g + 4);
-    const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-    u32x4 hi, lo;
-    split8(x, hi, lo);
-    rowm[row * (RP / 4) + 2 * g] = hi;
-    rowm[row * (RP / 4) + 2 * g + 1] = lo;
-    return;
-  }
-  const int64_t t = gid - na;
-  if (t >= npair * 4 * RP) return;
-  const int64_t p = t / (4 * RP);
-  const int rem = (int)(t - p * 4 * RP);
-  const int q = rem / RP, c = rem - q * RP;
-  float x[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int64_t j = 32 * p + jrow(q, e);
-    x[e] = j < blk ? P[j * RP + c] : 0.f;
-  }
-  u32x4 hi, lo;
-  split8(x, hi, lo);
-  u32x4* blkp = trans + p * (8 * RP);
-  blkp[(2 * q) * RP + c] = hi;
-  blkp[(2 * q + 1) * RP + c] = lo;
-}
-
 // X rows of one wave as split srcB operands: xh[t], xl[t] = X[row0 + l16][32t + 8q .. + 7].
 template <int RP>
 __device__ __forceinline__ void load_x(u32x4 (&xh)[RP / 32], u32x4 (&xl)[RP / 32],
@@ -128,48 +65,6 @@ __device__ __forceinline__ void load_x(u32x4 (&xh)[RP / 32], u32x4 (&xl)[RP / 32
     }
     split8(x, xh[t], xl[t]);
   }
-}
-
-// Load panel rows j0 .. j0 + NT - 1 into one buffer: the row-major rows (padded stride, rows at
-// or past jb1 zero-filled) and the transposed blocks of the pairs that hold rows below jb1.
-template <int RP, class C>
-__device__ __forceinline__ void stage_t(float* dst, const float* __restrict__ rowm,
-                                        const float* __restrict__ trans, int64_t j0, int64_t jb1,
-                                        int wave, int lane) {
-  constexpr int CPR = RP / 4;              // 16-byte chunks per row
-  constexpr int IPR = (CPR + 63) / 64;     // instructions per row
-#pragma unroll
-  for (int u = 0; u < C::NT / C::WAVES; ++u) {
-    const int r = wave + C::WAVES * u;
-    const int64_t j = j0 + r;
-#pragma unroll
-    for (int k = 0; k < IPR; ++k) {
-      const int c = 64 * k + lane;
-      if (j < jb1) {
-        if (CPR % 64 == 0 || c < CPR)
-          __builtin_amdgcn_global_load_lds((glb_void*)(rowm + j * RP + 4 * c),
-                                           (lds_void*)(dst + r * C::LS + 256 * k), 16, 0, 0);
-      } else if (CPR % 64 == 0 || c < CPR) {
-        *reinterpret_cast<float4*>(dst + r * C::LS + 4 * c) = float4{0.f, 0.f, 0.f, 0.f};
-      }
-    }
-  }
-  const int64_t p0 = j0 / 32;
-  const int64_t left = (jb1 - j0 + 31) / 32;
-  const int np = left < C::NT / 32 ? (int)left : C::NT / 32;
-  const int ninst = np * (C::TB / 256);  // 64 chunks of 16 bytes per instruction
-  float* tdst = dst + C::NT * C::LS;
-  const float* tsrc = trans + p0 * C::TB;
-  for (int i = wave; i < ninst; i += C::WAVES)
-    __builtin_amdgcn_global_load_lds((glb_void*)(tsrc + 256 * i + 4 * lane),
-                                     (lds_void*)(tdst + 256 * i), 16, 0, 0);
-}
-
-template <int RP>
-__device__ __forceinline__ void stage(float* dst, const float* __restrict__ rowm,
-                                      const float* __restrict__ trans, int64_t j0, int64_t jb1,
-                                      int wave, int lane) {
-  stage_t<RP, Cfg<RP>>(dst, rowm, trans, j0, jb1, wave, lane);
 }
 
 template <int RP>
@@ -215,50 +110,9 @@ __device__ __forceinline__ void stage32(float* dst, const float* __restrict__ ro
                                      (lds_void*)(tdst + 256 * i), 16, 0, 0);
 }
 
-// First product of pair jp: the two 16 x 16 L^T tiles (six accumulator chains, panel reads two
-// chunks ahead).
-template <int RP>
-__device__ __forceinline__ void gemm1_pair(floatx4& l0, floatx4& l1, const float* tile, int jp,
-                                           const u32x4 (&xh)[RP / 32],
-                                           const u32x4 (&xl)[RP / 32], int q, int l16) {
-  using C = Cfg<RP>;
-  constexpr int KC = RP / 32;
-  constexpr int LA = KC < 2 ? KC : 2;
-  const u32x4* r0 = reinterpret_cast<const u32x4*>(tile + (32 * jp + l16) * C::LS);
-  const u32x4* r1 = reinterpret_cast<const u32x4*>(tile + (32 * jp + 16 + l16) * C::LS);
-  floatx4 a0[3], a1[3];
-#pragma unroll
-  for (int h = 0; h < 3; ++h) a0[h] = a1[h] = floatx4{0.f, 0.f, 0.f, 0.f};
-  u32x4 h0[KC], o0[KC], h1[KC], o1[KC];
-#pragma unroll
-  for (int t = 0; t < LA; ++t) {
-    h0[t] = r0[2 * (4 * t + q)];
-    o0[t] = r0[2 * (4 * t + q) + 1];
-    h1[t] = r1[2 * (4 * t + q)];
-    o1[t] = r1[2 * (4 * t + q) + 1];
-  }
-#pragma unroll
-  for (int t = 0; t < KC; ++t) {
-    if (t + LA < KC) {
-      h0[t + LA] = r0[2 * (4 * (t + LA) + q)];
-      o0[t + LA] = r0[2 * (4 * (t + LA) + q) + 1];
-      h1[t + LA] = r1[2 * (4 * (t + LA) + q)];
-      o1[t + LA] = r1[2 * (4 * (t + LA) + q) + 1];
-    }
-    a0[0] = mfma(h0[t], xh[t], a0[0]);
-    a1[0] = mfma(h1[t], xh[t], a1[0]);
-    a0[1] = mfma(h0[t], xl[t], a0[1]);
-    a1[1] = mfma(h1[t], xl[t], a1[1]);
-    a0[2] = mfma(o0[t], xh[t], a0[2]);
-    a1[2] = mfma(o1[t], xh[t], a1[2]);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  l0 = a0[0] + (a0[1] + a0[2]);
-  l1 = a1[0] + (a1[1] + a1[2]);
-}
-
-// The rectified pair tile as the second product's split srcA operands; whether any of it is
-// positive (wave-uniform).
+// 16 x 16 form: the rectified 16 x 32 tile (l0: panel rows 4q + v, l1: 16 + 4q + v) as the
+// second product's split srcA operands, in the k order above; whether any of it is positive
+// (wave-uniform).
 __device__ __forceinline__ bool zsplit(floatx4 l0, floatx4 l1, u32x4& zh, u32x4& zl) {
   const float z[8] = {l0[0] > 0.f ? l0[0] : 0.f, l0[1] > 0.f ? l0[1] : 0.f,
                       l0[2] > 0.f ? l0[2] : 0.f, l0[3] > 0.f ? l0[3] : 0.f,
@@ -269,149 +123,9 @@ __device__ __forceinline__ bool zsplit(floatx4 l0, floatx4 l1, u32x4& zh, u32x4&
   return __ballot(pos) != 0;
 }
 
-// Second product of pair jp with operands (zh, zl); the rectify and split of the next pair's
-// tile (m0, m1) is placed after the first group of MFMAs, so that its vector work issues while
-// they run.
-template <int RP>
-__device__ __forceinline__ bool gemm2_pair(floatx4 (&y)[RP / 16], const float* trans, int jp,
-                                           u32x4 zh, u32x4 zl, floatx4 m0, floatx4 m1,
-                                           u32x4& nzh, u32x4& nzl, int q, int l16) {
-  using C = Cfg<RP>;
-  constexpr int CB = RP / 16, G = C::G;
-  const u32x4* bh = reinterpret_cast<const u32x4*>(trans + jp * C::TB) + (2 * q) * RP + l16;
-  const u32x4* bl = bh + RP;
-  u32x4 nh[G], nl[G];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    nh[g] = bh[16 * g];
-    nl[g] = bl[16 * g];
-  }
-  bool live = false;
-#pragma unroll
-  for (int cb0 = 0; cb0 < CB; cb0 += G) {
-    u32x4 ch[G], cl[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      ch[g] = nh[g];
-      cl[g] = nl[g];
-    }
-    if (cb0 + G < CB) {
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        nh[g] = bh[16 * (cb0 + G + g)];
-        nl[g] = bl[16 * (cb0 + G + g)];
-      }
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g) y[cb0 + g] = mfma(zh, ch[g], y[cb0 + g]);
-#pragma unroll
-    for (int g = 0; g < G; ++g) y[cb0 + g] = mfma(zh, cl[g], y[cb0 + g]);
-#pragma unroll
-    for (int g = 0; g < G; ++g) y[cb0 + g] = mfma(zl, ch[g], y[cb0 + g]);
-    if (cb0 == 0) live = zsplit(m0, m1, nzh, nzl);
-  }
-  return live;
-}
-
-// Both products over the pairs of one staged tile, software-pipelined: the first product of pair
-// jp + 1 is issued before the second product of pair jp, whose MFMAs then cover the rectify and
-// split of pair jp + 1.  Returns the pairs whose second product ran.
-template <int RP>
-__device__ __forceinline__ unsigned consume(const float* tile, int np, const u32x4 (&xh)[RP / 32],
-                                            const u32x4 (&xl)[RP / 32], floatx4 (&y)[RP / 16],
-                                            int q, int l16) {
-  using C = Cfg<RP>;
-  const float* trans = tile + C::NT * C::LS;
-  unsigned ran = 0;
-  floatx4 l0, l1;
-  gemm1_pair<RP>(l0, l1, tile, 0, xh, xl, q, l16);
-  u32x4 zh, zl;
-  bool live = zsplit(l0, l1, zh, zl);
-  for (int jp = 0; jp < np; ++jp) {
-    floatx4 m0 = floatx4{0.f, 0.f, 0.f, 0.f}, m1 = floatx4{0.f, 0.f, 0.f, 0.f};
-    if (jp + 1 < np) gemm1_pair<RP>(m0, m1, tile, jp + 1, xh, xl, q, l16);
-    u32x4 nzh, nzl;
-    bool nlive;
-    if (live) {
-      nlive = gemm2_pair<RP>(y, trans, jp, zh, zl, m0, m1, nzh, nzl, q, l16);
-      ++ran;
-    } else {
-      nlive = zsplit(m0, m1, nzh, nzl);
-    }
-    zh = nzh;
-    zl = nzl;
-    live = nlive;
-  }
-  return ran;
-}
-
-// One pipeline step: start the loads of the next tile into `nxt` (when not null) and consume
-// `cur`.  The restrict qualifiers let the compiler keep the reads of `cur` from waiting on the
-// direct loads into `nxt`.
-template <int RP>
-__device__ __forceinline__ unsigned step(const float* __restrict__ cur, float* __restrict__ nxt,
-                                     const float* __restrict__ rowm,
-                                     const float* __restrict__ trans, int64_t j0, int64_t jb1,
-                                     const u32x4 (&xh)[RP / 32], const u32x4 (&xl)[RP / 32],
-                                     floatx4 (&y)[RP / 16], int wave, int lane, int q, int l16) {
-  constexpr int NT = Cfg<RP>::NT;
-  if (nxt) stage<RP>(nxt, rowm, trans, j0 + NT, jb1, wave, lane);
-  const int64_t left = (jb1 - j0 + 31) / 32;
-  return consume<RP>(cur, left < NT / 32 ? (int)left : NT / 32, xh, xl, y, q, l16);
-}
-
 // Panel rows of split s: [start(s), start(s + 1)), starts rounded down to whole pairs.
 __host__ __device__ __forceinline__ int64_t pair_start(int s, int nsplit, int64_t blk) {
   return s >= nsplit ? blk : ((int64_t)s * blk / nsplit) / 32 * 32;
-}
-
-template <int RP>
-__global__ __launch_bounds__(64 * Cfg<RP>::WAVES) void bx_kernel(
-    const float* __restrict__ X, int64_t rows, const float* __restrict__ rowm,
-    const float* __restrict__ trans, int64_t blk, float* __restrict__ Ypart, int64_t y_stride,
-    int nsplit, int64_t row_tiles, float sgn, unsigned long long* __restrict__ live_slices) {
-  using C = Cfg<RP>;
-  constexpr int CB = RP / 16;
-  __shared__ __attribute__((aligned(16))) float smem[2 * C::TILE];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int q = lane >> 4, l16 = lane & 15;
-
-  const int64_t logical = xcd_logical(blockIdx.x, (int64_t)gridDim.x);
-  const int split = (int)(logical / row_tiles);
-  const int64_t rt = logical - (int64_t)split * row_tiles;
-  const int64_t jb0 = pair_start(split, nsplit, blk);
-  const int64_t jb1 = pair_start(split + 1, nsplit, blk);
-  const int64_t row0 = rt * C::ROWS + (int64_t)wave * 16;
-
-  u32x4 xh[RP / 32], xl[RP / 32];
-  load_x<RP>(xh, xl, X, rows, row0, q, l16);
-  floatx4 y[CB];
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb) y[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  if (jb0 < jb1) stage<RP>(smem, rowm, trans, jb0, jb1, wave, lane);
-  int cur = 0;
-  unsigned ran = 0;
-  for (int64_t j0 = jb0; j0 < jb1; j0 += C::NT, cur ^= 1) {
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the tile have landed
-    __syncthreads();                // every wave's have; the other buffer is free again
-    ran += step<RP>(smem + cur * C::TILE, j0 + C::NT < jb1 ? smem + (cur ^ 1) * C::TILE : nullptr, rowm,
-             trans, j0, jb1, xh, xl, y, wave, lane, q, l16);
-  }
-
-  float* Y = Ypart + (int64_t)split * y_stride;
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int64_t row = row0 + 4 * q + v;
-    if (row < rows) {
-#pragma unroll
-      for (int cb = 0; cb < CB; ++cb) Y[row * RP + 16 * cb + l16] = sgn * y[cb][v];
-    }
-  }
-  // a live 16 x 32 tile counts as its eight 16 x 4 slices of max(0, L)
-  if (live_slices && lane == 0 && ran) atomicAdd(live_slices, 8ull * ran);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -448,8 +162,8 @@ __device__ __forceinline__ int jrow32(int a, int h, int e) {
   return 16 * a + 8 * (e >> 2) + 4 * h + (e & 3);
 }
 
-// Row-major and transposed split copies for the 32-row form (row-major as bx_split_kernel; the
-// transposed blocks are Cfg32<RP>::RPC columns wide, zero past RP).
+// Row-major and transposed split copies for the 32-row form (row-major: row j as RP/8 groups of
+// 8 hi then 8 lo bf16; the transposed blocks are Cfg32<RP>::RPC columns wide, zero past RP).
 template <int RP>
 __global__ __launch_bounds__(256) void bx32_split_kernel(const float* __restrict__ P, int64_t blk,
                                                          int64_t npair, u32x4* __restrict__ rowm,
@@ -798,30 +512,6 @@ __global__ __launch_bounds__(64 * Cfg32<RP>::WAVES) void bx32_kernel(
 }  // namespace bx
 
 // Launchers: the panel split, then the contraction kernel over row_tiles x nsplit workgroups.
-template <int RP>
-static hipError_t bx_launch_t(const float* X, int64_t rows, const float* P, int64_t blk,
-                              float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
-                              unsigned long long* live, hipStream_t st) {
-  using C = bx::Cfg<RP>;
-  const int64_t npair = (blk + 31) / 32;
-  float* rowm = work;
-  float* trans = work + blk * RP;
-  const int64_t threads = blk * (RP / 8) + npair * 4 * RP;
-  hipLaunchKernelGGL(bx::bx_split_kernel<RP>, dim3((unsigned)((threads + 255) / 256)), dim3(256),
-                     0, st, P, blk, npair, reinterpret_cast<bx::u32x4*>(rowm),
-                     reinterpret_cast<bx::u32x4*>(trans));
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const int64_t row_tiles = (rows + C::ROWS - 1) / C::ROWS;
-  const int64_t total = row_tiles * nsplit;
-  if (total <= 0) return hipSuccess;
-  if (total > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(bx::bx_kernel<RP>, dim3((unsigned)total), dim3(64 * C::WAVES), 0, st, X, rows,
-                     rowm, trans, blk, Ypart, y_stride, nsplit, row_tiles, sgn, live);
-  return hipGetLastError();
-}
-
-// Ranks up to 128: 32 rows of X per wave on the 32 x 32 x 16 MFMA.
 template <int RP>
 static hipError_t bx32_launch_t(const float* X, int64_t rows, const float* P, int64_t blk,
                                 float* work, float* Ypart, int64_t y_stride, int nsplit,

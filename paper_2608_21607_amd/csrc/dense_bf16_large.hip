@@ -1,6 +1,7 @@
-// The both-products split-bf16 contraction at r_p = 512 (helpers in dense_bf16.h): one wave per
-// SIMD, whose output tiles sit in accumulation registers (compiled like dense_large.hip), and a
-// single row-major split panel read both ways.
+// The both-products split-bf16 contraction at r_p = 256 and 512 in the 16 x 16 x 32 form (helpers
+// in dense_bf16.h), with a single row-major split panel read both ways.  Compiled with the
+// default register allocation: at 512 the single wave per SIMD keeps its output tiles in
+// accumulation registers.
 
 #include "dense_bf16.h"
 #include "nmd_internal.h"
@@ -9,15 +10,15 @@ namespace nmd {
 namespace bx {
 
 // ---------------------------------------------------------------------------------------------
-// r_p = 512 (16 x 16 x 32 form, one wave per SIMD, 16 rows of X per wave).  Only the row-major
-// split panel is kept: the second product reads its operand, eight consecutive panel rows of one
-// column per lane, out of the same LDS rows with the transposing LDS read of gfx950
+// r_p = 256 (two waves per SIMD) and 512 (one wave per SIMD), 16 rows of X per wave.  Only the
+// row-major split panel is kept: the second product reads its operand, eight consecutive panel
+// rows of one column per lane, out of the same LDS rows with the transposing LDS read of gfx950
 // (ds_read_b64_tr_b16), so a panel element costs 4 bytes of traffic (bf16 hi and lo), as in the
-// fp32 kernel.  A 32-row block takes two 32 KB stages (the two 256-column halves of its rows);
-// a ring of four slots holds the block being computed and the next one, loaded while the
-// current one runs.  Each stage loads exactly 8 chunks of 1 KB per wave (rows past the panel
-// read a clamped row; their rectified values are masked to zero), so the per-wave load count
-// per stage is fixed for the vmcnt waits.
+// fp32 kernel.  A 32-row block takes r_p / 256 stages of 32 KB (its 256-column halves at 512); a
+// ring of four slots holds the block being computed and the next one, loaded while the current
+// one runs.  Each stage loads exactly 32 chunks of 1 KB (8 per wave at 512, 4 at 256; rows past
+// the panel read a clamped row, and their rectified values are masked to zero), so the per-wave
+// load count per stage is fixed for the vmcnt waits.
 //
 // Stage row layout (1 KB: 256 columns of one panel row): 32 hi chunks then 32 lo chunks of
 // 8 columns, chunk c of row r stored at c ^ f(r), f(r) = 2 (r & 3) + ((r >> 2) & 1).  Both reads
@@ -25,14 +26,17 @@ namespace bx {
 // one chunk) because f is a permutation of 0..7, the transposed read's (rows 4q..4q+3, two
 // adjacent chunks) because f(r) >> 1 takes four values there.
 
+template <int RP_>
 struct CfgL {
-  static constexpr int RP = 512;
-  static constexpr int WAVES = 4;                     // one per SIMD
+  static constexpr int RP = RP_;
+  static constexpr int WAVES = RP >= 512 ? 4 : 8;    // one wave per SIMD at 512, two at 256
   static constexpr int ROWS = 16 * WAVES;             // rows of X per workgroup
+  static constexpr int H = RP / 256;                  // 256-column stages per 32-row block
   static constexpr int SLOT = 8192;                   // floats per stage (32 KB)
   static constexpr int LPW = SLOT / 256 / WAVES;      // 1 KB direct loads per wave per stage
   static constexpr int KC = RP / 32;                  // 32-wide k chunks
   static constexpr int CB = RP / 16;                  // 16-column blocks of Y
+  static_assert(RP == 256 || RP == 512, "rank");
 };
 
 __device__ __forceinline__ int swz_l(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
@@ -50,11 +54,11 @@ __device__ __forceinline__ void ring_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Row-major split panel for r_p = 512: per row, for each 256-column half, the hi chunks of its
-// 32 groups of 8 columns, then their lo chunks.
+// Row-major split panel: per row, for each 256-column half, the hi chunks of its 32 groups of 8
+// columns, then their lo chunks.
+template <int RP>
 __global__ __launch_bounds__(256) void bxl_split_kernel(const float* __restrict__ P, int64_t blk,
                                                         u32x4* __restrict__ rowm) {
-  constexpr int RP = 512;
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (gid >= blk * (RP / 8)) return;
   const int64_t row = gid / (RP / 8);
@@ -71,9 +75,10 @@ __global__ __launch_bounds__(256) void bxl_split_kernel(const float* __restrict_
 
 // Issue the direct loads of half h (columns 256 h ..) of the 32-row block at panel row j0 into
 // `slot`: row r of the block goes to slot row r, its chunk c to position c ^ f(r).
+template <int RP>
 __device__ __forceinline__ void stage_l(float* slot, int h, const float* __restrict__ rowm,
                                         int64_t j0, int64_t blk, int wave, int lane) {
-  using C = CfgL;
+  using C = CfgL<RP>;
 #pragma unroll
   for (int u = 0; u < C::LPW; ++u) {
     const int r = wave + C::WAVES * u;          // row of the block (0..31)
@@ -87,9 +92,10 @@ __device__ __forceinline__ void stage_l(float* slot, int h, const float* __restr
 
 // First-product chunks of one k-half (a stage slot) into the six chains: a0 for panel rows
 // 0..15 of the block, a1 for rows 16..31 (hi x hi, hi x lo, lo x hi each).
+template <int RP>
 __device__ __forceinline__ void gemm1_half(floatx4 (&a0)[3], floatx4 (&a1)[3], const float* slot,
-                                           int half, const u32x4 (&xh)[CfgL::KC],
-                                           const u32x4 (&xl)[CfgL::KC], int q, int l16) {
+                                           int half, const u32x4 (&xh)[RP / 32],
+                                           const u32x4 (&xl)[RP / 32], int q, int l16) {
   const u32x4* r0 = reinterpret_cast<const u32x4*>(slot + 256 * l16);
   const u32x4* r1 = reinterpret_cast<const u32x4*>(slot + 256 * (16 + l16));
   const int sw = swz_l(l16);  // rows l16 and 16 + l16 share f
@@ -150,7 +156,8 @@ __device__ __forceinline__ void load_b_tr(u32x4& bh, u32x4& bl, const char* base
 }
 
 // Second product for one column half (a stage slot).
-__device__ __forceinline__ void gemm2_half(floatx4 (&y)[CfgL::CB], const float* slot, int half,
+template <int RP>
+__device__ __forceinline__ void gemm2_half(floatx4 (&y)[RP / 16], const float* slot, int half,
                                            u32x4 zh, u32x4 zl, int q, int l16) {
   const char* base = reinterpret_cast<const char*>(slot);
   const int jr = 4 * q + (l16 >> 2), jc = l16 & 3, sw = swz_l(jr);
@@ -180,12 +187,14 @@ __device__ __forceinline__ void gemm2_half(floatx4 (&y)[CfgL::CB], const float* 
   }
 }
 
-__global__ __launch_bounds__(64 * CfgL::WAVES) void bxl_kernel(
+template <int RP>
+__global__ __launch_bounds__(64 * CfgL<RP>::WAVES) void bxl_kernel(
     const float* __restrict__ X, int64_t rows, const float* __restrict__ rowm, int64_t blk,
     float* __restrict__ Ypart, int64_t y_stride, int nsplit, int64_t row_tiles, float sgn,
     unsigned long long* __restrict__ live_slices) {
-  using C = CfgL;
+  using C = CfgL<RP>;
   __shared__ __attribute__((aligned(16))) float ring[4 * C::SLOT];
+  static_assert(C::H <= 2, "the ring holds two blocks of two stages");
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -199,7 +208,7 @@ __global__ __launch_bounds__(64 * CfgL::WAVES) void bxl_kernel(
   const int64_t row0 = rt * C::ROWS + (int64_t)wave * 16;
 
   u32x4 xh[C::KC], xl[C::KC];
-  load_x<C::RP>(xh, xl, X, rows, row0, q, l16);
+  load_x<RP>(xh, xl, X, rows, row0, q, l16);
   floatx4 y[C::CB];
   {
     // zero the output tiles with an MFMA of zero operands: their loop-carried values then start
@@ -212,28 +221,33 @@ __global__ __launch_bounds__(64 * CfgL::WAVES) void bxl_kernel(
   const int64_t nblk = (jb1 - jb0 + 31) / 32;
   unsigned ran = 0;
   if (nblk > 0) {
-    stage_l(ring, 0, rowm, jb0, blk, wave, lane);
-    stage_l(ring + C::SLOT, 1, rowm, jb0, blk, wave, lane);
+    // stage h of block b goes to slot (H b + h) mod 4: at H = 2 the ring holds this block and
+    // the next, at H = 1 the block and the next three slots
+#pragma unroll
+    for (int h = 0; h < C::H; ++h) stage_l<RP>(ring + h * C::SLOT, h, rowm, jb0, blk, wave, lane);
     for (int64_t b = 0; b < nblk; ++b) {
       const int64_t j0 = jb0 + 32 * b;
-      float* s0 = ring + 2 * (int)(b & 1) * C::SLOT;
-      float* s1 = s0 + C::SLOT;
-      // half 0 of this block landed for every wave; every wave is done with the previous block
-      ring_barrier<C::LPW>();
+      const float* s0 = ring + (int)((C::H * b) & 3) * C::SLOT;
+      const float* s1 = C::H > 1 ? s0 + C::SLOT : s0;
+      // stage 0 of this block landed for every wave; every wave is done with the previous block
+      ring_barrier<(C::H - 1) * C::LPW>();
       const bool more = b + 1 < nblk;
       if (more) {
-        float* n0 = ring + 2 * (int)((b + 1) & 1) * C::SLOT;
-        stage_l(n0, 0, rowm, j0 + 32, blk, wave, lane);
-        stage_l(n0 + C::SLOT, 1, rowm, j0 + 32, blk, wave, lane);
+#pragma unroll
+        for (int h = 0; h < C::H; ++h)
+          stage_l<RP>(ring + (int)((C::H * (b + 1) + h) & 3) * C::SLOT, h, rowm, j0 + 32, blk,
+                      wave, lane);
       }
       floatx4 a0[3], a1[3];
 #pragma unroll
       for (int h = 0; h < 3; ++h) a0[h] = a1[h] = floatx4{0.f, 0.f, 0.f, 0.f};
-      gemm1_half(a0, a1, s0, 0, xh, xl, q, l16);
-      // half 1 of this block landed for every wave (the next block's loads stay in flight)
-      if (more) ring_barrier<2 * C::LPW>();
-      else ring_barrier<0>();
-      gemm1_half(a0, a1, s1, 1, xh, xl, q, l16);
+      gemm1_half<RP>(a0, a1, s0, 0, xh, xl, q, l16);
+      if constexpr (C::H > 1) {
+        // stage 1 of this block landed for every wave (the next block's loads stay in flight)
+        if (more) ring_barrier<C::H * C::LPW>();
+        else ring_barrier<0>();
+        gemm1_half<RP>(a0, a1, s1, 1, xh, xl, q, l16);
+      }
       const floatx4 l0 = a0[0] + (a0[1] + a0[2]);
       const floatx4 l1 = a1[0] + (a1[1] + a1[2]);
       const int valid = (int)(jb1 - j0);  // panel rows of this block inside the range
@@ -246,8 +260,8 @@ __global__ __launch_bounds__(64 * CfgL::WAVES) void bxl_kernel(
       u32x4 zh, zl;
       if (zsplit(m0, m1, zh, zl)) {
         ++ran;
-        gemm2_half(y, s0, 0, zh, zl, q, l16);
-        gemm2_half(y, s1, 1, zh, zl, q, l16);
+        gemm2_half<RP>(y, s0, 0, zh, zl, q, l16);
+        if constexpr (C::H > 1) gemm2_half<RP>(y, s1, 1, zh, zl, q, l16);
       }
     }
   }
@@ -268,22 +282,33 @@ __global__ __launch_bounds__(64 * CfgL::WAVES) void bxl_kernel(
 }  // namespace bx
 
 // r_p = 512: staged four-slot form.
-hipError_t launch_bf16x3_512(const float* X, int64_t rows, const float* P, int64_t blk,
+template <int RP>
+static hipError_t bxl_launch(const float* X, int64_t rows, const float* P, int64_t blk,
                              float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
                              unsigned long long* live, hipStream_t st) {
-  using C = bx::CfgL;
-  const int64_t threads = blk * (C::RP / 8);
-  hipLaunchKernelGGL(bx::bxl_split_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
-                     st, P, blk, reinterpret_cast<bx::u32x4*>(work));
+  using C = bx::CfgL<RP>;
+  const int64_t threads = blk * (RP / 8);
+  hipLaunchKernelGGL(bx::bxl_split_kernel<RP>, dim3((unsigned)((threads + 255) / 256)), dim3(256),
+                     0, st, P, blk, reinterpret_cast<bx::u32x4*>(work));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t row_tiles = (rows + C::ROWS - 1) / C::ROWS;
   const int64_t total = row_tiles * nsplit;
   if (total <= 0) return hipSuccess;
   if (total > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(bx::bxl_kernel, dim3((unsigned)total), dim3(64 * C::WAVES), 0, st, X, rows,
-                     work, blk, Ypart, y_stride, nsplit, row_tiles, sgn, live);
+  hipLaunchKernelGGL(bx::bxl_kernel<RP>, dim3((unsigned)total), dim3(64 * C::WAVES), 0, st, X,
+                     rows, work, blk, Ypart, y_stride, nsplit, row_tiles, sgn, live);
   return hipGetLastError();
+}
+
+hipError_t launch_bf16x3_staged(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
+                                float* work, float* Ypart, int64_t y_stride, int nsplit,
+                                float sgn, unsigned long long* live, hipStream_t st) {
+  switch (rp) {
+    case 256: return bxl_launch<256>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, live, st);
+    case 512: return bxl_launch<512>(X, rows, P, blk, work, Ypart, y_stride, nsplit, sgn, live, st);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace nmd

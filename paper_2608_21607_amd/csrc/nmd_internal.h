@@ -58,10 +58,11 @@ int64_t bf16x3_pair_start(int s, int nsplit, int64_t blk);
 hipError_t launch_bf16x3(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
                          float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
                          unsigned long long* live, hipStream_t st);
-// The rp = 512 form (dense_bf16_large.hip), same contract.
-hipError_t launch_bf16x3_512(const float* X, int64_t rows, const float* P, int64_t blk,
-                             float* work, float* Ypart, int64_t y_stride, int nsplit, float sgn,
-                             unsigned long long* live, hipStream_t st);
+// The rp = 256 and 512 form (dense_bf16_large.hip), same contract; at these ranks `work` holds
+// only the row-major split copy (bf16x3_work_floats = blk * rp).
+hipError_t launch_bf16x3_staged(const float* X, int64_t rows, const float* P, int64_t blk, int rp,
+                                float* work, float* Ypart, int64_t y_stride, int nsplit,
+                                float sgn, unsigned long long* live, hipStream_t st);
 
 // Sparse correction: for every item, c = sum over its entries of (s - min(0, x_row . p_j)) p_j;
 // a row with a single item gets Y[row] = c (accumulate = 0) or Y[row] += c (accumulate = 1);

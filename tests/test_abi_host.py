@@ -142,11 +142,12 @@ def test_rectified_contraction_argument_checks(L):
 
 
 def test_bf16x3_workspace_size(L):
-    """blk r + 32 ceil(blk / 32) max(r, 32) floats: the row-major copy and the pair-padded,
-    at least 32-column transposed copy."""
-    for blk, r in ((1, 16), (40, 16), (1, 32), (31, 64), (32, 64), (33, 128), (2500, 128), (8192, 256),
-                   (1, 512), (33, 512)):
+    """blk r + 32 ceil(blk / 32) max(r, 32) floats at r <= 128: the row-major copy and the
+    pair-padded, at least 32-column transposed copy; blk r at r = 256 and 512 (row-major only)."""
+    for blk, r in ((1, 16), (40, 16), (1, 32), (31, 64), (32, 64), (33, 128), (2500, 128)):
         assert nmd.bf16x3_workspace_floats(blk, r) == blk * r + 32 * ((blk + 31) // 32) * max(r, 32)
+    for blk, r in ((1, 256), (8192, 256), (33, 512), (50000, 512)):
+        assert nmd.bf16x3_workspace_floats(blk, r) == blk * r
     assert nmd.bf16x3_workspace_floats(0, 64) == -1
     assert nmd.bf16x3_workspace_floats(10, 8) == -1
     assert nmd.bf16x3_workspace_floats(10, 384) == -1

@@ -227,11 +227,12 @@ def test_rectified_contraction_bf16x3_sparse_and_zero(r):
     assert not torch.any(Y0 != 0).item()
 
 
-def test_rectified_contraction_bf16x3_workspace_reuse():
+@pytest.mark.parametrize("r", [64, 256, 512])
+def test_rectified_contraction_bf16x3_workspace_reuse(r):
     """Two calls in a row on one workspace, the second with a shorter panel: the second result
     depends only on its own inputs."""
-    g = np.random.default_rng(77)
-    r = 64
+    _say("rectified_contraction_bf16x3 workspace reuse", 200, 700, r)
+    g = np.random.default_rng(77 + r)
     A = g.standard_normal((200, r)).astype(np.float32)
     B1 = g.standard_normal((700, r)).astype(np.float32)
     B2 = g.standard_normal((45, r)).astype(np.float32)
