@@ -196,7 +196,8 @@ SPLIT_TOL = 1e-4
 
 @pytest.mark.parametrize("r,rows,blk", [(16, 700, 999), (32, 300, 1000), (64, 257, 517), (128, 129, 33),
                                          (128, 1000, 2500), (256, 340, 517), (64, 5, 7),
-                                         (512, 300, 517), (512, 70, 31), (512, 129, 96)])
+                                         (512, 300, 517), (512, 70, 31), (512, 129, 96),
+                                         (256, 5, 7), (256, 1, 1), (512, 1, 1), (512, 17, 33)])
 def test_rectified_contraction_bf16x3(r, rows, blk):
     """Both products on split bf16: N(0,1) factors (about half of L positive, every 16 x 32
     tile live), ragged rows and panel sizes (a panel shorter than one 32-row pair included)."""
