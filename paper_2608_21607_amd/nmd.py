@@ -241,7 +241,7 @@ def bf16x3_workspace_floats(blk, r) -> int:
 
 def rectified_contraction_bf16x3(A, B, Y=None, work=None, stream=None):
     """Y = max(0, A B^T) B with both products on split bf16 MFMA (A: rows x r, B: blk x r,
-    float32 CUDA tensors, r in {16, 32, 64, 128, 256}; work: float32 workspace of at least
+    float32 CUDA tensors, r in {16, 32, 64, 128, 256, 512}; work: float32 workspace of at least
     bf16x3_workspace_floats(blk, r) elements)."""
     import torch
     rows, r = A.shape
