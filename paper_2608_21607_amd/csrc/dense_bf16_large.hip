@@ -250,7 +250,8 @@ __global__ __launch_bounds__(64 * CfgL<RP>::WAVES) void bxl_kernel(
       }
       const floatx4 l0 = a0[0] + (a0[1] + a0[2]);
       const floatx4 l1 = a1[0] + (a1[1] + a1[2]);
-      const int valid = (int)(jb1 - j0);  // panel rows of this block inside the range
+      // panel rows of this block inside the range (only values below 32 mask anything)
+      const int valid = (int)(jb1 - j0 < 32 ? jb1 - j0 : 32);
       floatx4 m0, m1;
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
