@@ -160,18 +160,18 @@ def config5():
     return p, S, S.T.tocsr()
 
 
-def test_config5_first_steps_sampled(config5):
+def test_config5_full_sweep_stepwise_sampled(config5):
     """The 500000 x 50000 co-occurrence workload at rank 512 (about 100M nonzeros, Zipf rows
-    and columns, the heaviest rows fully dense): the first four steps of sweep 0, each checked
-    on sampled rows."""
+    and columns, the heaviest rows fully dense): all 38 steps of sweep 0, each checked on
+    sampled rows."""
     p, S, ST = config5
-    _say("config 5 full size, first steps checked on sampled rows", p.m, p.n, p.nnz)
-    stepwise_sampled(p, S, ST, n_steps=4, nsample=64)
+    _say("config 5 full sweep, every step checked on sampled rows", p.m, p.n, p.nnz)
+    stepwise_sampled(p, S, ST, nsample=48)
 
 
-def test_config5_split_bf16_first_steps_sampled(config5):
-    """The split-bf16 option on the co-occurrence workload at rank 512: the first two steps of
-    sweep 0 (one of each factor), each checked on sampled rows."""
+def test_config5_split_bf16_full_sweep_stepwise_sampled(config5):
+    """The split-bf16 option on the co-occurrence workload at rank 512: all 38 steps of
+    sweep 0, each checked on sampled rows."""
     p, S, ST = config5
-    _say("config 5 split bf16, first steps checked on sampled rows", p.m, p.n, p.nnz)
-    stepwise_sampled(p, S, ST, n_steps=2, nsample=64, flags=nmd.FLAG_SPLIT_BF16)
+    _say("config 5 split bf16, every step checked on sampled rows", p.m, p.n, p.nnz)
+    stepwise_sampled(p, S, ST, nsample=48, flags=nmd.FLAG_SPLIT_BF16)
