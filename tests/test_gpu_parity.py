@@ -161,6 +161,27 @@ def test_rectified_contraction_paper_shape_sampled(r):
     assert rel(Y[idx].cpu().numpy(), want) < 2e-5
 
 
+@pytest.mark.parametrize("split", [False, True])
+@pytest.mark.parametrize("rows,blk", [(500_000, 7142), (50_000, 16130)])
+def test_rectified_contraction_cooccurrence_shapes_sampled(rows, blk, split):
+    """r = 512 at the co-occurrence workload's step shapes (W-step: 500000 rows against a 7142-row
+    panel; H-step: 50000 rows against 16130), N(0,1) factors so that every tile runs the second
+    product; 64 sampled output rows against the oracle, fp32 and split bf16."""
+    r = 512
+    _say("rectified_contraction co-occurrence shape", rows, blk, r, "split" if split else "fp32")
+    g = torch.Generator(device="cuda").manual_seed(rows + blk)
+    A = torch.randn((rows, r), generator=g, device="cuda")
+    B = torch.randn((blk, r), generator=g, device="cuda")
+    Y = nmd.rectified_contraction_bf16x3(A, B) if split else nmd.rectified_contraction(A, B)
+    torch.cuda.synchronize()
+    idx = np.random.default_rng(rows + blk).choice(rows, 64, replace=False)
+    want = salsa.rectified_contraction(A[idx].cpu().numpy(), B.cpu().numpy())
+    e = rel(Y[idx].cpu().numpy(), want)
+    print(f"r = 512 at {rows} x {blk} ({'split' if split else 'fp32'}): rel err {e:.2e}")
+    assert e < (SPLIT_TOL if split else 2e-5)
+    del A, B, Y
+
+
 def test_graph_tenth_two_sweeps_gathered_second_product():
     """The graph workload at a tenth of its size (13926 x 13926, r = 256, ~1.7M nonzeros), two
     stochastic sweeps.  Sweep 0 starts with S-hat = 0; in sweep 1 S-hat is sparse and positive,
