@@ -21,10 +21,12 @@ namespace bx {
 // load count per stage is fixed for the vmcnt waits.
 //
 // Stage row layout (1 KB: 256 columns of one panel row): 32 hi chunks then 32 lo chunks of
-// 8 columns, chunk c of row r stored at c ^ f(r), f(r) = 2 (r & 3) + ((r >> 2) & 1).  Both reads
-// then touch distinct 16-byte bank groups in each 128 bytes: the first product's (rows 0..7 of
-// one chunk) because f is a permutation of 0..7, the transposed read's (rows 4q..4q+3, two
-// adjacent chunks) because f(r) >> 1 takes four values there.
+// 8 columns, chunk c of row r stored at c ^ f(r), f(r) = 2 (r & 7) + ((r >> 3) & 1).  Both reads
+// then touch 16 distinct 16-byte bank groups in each 256 bytes: the first product's (rows 0..15
+// of one chunk) because f is a permutation of 0..15, the transposing read's (per 32 lanes, rows
+// 8p..8p+7, two adjacent chunks) because f(r) >> 1 = r & 7 takes eight values there.  Measured,
+// this halves the LDS bank-conflict cycles of a three-bit swizzle (2.67 to 1.33 per LDS
+// instruction) at the same speed or slightly better.
 
 template <int RP_>
 struct CfgL {
@@ -39,7 +41,7 @@ struct CfgL {
   static_assert(RP == 256 || RP == 512, "rank");
 };
 
-__device__ __forceinline__ int swz_l(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+__device__ __forceinline__ int swz_l(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
 
 // Workgroup barrier for the staged ring: this wave's direct loads up to the last N have landed
 // in LDS (vmcnt <= N) and its LDS reads are done (lgkmcnt 0), then s_barrier.  Unlike
