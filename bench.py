@@ -86,14 +86,15 @@ def kernel_mb(steps, warmup):
     """The fused rectified contraction Y = max(0, A B^T) B alone at the shape of the paper's
     kernel table: A 250000 x r, B 2500 x r, N(0,1) entries.  About half of L is positive, so
     every slice of the second product runs and the work is 4 rows blk r flops.  Timed for the
-    fp32 kernel and, from r = 32, for the kernel with both products on split bf16 (bf16x3)."""
+    fp32 kernel and for the kernel with both products on split bf16 (bf16x3), at the paper's
+    ranks 16 to 128 and at the workloads' ranks 256 and 512 (no paper figure there)."""
     import torch
 
     import paper_2608_21607_amd as nmd
 
     rows, blk = 250_000, 2500
     res = []
-    for r in (16, 32, 64, 128):
+    for r in (16, 32, 64, 128, 256, 512):
         g = torch.Generator(device="cuda").manual_seed(r)
         A = torch.randn((rows, r), generator=g, device="cuda")
         B = torch.randn((blk, r), generator=g, device="cuda")
@@ -123,7 +124,7 @@ def kernel_mb(steps, warmup):
                 row.update({"bf16x3_ms_per_launch": ms, "bf16x3_tflops": tflops,
                             "bf16x3_frac_of_peak": tflops / (PEAK_BF16_MFMA / 3.0)})
             log(f"r = {r} {tag}: {ms:.3f} ms per launch, {tflops:.1f} TFLOP/s")
-        h100, rtx = PAPER_FUSED_TF32[r]
+        h100, rtx = PAPER_FUSED_TF32.get(r, (None, None))
         row.update({"paper_tf32_h100_pcie": h100, "paper_tf32_rtx_pro_6000": rtx})
         res.append(row)
     return {"metric": "fused rectified contraction TFLOP/s (4 rows blk r per launch)",
