@@ -389,6 +389,28 @@ def test_stochastic_planted_reduced_split_bf16():
     assert ew < TOL and eh < TOL
 
 
+@pytest.mark.parametrize("r", [200, 480])
+def test_graph_small_split_bf16_padded_rank(r):
+    """The split-bf16 flag at ranks that pad (200 -> 256, 480 -> 512: the staged kernels with
+    zero padding columns) on the graph workload at a tenth of its size (two 8192-row blocks per
+    side), two stochastic sweeps, so that the second product runs in the second: W, H within
+    the 1e-4 bar.  (Much smaller problems at these ranks amplify any perturbation several-fold
+    per sweep, fp32 included, or leave the oracle's Gram matrices singular.)"""
+    p = gen.config(4, scale=0.1)
+    p.r = r
+    p.W0, p.H0 = gen.sign_constrained_init(p.m, p.n, r, float(p.val.mean()), 1004)
+    _say("graph workload at scale 0.1, split bf16, padded rank", p.m, p.n, r)
+    ctx = make_ctx(p, flags=nmd.FLAG_SPLIT_BF16)
+    W, H = dev(p.W0), dev(p.H0)
+    ctx.sweep(W, H, 2)
+    run, total, entries = ctx.dense_blocks()
+    assert total > 0 and run > 0 and entries == 0
+    Wo, Ho, _ = oracle_run(p, 2)
+    ew, eh = rel(W.cpu().numpy(), Wo), rel(H.cpu().numpy(), Ho)
+    print(f"split bf16, r = {r}, two sweeps: rel err W {ew:.2e} H {eh:.2e}, live slices {run / total:.3f}")
+    assert ew < TOL and eh < TOL
+
+
 def test_stochastic_three_sweeps_and_persistent_state():
     """Sweeps run in one call equal the same sweeps run one call at a time (the sweep counter
     and the momentum persist); after reset the first sweep repeats bit for bit."""
