@@ -277,16 +277,18 @@ __device__ __forceinline__ void load_blk32(Ops32<RP>& o, const float* tile, int 
 template <int RP>
 __device__ __forceinline__ floatx16 mma_blk32(const Ops32<RP>& o, const u32x4 (&xh)[RP / 16],
                                               const u32x4 (&xl)[RP / 16]) {
-  floatx16 a0, a1;
+  // one accumulator chain: at r_p <= 32 it is at most six MFMAs long, and adding two chains
+  // would cost 16 vector adds per block in a kernel that is bound by its vector work
+  floatx16 a0;
 #pragma unroll
-  for (int v = 0; v < 16; ++v) a0[v] = a1[v] = 0.f;
+  for (int v = 0; v < 16; ++v) a0[v] = 0.f;
 #pragma unroll
   for (int t = 0; t < RP / 16; ++t) {
     a0 = mfma32(o.h[t], xh[t], a0);
-    a1 = mfma32(o.h[t], xl[t], a1);
+    a0 = mfma32(o.h[t], xl[t], a0);
     a0 = mfma32(o.l[t], xh[t], a0);
   }
-  return a0 + a1;
+  return a0;
 }
 
 // Rectified block as the second product's split srcA operands (a = 0: registers 0..7,
@@ -295,18 +297,18 @@ __device__ __forceinline__ bool zsplit32(floatx16 l, u32x4 (&zh)[2], u32x4 (&zl)
   float z[16];
 #pragma unroll
   for (int v = 0; v < 16; ++v) z[v] = l[v] > 0.f ? l[v] : 0.f;
-  float s = 0.f;
 #pragma unroll
   for (int a = 0; a < 2; ++a) {
     float x[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      x[e] = z[8 * a + e];
-      s += x[e];
-    }
+    for (int e = 0; e < 8; ++e) x[e] = z[8 * a + e];
     split8(x, zh[a], zl[a]);
   }
-  return __ballot(s > 0.f) != 0;
+  // live when any hi part is nonzero (a value whose hi part rounds to zero has a zero lo part
+  // too, so it adds nothing to the second product)
+  const unsigned any = (zh[0][0] | zh[0][1]) | (zh[0][2] | zh[0][3]) | (zh[1][0] | zh[1][1]) |
+                       (zh[1][2] | zh[1][3]);
+  return __ballot(any != 0u) != 0;
 }
 
 // Second product of block jp into the 32 x 32 tiles of Y; with NEXT the next block's rectify
