@@ -34,26 +34,30 @@ METRIC = "ALS sweeps/sec and dense-equiv TFLOP/s (4mnr/sweep), % of fp32 MFMA pe
 # HBM traffic of the fused dense kernel, from two rocprofv3 --pmc passes (FETCH_SIZE, then
 # WRITE_SIZE) scaled by the same counters on a plain copy of known size; valid only for the
 # kernel sources it was taken on.
+_CSRC = os.path.join(ROOT, "paper_2608_21607_amd", "csrc")
+_SPLIT_SOURCES = ("tile.h", "dense_kernel.h", "dense_bf16.h", "dense_bf16.hip", "dense_bf16_large.hip")
+# (variant, workload) -> counter summary, and the sources of the dense kernel it measured
 TRAFFIC_FILES = {
-    "fp32": os.path.join(ROOT, "profiles", "dense_r256_graph139255_traffic.json"),
-    "split_bf16": os.path.join(ROOT, "profiles", "bf16x3_r256_graph139255_traffic.json"),
+    ("fp32", 4): os.path.join(ROOT, "profiles", "dense_r256_graph139255_traffic.json"),
+    ("split_bf16", 4): os.path.join(ROOT, "profiles", "bf16x3_r256_graph139255_traffic.json"),
+    ("fp32", 5): os.path.join(ROOT, "profiles", "dense_r512_cooc500000x50000_traffic.json"),
+    ("split_bf16", 5): os.path.join(ROOT, "profiles", "bf16x3_r512_cooc500000x50000_traffic.json"),
 }
 KERNEL_SOURCES = {
-    "fp32": [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f)
-             for f in ("tile.h", "dense_kernel.h", "dense.hip")],
-    "split_bf16": [os.path.join(ROOT, "paper_2608_21607_amd", "csrc", f)
-                   for f in ("tile.h", "dense_kernel.h", "dense_bf16.h", "dense_bf16.hip",
-                             "dense_bf16_large.hip")],
+    ("fp32", 4): [os.path.join(_CSRC, f) for f in ("tile.h", "dense_kernel.h", "dense.hip")],
+    ("split_bf16", 4): [os.path.join(_CSRC, f) for f in _SPLIT_SOURCES],
+    ("fp32", 5): [os.path.join(_CSRC, f) for f in ("tile.h", "dense_kernel.h", "dense_large.hip")],
+    ("split_bf16", 5): [os.path.join(_CSRC, f) for f in _SPLIT_SOURCES],
 }
 
 
-def kernel_source_hash(variant="fp32"):
+def kernel_source_hash(variant="fp32", config=4):
     """SHA-256 of the dense kernel's sources with // comments, trailing blanks and blank lines
     removed, so that it changes with the code and not with its comments."""
     import hashlib
     import re
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES[variant]:
+    for f in KERNEL_SOURCES[(variant, config)]:
         with open(f) as fh:
             for line in fh:
                 code = re.sub(r"//.*", "", line).rstrip()
@@ -65,12 +69,15 @@ def kernel_source_hash(variant="fp32"):
 def measured_traffic(config, variant="fp32"):
     """Bytes per dense-kernel launch from the committed counter summary, or None when the
     summary is missing, was taken on another workload, or the kernel has changed since."""
+    if (variant, config) not in TRAFFIC_FILES:
+        return None
     try:
-        with open(TRAFFIC_FILES[variant]) as f:
+        with open(TRAFFIC_FILES[(variant, config)]) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_sha256") != kernel_source_hash(variant) or t.get("config") != config:
+    if (t.get("kernel_source_sha256") != kernel_source_hash(variant, config)
+            or t.get("config") != config):
         return None
     return t.get("traffic_bytes_per_launch")
 
