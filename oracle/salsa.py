@@ -249,3 +249,47 @@ def zb_product(S_rows, X, P, j0, j1, rows=None):
     L = X[idx] @ PJ.T
     Sd = S_rows[:, j0:j1].tocsr()[idx].toarray()
     return z_update(Sd, L) @ PJ
+
+
+# --------------------------------------------------------------------------------------------
+# Step-size safeguard (a reading of Sec. 7 and the appendix on experimental settings)
+# --------------------------------------------------------------------------------------------
+
+def guarded_sweeps(S, ST, st: State, block_m, block_n, seed, n_sweeps, mode="stochastic",
+                   eta=1.0, gamma=0.0, tol=0.0, eta_min=0.0, row_chunk=4096):
+    """n_sweeps accepted sweeps under a step-size safeguard.
+
+    The paper notes that the stochastic updates can diverge when the step size is too large
+    (Sec. 7) and lowers the step size for the models that need it (appendix on experimental
+    settings, hyperparameter table); it gives no automatic rule.  The rule read here: after each
+    sweep the objective is evaluated; a sweep that leaves it above (1 + tol) times its value
+    before the sweep (or not finite) is undone -- both factors and the sweep counter return to
+    their values before the sweep -- the momentum buffers are cleared (a restart of the heavy
+    ball), the step size is halved, and the sweep is run again with the same block order.  The
+    comparison is made on the squared objective, f_new^2 > (1 + tol)^2 f_old^2.  Halving stops
+    with a ValueError once the step size would fall below eta_min.
+
+    Returns (eta, f, rejected): the step size in force at the end, the objective before the
+    first sweep and after each accepted sweep (n_sweeps + 1 values), and the list of
+    (sweep counter, step size, objective) of each rejected attempt."""
+    f_prev = objective(S, st.W, st.H)
+    fs = [f_prev]
+    rejected = []
+    done = 0
+    while done < n_sweeps:
+        saved = (st.A.copy(), st.B.copy(), st.t)
+        sweep(S, ST, st, block_m, block_n, seed, mode, eta, gamma, row_chunk)
+        f = objective(S, st.W, st.H)
+        if not (f * f <= (1.0 + tol) ** 2 * f_prev * f_prev):
+            rejected.append((saved[2], eta, f))
+            st.A, st.B, st.t = saved
+            st.VA = np.zeros_like(st.A)
+            st.VB = np.zeros_like(st.B)
+            eta = 0.5 * eta
+            if eta < eta_min:
+                raise ValueError("step size fell below eta_min")
+            continue
+        f_prev = f
+        fs.append(f)
+        done += 1
+    return eta, fs, rejected

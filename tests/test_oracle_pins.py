@@ -422,3 +422,178 @@ def test_balanced_partition():
         sizes = np.diff(b)
         assert b[0] == 0 and b[-1] == size
         assert sizes.max() <= block and sizes.max() - sizes.min() <= 1
+
+
+# --------------------------------------------------- metrics: eq. RMSE and eq. WJD by value
+def _hand_case():
+    """S and L whose eq. RMSE and eq. WJD were worked out by hand (Sec. 3.1).
+
+    S = [[2, 0, 0], [1, 3, 0]], L = [[1, 1, -2], [-1, 3, 1/2]], so S-hat = max(0, L) =
+    [[1, 1, 0], [0, 3, 1/2]].
+      S - S-hat = [[1, -1, 0], [1, 0, -1/2]]: squared sum 13/4; ||S||_F^2 = 14.
+      RMSE = sqrt(13/56).
+      sum min(S, S-hat) = 1 + 3 = 4; sum max(S, S-hat) = 2 + 1 + 1 + 3 + 1/2 = 15/2.
+      WJD = 1 - 4 / (15/2) = 7/15.
+    (A denominator of sum S = 6 would give 1/3, of sum S-hat = 11/2 would give 3/11.)"""
+    S = np.array([[2.0, 0.0, 0.0], [1.0, 3.0, 0.0]])
+    L = np.array([[1.0, 1.0, -2.0], [-1.0, 3.0, 0.5]])
+    return S, L, math.sqrt(13.0 / 56.0), 7.0 / 15.0
+
+
+def test_rmse_and_wjd_hand_computed_values():
+    """eq. RMSE and eq. WJD on a 2 x 3 case computed by hand, for the dense metrics and for the
+    row-tiled metrics over factors W H = L (W = I, H = L), at several row tilings."""
+    S, L, rmse_ref, wjd_ref = _hand_case()
+    Shat = np.maximum(0.0, L)
+    assert abs(salsa.rmse_dense(S, Shat) - rmse_ref) < 1e-15
+    assert abs(salsa.wjd_dense(S, Shat) - wjd_ref) < 1e-15
+    Ssp = sp.csr_matrix(S)
+    W = np.eye(2)
+    for chunk in (1, 2, 2048):
+        assert abs(salsa.rmse(Ssp, W, L, row_chunk=chunk) - rmse_ref) < 1e-15
+        assert abs(salsa.wjd(Ssp, W, L, row_chunk=chunk) - wjd_ref) < 1e-15
+    # the objective on the same case by hand: zeros of S contribute max(0, L)^2 = 1 and 1/4,
+    # nonzeros (S - L)^2 = 1, 4, 0: total 25/4, so f = sqrt(25/56) (eqs. auxCost, SLloss)
+    assert abs(salsa.objective(Ssp, W, L) - math.sqrt(25.0 / 56.0)) < 1e-15
+
+
+@pytest.mark.parametrize("c", [0.25, 0.5, 1.0, 2.0, 5.0])
+def test_rmse_and_wjd_of_a_scaled_reconstruction(c):
+    """Closed forms for S-hat = c S (c > 0): every entry has min = min(1, c) S_ij and
+    max = max(1, c) S_ij, so WJD = 1 - min(c, 1/c), and RMSE = |1 - c| (Sec. 3.1). Both
+    vanish exactly at c = 1 (S = S-hat)."""
+    rng = np.random.default_rng(8)
+    S = np.where(rng.random((31, 17)) < 0.2, rng.uniform(0.5, 4.0, (31, 17)), 0.0)
+    assert abs(salsa.wjd_dense(S, c * S) - (1.0 - min(c, 1.0 / c))) < 1e-14
+    assert abs(salsa.rmse_dense(S, c * S) - abs(1.0 - c)) < 1e-14
+    # tiled forms: L = c S written as W H with W = c I
+    Ssp = sp.csr_matrix(S)
+    for chunk in (1, 5, 2048):
+        assert abs(salsa.wjd(Ssp, c * np.eye(31), S, row_chunk=chunk)
+                   - (1.0 - min(c, 1.0 / c))) < 1e-14
+        assert abs(salsa.rmse(Ssp, c * np.eye(31), S, row_chunk=chunk) - abs(1.0 - c)) < 1e-14
+
+
+def test_tiled_metrics_match_dense_on_random_factors():
+    """The row-tiled metrics equal the dense definitions for any tiling (Sec. 3.1), on random
+    factors whose L has entries of both signs."""
+    rng = np.random.default_rng(9)
+    m, n, r = 23, 19, 3
+    S = np.where(rng.random((m, n)) < 0.25, rng.uniform(0.1, 3.0, (m, n)), 0.0)
+    W = rng.normal(size=(m, r))
+    H = rng.normal(size=(r, n))
+    Shat = np.maximum(0.0, W @ H)
+    Ssp = sp.csr_matrix(S)
+    for chunk in (1, 4, 7, 2048):
+        assert abs(salsa.rmse(Ssp, W, H, row_chunk=chunk) - salsa.rmse_dense(S, Shat)) < 1e-14
+        assert abs(salsa.wjd(Ssp, W, H, row_chunk=chunk) - salsa.wjd_dense(S, Shat)) < 1e-14
+
+
+# ------------------------------------ step codes -> blocks (eqs. lsqA_sto and its H analogue)
+def _projected_z(Sblk, Lblk):
+    """Z entry by entry as the nearest point to L_ij of the set {z : max(0, z) = S_ij}: the
+    single point S_ij when S_ij > 0, else the half-line z <= 0 (Sec. 3.2)."""
+    Z = np.empty_like(Lblk)
+    for i in range(Lblk.shape[0]):
+        for j in range(Lblk.shape[1]):
+            Z[i, j] = Sblk[i, j] if Sblk[i, j] > 0 else min(Lblk[i, j], 0.0)
+    return Z
+
+
+def test_step_codes_select_the_blocks_the_partition_names():
+    """Each step code updates the factor and block it names: +k fits every row of A to the
+    columns of column block k-1 (eq. lsqA_sto, eta = 1, no momentum), -k every row of B to
+    the rows of row block k-1 (the analogous update of Sec. 4.1). m != n and the row and
+    column blocks differ, so swapped bounds, a swapped sign convention or an off-by-one code
+    would all fail. Expected values: numpy.linalg.lstsq on blocks sliced by hand from bounds
+    worked out by hand from the balanced partition."""
+    m, n, r = 13, 11, 2
+    S, W, H = _rand_problem(m, n, r, 0.35, 31, sign_init=False)
+    Sd = S.toarray()
+    # balanced partition by hand: R = ceil(13/5) = 3 row blocks [floor(13k/3)], C = ceil(11/4)
+    # = 3 column blocks [floor(11k/3)]
+    rows = [0, 4, 8, 13]
+    cols = [0, 3, 7, 11]
+    assert list(partition.bounds(m, 5)) == rows and list(partition.bounds(n, 4)) == cols
+    codes = [+2, -3, +1, -1, +3, -2, +2]
+    st = salsa.State(W, H)
+    A = W.copy()
+    B = H.T.copy()
+    for code in codes:
+        salsa.run_steps(S, S.T.tocsr(), st, [code], 5, 4, 1.0, 0.0)
+        if code > 0:
+            j0, j1 = cols[code - 1], cols[code]
+            Z = _projected_z(Sd[:, j0:j1], A @ B[j0:j1].T)
+            A = np.linalg.lstsq(B[j0:j1], Z.T, rcond=None)[0].T
+        else:
+            i0, i1 = rows[-code - 1], rows[-code]
+            Z = _projected_z(Sd[i0:i1, :], A[i0:i1] @ B.T)
+            B = np.linalg.lstsq(A[i0:i1], Z, rcond=None)[0].T
+        np.testing.assert_allclose(st.A, A, rtol=1e-9, atol=1e-11)
+        np.testing.assert_allclose(st.B, B, rtol=1e-9, atol=1e-11)
+
+
+# ------------------------------------------- step-size safeguard (reading of Sec. 7, App. B)
+def _guard_case():
+    m, n, r = 240, 200, 8
+    row_ptr, col, val = gen.random_sparse(m, n, 0.1, 6)
+    S = salsa.csr_matrix(m, n, row_ptr, col, val)
+    W, H = gen.sign_constrained_init(m, n, r, float(val.mean()), 9)
+    return S, W, H
+
+
+def test_guard_without_rises_equals_plain_sweeps():
+    """When no sweep raises the objective beyond the tolerance the safeguard is inert: the
+    factors, momenta and counter equal those of plain sweeps exactly."""
+    S, W, H = _guard_case()
+    ST = S.T.tocsr()
+    a = salsa.State(W, H)
+    eta, fs, rej = salsa.guarded_sweeps(S, ST, a, 60, 50, 3, 3, "stochastic", 0.3, 0.5,
+                                        tol=0.5)
+    b = salsa.State(W, H)
+    for _ in range(3):
+        salsa.sweep(S, ST, b, 60, 50, 3, "stochastic", 0.3, 0.5)
+    assert rej == [] and eta == 0.3 and len(fs) == 4
+    for x, y in ((a.A, b.A), (a.B, b.B), (a.VA, b.VA), (a.VB, b.VB)):
+        assert np.array_equal(x, y)
+    assert a.t == b.t == 3
+    assert abs(fs[-1] - salsa.objective(S, b.W, b.H)) == 0.0
+
+
+def test_guard_replays_as_plain_sweeps_with_restarts():
+    """A diverging setting (eta = 1, momentum 0.9, 20-row blocks): the safeguard's result equals
+    plain sweeps in which each rejected attempt is dropped, the momenta are cleared and the step
+    size halved before the same sweep is repeated.  Each rejected attempt really raised the
+    objective and each accepted one did not (the rule's invariant), and the block order of a
+    repeated sweep is that of its counter."""
+    S, W, H = _guard_case()
+    ST = S.T.tocsr()
+    g = salsa.State(W, H)
+    eta_end, fs, rej = salsa.guarded_sweeps(S, ST, g, 20, 20, 3, 6, "stochastic", 1.0, 0.9)
+    assert len(rej) >= 3
+    st = salsa.State(W, H)
+    eta, f_prev, log = 1.0, salsa.objective(S, W, H), list(rej)
+    accepted = [f_prev]
+    for t in range(6):
+        while log and log[0][0] == t:
+            t_rej, eta_rej, f_rej = log.pop(0)
+            assert eta_rej == eta
+            trial = salsa.State(st.W, st.H)
+            trial.VA, trial.VB, trial.t = st.VA.copy(), st.VB.copy(), st.t
+            salsa.sweep(S, ST, trial, 20, 20, 3, "stochastic", eta, 0.9)
+            f_trial = salsa.objective(S, trial.W, trial.H)
+            assert f_trial == f_rej and f_trial > f_prev
+            st.VA[:] = 0.0
+            st.VB[:] = 0.0
+            eta *= 0.5
+        assert st.t == t
+        salsa.sweep(S, ST, st, 20, 20, 3, "stochastic", eta, 0.9)
+        f = salsa.objective(S, st.W, st.H)
+        assert f <= f_prev
+        accepted.append(f)
+        f_prev = f
+    assert eta == eta_end and accepted == fs
+    assert np.array_equal(st.A, g.A) and np.array_equal(st.B, g.B)
+    with pytest.raises(ValueError):
+        salsa.guarded_sweeps(S, ST, salsa.State(W, H), 20, 20, 3, 6, "stochastic", 1.0, 0.9,
+                             eta_min=0.3)
