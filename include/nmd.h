@@ -36,7 +36,9 @@ enum {
   NMD_EDEVICE = -3,    /* a HIP runtime call failed or no usable gfx950 device             */
   NMD_ENOTPD = -4,     /* a Gram matrix B_J^T B_J or A_I^T A_I was not positive definite    */
   NMD_ESTATE = -5,     /* call out of order (e.g. a sweep before nmd_set_sparse_csr)         */
-  NMD_ENONFINITE = -6  /* an updated factor entry was NaN or infinite                       */
+  NMD_ENONFINITE = -6, /* an updated factor entry was NaN or infinite                      */
+  NMD_ESTEP = -7       /* the step-size safeguard (NMD_FLAG_GUARD) would lower the step size
+                          below eta_min                                                     */
 };
 
 enum { NMD_DETERMINISTIC = 0, NMD_STOCHASTIC = 1 };
@@ -48,7 +50,7 @@ enum {
                           nmd_reset                                                       */
   NMD_FLAG_TIMING = 2u, /* record HIP events around every kernel class (see
                           nmd_get_kernel_timing); adds a few microseconds per step        */
-  NMD_FLAG_SPLIT_BF16 = 4u /* padded rank r_p in {16, 32, 64, 128, 256, 512}, i.e. r <= 32
+  NMD_FLAG_SPLIT_BF16 = 4u, /* padded rank r_p in {16, 32, 64, 128, 256, 512}, i.e. r <= 32
                           or r in 49..64, 65..128, 193..256, 449..512 (other ranks ignore
                           it): both
                           products of the dense contraction,
@@ -61,6 +63,23 @@ enum {
                           Needs nmd_bf16x3_workspace_floats(max(m, n), r_p) floats more
                           device memory.  It adds one small kernel per step, so on steps
                           too small to fill the GPU it can cost more than it saves         */
+  NMD_FLAG_SWEEP_OBJECTIVE = 8u, /* evaluate the objective (as nmd_objective) on the device
+                          before the first sweep of a call and after each sweep, into a
+                          device buffer read by nmd_get_sweep_objectives; no extra
+                          synchronisation.  Costs one objective evaluation per sweep         */
+  NMD_FLAG_GUARD = 16u /* step-size safeguard; implies NMD_FLAG_SWEEP_OBJECTIVE.  The paper
+                          notes that too large a step size makes the stochastic updates
+                          diverge (Sec. 7) and lowers the step size for the models that need
+                          it (appendix on experimental settings), without an automatic rule.
+                          Rule used here: a sweep that leaves the objective above
+                          (1 + guard_tol) times its value before the sweep, or not finite, is
+                          undone (W, H and the sweep counter return to their values before
+                          it), both momentum buffers are cleared, eta is halved and the sweep
+                          is run again with the same block order.  Decided on the device
+                          after each sweep; the host only learns of it when the call ends,
+                          so the sweeps enqueued after a rejected one are skipped and
+                          enqueued again.  The lowered eta persists in the context
+                          (nmd_get_step_size; nmd_reset restores the initial one)            */
 };
 
 typedef struct {
@@ -70,8 +89,14 @@ typedef struct {
   float eta;         /* step size eta > 0 of eq. lsqA_sto (1 = exact mini-batch solve)      */
   float momentum;    /* gamma in [0, 1): V <- gamma V + eta (X - A), A <- A + V            */
   uint32_t flags;    /* NMD_FLAG_* bits                                                     */
+  float guard_tol;   /* NMD_FLAG_GUARD: relative rise of the objective a sweep may cause
+                        before it is undone, >= 0 (0: any rise)                             */
+  float eta_min;     /* NMD_FLAG_GUARD: halving that would take eta below this fails with
+                        NMD_ESTEP; 0 means eta / 1024 (ten halvings)                        */
 } nmd_options;
-/* Defaults when opts == NULL: NMD_DETERMINISTIC, eta = 1, momentum = 0, flags = 0. */
+/* Defaults when opts == NULL: NMD_DETERMINISTIC, eta = 1, momentum = 0, flags = 0,
+ * guard_tol = 0, eta_min = 0.  A caller built against the earlier five-field struct (size 20)
+ * is accepted; the two later fields then take their defaults. */
 
 /*
  * nmd_create - a context for an m x n problem fitted at rank r.
@@ -112,9 +137,12 @@ int nmd_set_sparse_csr(nmd_ctx* ctx, int64_t nnz, const int64_t* row_ptr, const 
  * across calls (nmd_reset clears them).  Returns NMD_ESTATE without S, NMD_EINVAL on NULL
  * pointers or n_sweeps < 1, NMD_ENOTPD / NMD_ENONFINITE when the device rejects a step: the
  * later steps are skipped, W and H receive the factors after the last completed step (the
- * momenta are kept at that state too) and nmd_last_error names the sweep and step.
- * NMD_EDEVICE on a HIP failure.  Unless NMD_FLAG_ASYNC is set the call synchronises the stream
- * before returning.
+ * momenta are kept at that state too) and nmd_last_error names the sweep and step; the sweep
+ * counter then counts only the sweeps that completed.  With NMD_FLAG_GUARD, NMD_ESTEP when the
+ * safeguard would lower eta below eta_min: W and H then hold the factors before the rejected
+ * sweep.  NMD_EDEVICE on a HIP failure.  Unless NMD_FLAG_ASYNC is set the call synchronises the
+ * stream before returning (NMD_FLAG_GUARD ignores NMD_FLAG_ASYNC: it must read the device's
+ * decision).
  */
 int nmd_als_block_sweep(nmd_ctx* ctx, float* W, float* H, int32_t n_sweeps, void* hip_stream);
 
@@ -135,6 +163,22 @@ int nmd_objective(nmd_ctx* ctx, const float* W, const float* H, double* out_obj,
  * Synchronises the stream.  Errors as for nmd_objective.
  */
 int nmd_metrics(nmd_ctx* ctx, const float* W, const float* H, double* out, void* hip_stream);
+
+/*
+ * nmd_get_sweep_objectives - with NMD_FLAG_SWEEP_OBJECTIVE or NMD_FLAG_GUARD, the objectives
+ * of the last nmd_als_block_sweep call: out[0] before its first sweep, out[k] after its k-th
+ * (accepted) sweep, k = 1 .. n_sweeps (eq. auxCost, as nmd_objective).  `out`: host memory for
+ * cap doubles.  Returns the count (n_sweeps + 1; 0 before any such call), NMD_EINVAL if cap is
+ * too small.  Synchronises the device.
+ */
+int nmd_get_sweep_objectives(nmd_ctx* ctx, double* out, int64_t cap);
+
+/*
+ * nmd_get_step_size - the step size eta now in force (lowered by NMD_FLAG_GUARD) and, when
+ * `rejected` is not NULL, the number of sweeps the safeguard has undone since nmd_create or
+ * nmd_reset.
+ */
+int nmd_get_step_size(const nmd_ctx* ctx, float* eta, int64_t* rejected);
 
 /* nmd_destroy - frees the context and its device memory; NULL-safe. */
 void nmd_destroy(nmd_ctx* ctx);
@@ -165,7 +209,8 @@ int nmd_get_block_nnz(const nmd_ctx* ctx, int32_t side, int64_t* out, int64_t ca
  * returns K + 1 or a negative code.  Host only. */
 int nmd_get_block_bounds(const nmd_ctx* ctx, int32_t side, int64_t* out, int64_t cap);
 
-/* nmd_reset - zeroes the momentum buffers and the sweep counter, and clears a step rejection
+/* nmd_reset - zeroes the momentum buffers and the sweep counter, restores the step size given
+ * at creation (and the count of rejected sweeps, NMD_FLAG_GUARD), and clears a step rejection
  * left pending on the device (see NMD_FLAG_ASYNC).  Synchronises the device. */
 int nmd_reset(nmd_ctx* ctx);
 

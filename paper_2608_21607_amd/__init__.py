@@ -8,5 +8,6 @@ from .nmd import (  # noqa: F401
     Context, NmdError, rectified_contraction, rectified_contraction_bf16x3,
     bf16x3_workspace_floats, lib,
     header_functions, DETERMINISTIC, STOCHASTIC, FLAG_ASYNC, FLAG_TIMING, FLAG_SPLIT_BF16,
-    KERNEL_DENSE, KERNEL_SPARSE, KERNEL_FACTOR, KERNEL_APPLY,
+    FLAG_SWEEP_OBJECTIVE, FLAG_GUARD, KERNEL_DENSE, KERNEL_SPARSE, KERNEL_FACTOR, KERNEL_APPLY,
+    OK, EINVAL, ENOMEM, EDEVICE, ENOTPD, ESTATE, ENONFINITE, ESTEP,
 )

@@ -9,6 +9,7 @@
 
 #include <algorithm>
 #include <climits>
+#include <cstddef>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -214,6 +215,9 @@ struct nmd_ctx {
   nmd_options opt{};
   std::vector<int64_t> rb, cb;  // row and column block bounds
   int64_t t = 0;
+  float eta0 = 1.0f;           // step size at creation (the safeguard may lower opt.eta)
+  int64_t rejected = 0;        // sweeps undone by the step-size safeguard
+  int last_fail_step = -1;     // step id of the last step the device rejected
   std::string err;
 
   bool has_S = false;
@@ -243,6 +247,10 @@ struct nmd_ctx {
   double* objpart = nullptr;
   int64_t objpart_count = 0;
   double* objout = nullptr;
+  // per-sweep objectives (sums of squares) of the last sweep call: [0] before its first sweep
+  double* fhist = nullptr;
+  int64_t fhist_cap = 0, fcount = 0;
+  float *SA = nullptr, *SB = nullptr;  // the factors before the current sweep (safeguard)
   int* status = nullptr;
   unsigned long long* g2 = nullptr;  // [0] S-hat slices whose second product ran whole,
                                      // [1] S-hat entries taken through gathered slices
@@ -328,6 +336,10 @@ void free_device(nmd_ctx* c) {
   dfree(c->Gtmp);
   dfree(c->Gpart);
   dfree(c->objout);
+  dfree(c->fhist);
+  c->fhist_cap = c->fcount = 0;
+  dfree(c->SA);
+  dfree(c->SB);
   dfree(c->status);
   dfree(c->g2);
   if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
@@ -674,6 +686,7 @@ int conclude(nmd_ctx* c, float* W, float* H, hipStream_t st, int64_t first_sweep
     return NMD_OK;
   }
   const int step = c->h_status[1];
+  c->last_fail_step = step;
   for (auto it = c->enqueued.rbegin(); it != c->enqueued.rend(); ++it)
     if (it->first >= step) swap_side(c, it->second);  // undo the steps from the rejected one on
   int rc = store_factors(c, W, H, st);
@@ -697,13 +710,9 @@ int check_ready(nmd_ctx* c, const void* W, const void* H) {
   return NMD_OK;
 }
 
-// The sums of the objective kernel (one, or five with `metrics`), reduced on the device in a
-// fixed order and copied to q[].
-int objective_sums(nmd_ctx* c, const float* W, const float* H, hipStream_t st, bool metrics,
-                   double* q) {
-  int rc;
-  if ((rc = ensure_device(c))) return rc;
-  if ((rc = load_factors(c, W, H, st))) return rc;
+// Enqueues the objective kernel on the current panels A and B and its fixed-order reductions
+// into dst[0] (dst[0..4] with `metrics`).
+int enqueue_objective(nmd_ctx* c, hipStream_t st, bool metrics, double* dst) {
   const Side& sd = c->ws;
   const int64_t rw = nmd::dense_rows_per_wg(c->rp);
   const int64_t units = ((c->m + rw - 1) / rw) * sd.nblk();
@@ -717,10 +726,157 @@ int objective_sums(nmd_ctx* c, const float* W, const float* H, hipStream_t st, b
   const int nq = metrics ? 5 : 1;
   if (nq * npart > c->objpart_count) return fail(c, NMD_EDEVICE, "internal: objective buffer");
   for (int k = 0; k < nq; ++k)
-    HIP_TRY(c, nmd::launch_sum(c->objpart + (int64_t)k * npart, npart, c->objout + k, st));
+    HIP_TRY(c, nmd::launch_sum(c->objpart + (int64_t)k * npart, npart, dst + k, st));
+  return NMD_OK;
+}
+
+// The sums of the objective kernel (one, or five with `metrics`), reduced on the device in a
+// fixed order and copied to q[].
+int objective_sums(nmd_ctx* c, const float* W, const float* H, hipStream_t st, bool metrics,
+                   double* q) {
+  int rc;
+  if ((rc = ensure_device(c))) return rc;
+  if ((rc = load_factors(c, W, H, st))) return rc;
+  if ((rc = enqueue_objective(c, st, metrics, c->objout))) return rc;
+  const int nq = metrics ? 5 : 1;
   HIP_TRY(c, hipMemcpyAsync(c->h_obj, c->objout, nq * sizeof(double), hipMemcpyDeviceToHost, st));
   HIP_TRY(c, hipStreamSynchronize(st));
   for (int k = 0; k < 5; ++k) q[k] = k < nq ? c->h_obj[k] : 0.0;
+  return NMD_OK;
+}
+
+// Enqueues the steps of one sweep (its block list, or the two full half-steps in deterministic
+// mode) with step ids from *step_id on.
+int enqueue_sweep(nmd_ctx* c, const std::vector<int32_t>& list, bool full_halves, int* step_id,
+                  hipStream_t st) {
+  int rc;
+  if (full_halves) {
+    if ((rc = factor_step(c, true, -1, c->opt.eta, c->opt.momentum, *step_id, st))) return rc;
+    *step_id += (int)c->ws.nblk();
+    if ((rc = factor_step(c, false, -1, c->opt.eta, c->opt.momentum, *step_id, st))) return rc;
+    *step_id += (int)c->hs.nblk();
+    return NMD_OK;
+  }
+  for (int32_t code : list) {
+    const bool w = code > 0;
+    const int32_t b = (w ? code : -code) - 1;
+    if ((rc = factor_step(c, w, b, c->opt.eta, c->opt.momentum, *step_id, st))) return rc;
+    ++*step_id;
+  }
+  return NMD_OK;
+}
+
+int run(nmd_ctx* c, float* W, float* H, const std::vector<std::vector<int32_t>>& lists,
+        bool full_halves, hipStream_t st) {
+  int rc = ensure_device(c);
+  if (rc) return rc;
+  if ((rc = load_factors(c, W, H, st))) return rc;
+  c->enqueued.clear();
+  int step_id = 0;
+  for (const auto& list : lists)
+    if ((rc = enqueue_sweep(c, list, full_halves, &step_id, st))) return rc;
+  return NMD_OK;
+}
+
+// Sweeps with the objective evaluated on the device after each one (NMD_FLAG_SWEEP_OBJECTIVE)
+// and, with `guard`, the step-size safeguard of NMD_FLAG_GUARD: before each sweep the factors
+// are copied aside; after it a one-thread kernel compares the objective with the one before
+// and flags a rise in the status word, which stops every later step and copy of the call.
+// When the call's work has run the host reads the status once: on a rise it restores the
+// factors from the copies, clears the momenta, halves eta and enqueues the remaining sweeps
+// again from the rejected one (same sweep counter, same block order).
+int sweeps_tracked(nmd_ctx* c, float* W, float* H, int32_t n_sweeps, hipStream_t st, bool guard) {
+  int rc = ensure_device(c);
+  if (rc) return rc;
+  const bool sto = c->opt.mode == NMD_STOCHASTIC;
+  const int32_t steps_per = c->hs.nblk() + c->ws.nblk();
+  const int64_t ma = (c->m + 256) * (int64_t)c->rp, nb = (c->n + 256) * (int64_t)c->rp;
+  if (c->fhist_cap < (int64_t)n_sweeps + 1) {
+    dfree(c->fhist);
+    c->fhist_cap = 0;
+    if (dalloc(&c->fhist, (int64_t)n_sweeps + 1) != hipSuccess)
+      return fail(c, NMD_ENOMEM, "device allocation of the objective history failed");
+    c->fhist_cap = (int64_t)n_sweeps + 1;
+  }
+  if (guard && (!c->SA || !c->SB)) {
+    if (dalloc(&c->SA, ma) != hipSuccess || dalloc(&c->SB, nb) != hipSuccess) {
+      dfree(c->SA);
+      dfree(c->SB);
+      return fail(c, NMD_ENOMEM, "device allocation of the safeguard copies failed");
+    }
+  }
+  c->fcount = 0;
+  if ((rc = load_factors(c, W, H, st))) return rc;
+  if ((rc = enqueue_objective(c, st, false, c->fhist))) return rc;
+  const float eta_floor = c->opt.eta_min > 0.0f ? c->opt.eta_min : c->eta0 / 1024.0f;
+  const double tol2 = (1.0 + (double)c->opt.guard_tol) * (1.0 + (double)c->opt.guard_tol);
+  int32_t done = 0;
+  while (done < n_sweeps) {
+    const int64_t first = c->t;
+    c->enqueued.clear();
+    int step_id = 0;
+    for (int32_t s = done; s < n_sweeps; ++s) {
+      const std::vector<int32_t> list =
+          make_schedule(c->seed, first + (s - done), c->hs.nblk(), c->ws.nblk(), sto);
+      if (guard) {
+        HIP_TRY(c, nmd::launch_guarded_copy(c->A, c->SA, ma, c->status, st));
+        HIP_TRY(c, nmd::launch_guarded_copy(c->B, c->SB, nb, c->status, st));
+      }
+      const int sweep_first_step = step_id;
+      if ((rc = enqueue_sweep(c, list, !sto, &step_id, st))) return rc;
+      if ((rc = enqueue_objective(c, st, false, c->fhist + s + 1))) return rc;
+      if (guard)
+        HIP_TRY(c, nmd::launch_guard(c->fhist + s, c->fhist + s + 1, tol2, c->status,
+                                     sweep_first_step, st));
+    }
+    if ((c->opt.flags & NMD_FLAG_ASYNC) && !guard) {
+      c->t += n_sweeps - done;
+      c->fcount = (int64_t)n_sweeps + 1;
+      return store_factors(c, W, H, st);
+    }
+    HIP_TRY(c, hipMemcpyAsync(c->h_status, c->status, 2 * sizeof(int), hipMemcpyDeviceToHost, st));
+    HIP_TRY(c, hipStreamSynchronize(st));
+    const int flags = c->h_status[0];
+    if (flags == 0) {
+      c->t += n_sweeps - done;
+      done = n_sweeps;
+      break;
+    }
+    const int step = c->h_status[1];
+    const int32_t bad = done + step / steps_per;  // the sweep of the first failure
+    if (flags == nmd::STATUS_RISE) {
+      // every step after the rise wrote nothing: the copies hold the factors before sweep `bad`
+      HIP_TRY(c, hipMemcpyAsync(c->A, c->SA, (size_t)ma * sizeof(float), hipMemcpyDeviceToDevice, st));
+      HIP_TRY(c, hipMemcpyAsync(c->B, c->SB, (size_t)nb * sizeof(float), hipMemcpyDeviceToDevice, st));
+      HIP_TRY(c, nmd::launch_zero(c->VA, ma, st));
+      HIP_TRY(c, nmd::launch_zero(c->VB, nb, st));
+      HIP_TRY(c, hipMemsetAsync(c->status, 0, sizeof(int), st));
+      HIP_TRY(c, hipMemsetAsync(c->status + 1, 0x7f, sizeof(int), st));
+      c->t = first + (bad - done);
+      c->rejected += 1;
+      const float eta_old = c->opt.eta;
+      c->opt.eta = 0.5f * eta_old;
+      done = bad;
+      if (c->opt.eta < eta_floor) {
+        c->opt.eta = eta_old;
+        c->fcount = (int64_t)done + 1;
+        if ((rc = store_factors(c, W, H, st))) return rc;
+        HIP_TRY(c, hipStreamSynchronize(st));
+        return fail(c, NMD_ESTEP,
+                    "sweep %lld raised the objective at eta = %g; halving would go below %g",
+                    (long long)c->t, (double)eta_old, (double)eta_floor);
+      }
+      continue;
+    }
+    // a step rejected by the device (Gram not positive definite, non-finite factor)
+    c->fcount = (int64_t)bad + 1;
+    rc = conclude(c, W, H, st, first, steps_per);  // step ids of this round start at `first`
+    c->t = first + (bad - done);
+    return rc;
+  }
+  c->fcount = (int64_t)n_sweeps + 1;
+  if ((rc = store_factors(c, W, H, st))) return rc;
+  HIP_TRY(c, hipStreamSynchronize(st));
   return NMD_OK;
 }
 
@@ -741,12 +897,14 @@ int nmd_create(nmd_ctx** out, int64_t m, int64_t n, int32_t r, int32_t block_m, 
     return fail(nullptr, NMD_EINVAL, "rank r = %d must satisfy 1 <= r <= min(m, n, 512)", r);
   if (block_m < 1 || block_n < 1)
     return fail(nullptr, NMD_EINVAL, "block sizes must be >= 1");
-  nmd_options o{sizeof(nmd_options), NMD_DETERMINISTIC, 1.0f, 0.0f, 0u};
+  nmd_options o{sizeof(nmd_options), NMD_DETERMINISTIC, 1.0f, 0.0f, 0u, 0.0f, 0.0f};
   if (opts) {
-    if (opts->size < sizeof(nmd_options))
-      return fail(nullptr, NMD_EINVAL, "opts->size = %u is smaller than sizeof(nmd_options)",
-                  opts->size);
-    o = *opts;
+    // the five-field form (through `flags`) is accepted; the later fields keep their defaults
+    const uint32_t five = (uint32_t)offsetof(nmd_options, guard_tol);
+    if (opts->size < five)
+      return fail(nullptr, NMD_EINVAL, "opts->size = %u is smaller than %u", opts->size, five);
+    std::memcpy(&o, opts, std::min<size_t>(opts->size, sizeof(nmd_options)));
+    o.size = sizeof(nmd_options);
   }
   if (o.mode != NMD_DETERMINISTIC && o.mode != NMD_STOCHASTIC)
     return fail(nullptr, NMD_EINVAL, "unknown mode %d", o.mode);
@@ -754,8 +912,13 @@ int nmd_create(nmd_ctx** out, int64_t m, int64_t n, int32_t r, int32_t block_m, 
     return fail(nullptr, NMD_EINVAL, "eta must be finite and >= 0");
   if (!(o.momentum >= 0.0f && o.momentum < 1.0f))
     return fail(nullptr, NMD_EINVAL, "momentum must lie in [0, 1)");
-  if (o.flags & ~(uint32_t)(NMD_FLAG_ASYNC | NMD_FLAG_TIMING | NMD_FLAG_SPLIT_BF16))
+  if (o.flags & ~(uint32_t)(NMD_FLAG_ASYNC | NMD_FLAG_TIMING | NMD_FLAG_SPLIT_BF16 |
+                            NMD_FLAG_SWEEP_OBJECTIVE | NMD_FLAG_GUARD))
     return fail(nullptr, NMD_EINVAL, "unknown option flags 0x%x", o.flags);
+  if (!(o.guard_tol >= 0.0f) || !std::isfinite(o.guard_tol))
+    return fail(nullptr, NMD_EINVAL, "guard_tol must be finite and >= 0");
+  if (!(o.eta_min >= 0.0f) || !std::isfinite(o.eta_min))
+    return fail(nullptr, NMD_EINVAL, "eta_min must be finite and >= 0");
   std::vector<int64_t> rb = balanced_bounds(m, block_m), cb = balanced_bounds(n, block_n);
   int64_t min_rb = m, min_cb = n;
   for (size_t k = 0; k + 1 < rb.size(); ++k) min_rb = std::min(min_rb, rb[k + 1] - rb[k]);
@@ -774,6 +937,7 @@ int nmd_create(nmd_ctx** out, int64_t m, int64_t n, int32_t r, int32_t block_m, 
   c->block_n = block_n;
   c->seed = seed;
   c->opt = o;
+  c->eta0 = o.eta;
   c->rb = std::move(rb);
   c->cb = std::move(cb);
   *out = c;
@@ -865,45 +1029,27 @@ int nmd_set_sparse_csr(nmd_ctx* c, int64_t nnz, const int64_t* row_ptr, const in
   return NMD_OK;
 }
 
-static int run(nmd_ctx* c, float* W, float* H, const std::vector<std::vector<int32_t>>& lists,
-               bool full_halves, hipStream_t st) {
-  int rc = ensure_device(c);
-  if (rc) return rc;
-  if ((rc = load_factors(c, W, H, st))) return rc;
-  c->enqueued.clear();
-  int step_id = 0;
-  for (const auto& list : lists) {
-    if (full_halves) {
-      if ((rc = factor_step(c, true, -1, c->opt.eta, c->opt.momentum, step_id, st))) return rc;
-      step_id += (int)c->ws.nblk();
-      if ((rc = factor_step(c, false, -1, c->opt.eta, c->opt.momentum, step_id, st))) return rc;
-      step_id += (int)c->hs.nblk();
-      continue;
-    }
-    for (int32_t code : list) {
-      const bool w = code > 0;
-      const int32_t b = (w ? code : -code) - 1;
-      if ((rc = factor_step(c, w, b, c->opt.eta, c->opt.momentum, step_id, st))) return rc;
-      ++step_id;
-    }
-  }
-  return NMD_OK;
-}
-
 int nmd_als_block_sweep(nmd_ctx* c, float* W, float* H, int32_t n_sweeps, void* hip_stream) {
   int rc = check_ready(c, W, H);
   if (rc) return rc;
   if (n_sweeps < 1) return fail(c, NMD_EINVAL, "n_sweeps must be >= 1");
   hipStream_t st = (hipStream_t)hip_stream;
   const bool sto = c->opt.mode == NMD_STOCHASTIC;
-  std::vector<std::vector<int32_t>> lists;
-  for (int32_t s = 0; s < n_sweeps; ++s)
-    lists.push_back(make_schedule(c->seed, c->t + s, c->hs.nblk(), c->ws.nblk(), sto));
-  const int64_t first = c->t;
-  rc = run(c, W, H, lists, !sto, st);
-  if (rc) return rc;
-  c->t += n_sweeps;
-  return conclude(c, W, H, st, first, c->hs.nblk() + c->ws.nblk());
+  const int32_t steps_per = c->hs.nblk() + c->ws.nblk();
+  const bool guard = (c->opt.flags & NMD_FLAG_GUARD) != 0;
+  if (!guard && !(c->opt.flags & NMD_FLAG_SWEEP_OBJECTIVE)) {
+    std::vector<std::vector<int32_t>> lists;
+    for (int32_t s = 0; s < n_sweeps; ++s)
+      lists.push_back(make_schedule(c->seed, c->t + s, c->hs.nblk(), c->ws.nblk(), sto));
+    const int64_t first = c->t;
+    rc = run(c, W, H, lists, !sto, st);
+    if (rc) return rc;
+    c->t += n_sweeps;
+    rc = conclude(c, W, H, st, first, steps_per);
+    if (rc == NMD_ENOTPD || rc == NMD_ENONFINITE) c->t = first + c->last_fail_step / steps_per;
+    return rc;
+  }
+  return sweeps_tracked(c, W, H, n_sweeps, st, guard);
 }
 
 int nmd_run_steps(nmd_ctx* c, float* W, float* H, const int32_t* steps, int32_t n_steps,
@@ -986,6 +1132,9 @@ int nmd_reset(nmd_ctx* c) {
   if (!c) return NMD_EINVAL;
   c->err.clear();
   c->t = 0;
+  c->opt.eta = c->eta0;
+  c->rejected = 0;
+  c->fcount = 0;
   if (c->dev_ready) {
     HIP_TRY(c, hipSetDevice(c->device));
     HIP_TRY(c, hipDeviceSynchronize());
@@ -995,6 +1144,26 @@ int nmd_reset(nmd_ctx* c) {
     HIP_TRY(c, hipMemset(c->status + 1, 0x7f, sizeof(int)));
     HIP_TRY(c, hipDeviceSynchronize());
   }
+  return NMD_OK;
+}
+
+int nmd_get_sweep_objectives(nmd_ctx* c, double* out, int64_t cap) {
+  if (!c || (!out && cap > 0)) return NMD_EINVAL;
+  c->err.clear();
+  if (c->fcount == 0) return 0;
+  if (cap < c->fcount) return fail(c, NMD_EINVAL, "cap %lld < %lld objectives", (long long)cap,
+                                   (long long)c->fcount);
+  HIP_TRY(c, hipSetDevice(c->device));
+  HIP_TRY(c, hipDeviceSynchronize());
+  HIP_TRY(c, hipMemcpy(out, c->fhist, (size_t)c->fcount * sizeof(double), hipMemcpyDeviceToHost));
+  for (int64_t k = 0; k < c->fcount; ++k) out[k] = std::sqrt(std::max(out[k], 0.0)) / c->s_norm;
+  return (int)c->fcount;
+}
+
+int nmd_get_step_size(const nmd_ctx* c, float* eta, int64_t* rejected) {
+  if (!c || !eta) return NMD_EINVAL;
+  *eta = c->opt.eta;
+  if (rejected) *rejected = c->rejected;
   return NMD_OK;
 }
 

@@ -67,6 +67,31 @@ __global__ void zero_kernel(float* __restrict__ p, int64_t count) {
   if (e < count) p[e] = 0.f;
 }
 
+// A copy that does nothing once the status word holds a failure (the snapshot of the factors
+// before a sweep must not be overwritten by the state after a sweep that was rejected).
+__global__ void guarded_copy_kernel(const float4* __restrict__ src, float4* __restrict__ dst,
+                                    int64_t n4, const int* status) {
+  if (*(volatile const int*)status != 0) return;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e < n4) dst[e] = src[e];
+}
+
+__global__ void guarded_copy_tail_kernel(const float* __restrict__ src, float* __restrict__ dst,
+                                         int64_t begin, int64_t count, const int* status) {
+  if (*(volatile const int*)status != 0) return;
+  const int64_t e = begin + (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e < count) dst[e] = src[e];
+}
+
+__global__ void guard_kernel(const double* __restrict__ q_old, const double* __restrict__ q_new,
+                             double tol2, int* status, int step_id) {
+  if (threadIdx.x != 0 || *(volatile const int*)status != 0) return;
+  if (!(*q_new <= tol2 * *q_old)) {
+    atomicOr(&status[0], (int)STATUS_RISE);
+    atomicMin(&status[1], step_id);
+  }
+}
+
 // One workgroup: per-thread strided partial sums, then a fixed-order tree.
 __global__ __launch_bounds__(256) void sum_kernel(const double* __restrict__ partial,
                                                   int64_t count, double* __restrict__ out) {
@@ -115,6 +140,31 @@ hipError_t launch_transpose_out(const float* B, int rp, int64_t n, float* H, int
 hipError_t launch_zero(float* p, int64_t count, hipStream_t st) {
   if (count <= 0) return hipSuccess;
   hipLaunchKernelGGL(zero_kernel, dim3(blocks(count)), dim3(256), 0, st, p, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_guarded_copy(const float* src, float* dst, int64_t count, const int* status,
+                               hipStream_t st) {
+  const int64_t n4 = count / 4;
+  if (n4 > 0 && ((uintptr_t)src % 16 == 0) && ((uintptr_t)dst % 16 == 0)) {
+    hipLaunchKernelGGL(guarded_copy_kernel, dim3(blocks(n4)), dim3(256), 0, st,
+                       (const float4*)src, (float4*)dst, n4, status);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (count > 4 * n4)
+      hipLaunchKernelGGL(guarded_copy_tail_kernel, dim3(1), dim3(256), 0, st, src, dst, 4 * n4,
+                         count, status);
+    return hipGetLastError();
+  }
+  if (count > 0)
+    hipLaunchKernelGGL(guarded_copy_tail_kernel, dim3(blocks(count)), dim3(256), 0, st, src, dst,
+                       (int64_t)0, count, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_guard(const double* q_old, const double* q_new, double tol2, int* status,
+                        int step_id, hipStream_t st) {
+  hipLaunchKernelGGL(guard_kernel, dim3(1), dim3(64), 0, st, q_old, q_new, tol2, status, step_id);
   return hipGetLastError();
 }
 

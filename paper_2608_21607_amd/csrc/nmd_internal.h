@@ -6,6 +6,9 @@
 
 namespace nmd {
 
+// Device status word: status[0] holds flag bits, status[1] the first failing step id.
+enum { STATUS_NOTPD = 1, STATUS_NONFINITE = 2, STATUS_RISE = 4 };
+
 // One unit of sparse work: `count` consecutive entries (begin .. begin+count) of one row of a
 // block.  slot < 0: the row has a single item and its result is added to Y directly; else the
 // partial result goes to scratch row `slot` and a fix-up pass adds the row's slots in order.
@@ -100,6 +103,13 @@ hipError_t launch_transpose_in(const float* H, int r, int64_t n, float* B, int r
 hipError_t launch_transpose_out(const float* B, int rp, int64_t n, float* H, int r,
                                 hipStream_t st);
 hipError_t launch_zero(float* p, int64_t count, hipStream_t st);
+// dst = src (count floats) unless status[0] is already set.
+hipError_t launch_guarded_copy(const float* src, float* dst, int64_t count, const int* status,
+                               hipStream_t st);
+// Step-size safeguard: unless status[0] is already set, flags STATUS_RISE with step_id when
+// *q_new is not <= tol2 * *q_old (objective sums of squares; NaN counts as a rise).
+hipError_t launch_guard(const double* q_old, const double* q_new, double tol2, int* status,
+                        int step_id, hipStream_t st);
 
 // Objective: per-workgroup fp64 sums of the eq. SLloss terms over (row tile, column block,
 // sub-split); rowptr holds, per column block, the row pointers of the W-side entries.  With

@@ -16,8 +16,6 @@
 
 namespace nmd {
 
-enum { STATUS_NOTPD = 1, STATUS_NONFINITE = 2 };
-
 // status[0]: flag bits; status[1]: first failing step id.
 __device__ __forceinline__ void flag(int* status, int bit, int step_id) {
   atomicOr(&status[0], bit);

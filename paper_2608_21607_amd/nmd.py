@@ -18,11 +18,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libnmd.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "nmd.h")
 
-OK, EINVAL, ENOMEM, EDEVICE, ENOTPD, ESTATE, ENONFINITE = 0, -1, -2, -3, -4, -5, -6
+OK, EINVAL, ENOMEM, EDEVICE, ENOTPD, ESTATE, ENONFINITE, ESTEP = 0, -1, -2, -3, -4, -5, -6, -7
 CODE_NAMES = {0: "NMD_OK", -1: "NMD_EINVAL", -2: "NMD_ENOMEM", -3: "NMD_EDEVICE",
-              -4: "NMD_ENOTPD", -5: "NMD_ESTATE", -6: "NMD_ENONFINITE"}
+              -4: "NMD_ENOTPD", -5: "NMD_ESTATE", -6: "NMD_ENONFINITE", -7: "NMD_ESTEP"}
 DETERMINISTIC, STOCHASTIC = 0, 1
-FLAG_ASYNC, FLAG_TIMING, FLAG_SPLIT_BF16 = 1, 2, 4
+FLAG_ASYNC, FLAG_TIMING, FLAG_SPLIT_BF16, FLAG_SWEEP_OBJECTIVE, FLAG_GUARD = 1, 2, 4, 8, 16
 KERNEL_DENSE, KERNEL_SPARSE, KERNEL_FACTOR, KERNEL_APPLY = 0, 1, 2, 3
 
 
@@ -35,7 +35,8 @@ class NmdError(RuntimeError):
 
 class Options(C.Structure):
     _fields_ = [("size", C.c_uint32), ("mode", C.c_int32), ("eta", C.c_float),
-                ("momentum", C.c_float), ("flags", C.c_uint32)]
+                ("momentum", C.c_float), ("flags", C.c_uint32), ("guard_tol", C.c_float),
+                ("eta_min", C.c_float)]
 
 
 _lib = None
@@ -64,6 +65,8 @@ def lib() -> C.CDLL:
         "nmd_get_block_bounds": (I32, [P, I32, P, I64]),
         "nmd_reset": (I32, [P]),
         "nmd_get_sweep_count": (I32, [P, C.POINTER(I64)]),
+        "nmd_get_sweep_objectives": (I32, [P, P, I64]),
+        "nmd_get_step_size": (I32, [P, C.POINTER(F), C.POINTER(I64)]),
         "nmd_run_steps": (I32, [P, P, P, P, I32, P]),
         "nmd_rectified_contraction": (I32, [P, I64, P, I64, I32, P, P]),
         "nmd_rectified_contraction_bf16x3": (I32, [P, I64, P, I64, I32, P, P, P]),
@@ -116,10 +119,11 @@ class Context:
     """An nmd_ctx: the problem sizes, S, the block partition and the optimiser state."""
 
     def __init__(self, m, n, r, block_m, block_n, seed=1, mode="deterministic", eta=1.0,
-                 momentum=0.0, flags=0):
+                 momentum=0.0, flags=0, guard_tol=0.0, eta_min=0.0):
         self._p = None
         md = {"deterministic": DETERMINISTIC, "stochastic": STOCHASTIC}.get(mode, mode)
-        opts = Options(C.sizeof(Options), int(md), float(eta), float(momentum), int(flags))
+        opts = Options(C.sizeof(Options), int(md), float(eta), float(momentum), int(flags),
+                       float(guard_tol), float(eta_min))
         p = C.c_void_p()
         _check(lib().nmd_create(C.byref(p), int(m), int(n), int(r), int(block_m), int(block_n),
                                 int(seed) & (2**64 - 1), C.byref(opts)), None)
@@ -156,6 +160,22 @@ class Context:
         _check(lib().nmd_als_block_sweep(self._p, _dev_ptr(W, (self.m, self.r), "W"),
                                          _dev_ptr(H, (self.r, self.n), "H"), int(n_sweeps),
                                          _stream_handle(stream)), self._p)
+
+    def sweep_objectives(self):
+        """Objectives before and after each sweep of the last sweep call (NMD_FLAG_GUARD or
+        NMD_FLAG_SWEEP_OBJECTIVE)."""
+        cap = 1 << 16
+        out = np.zeros(cap, dtype=np.float64)
+        k = _check(lib().nmd_get_sweep_objectives(self._p, out.ctypes.data_as(C.c_void_p), cap),
+                   self._p)
+        return out[:k].copy()
+
+    def step_size(self):
+        """(eta now in force, number of sweeps the safeguard has undone)."""
+        eta = C.c_float()
+        rej = C.c_int64()
+        _check(lib().nmd_get_step_size(self._p, C.byref(eta), C.byref(rej)), self._p)
+        return float(eta.value), int(rej.value)
 
     def run_steps(self, W, H, steps, stream=None):
         s = np.ascontiguousarray(steps, dtype=np.int32)

@@ -34,8 +34,10 @@ def test_every_declared_symbol_is_exported(L):
         assert core in names
 
 
-def _create(m, n, r, bm, bn, seed=1, mode=nmd.STOCHASTIC, eta=1.0, mom=0.0, size=None, flags=0):
-    opts = nmd.Options(C.sizeof(nmd.Options) if size is None else size, mode, eta, mom, flags)
+def _create(m, n, r, bm, bn, seed=1, mode=nmd.STOCHASTIC, eta=1.0, mom=0.0, size=None, flags=0,
+            guard_tol=0.0, eta_min=0.0):
+    opts = nmd.Options(C.sizeof(nmd.Options) if size is None else size, mode, eta, mom, flags,
+                       guard_tol, eta_min)
     p = C.c_void_p()
     rc = nmd.lib().nmd_create(C.byref(p), m, n, r, bm, bn, seed, C.byref(opts))
     return rc, p
@@ -57,11 +59,23 @@ def test_create_rejects_bad_options(L):
     assert _create(10, 10, 2, 5, 5, eta=float("nan"))[0] == nmd.EINVAL
     assert _create(10, 10, 2, 5, 5, mom=1.0)[0] == nmd.EINVAL
     assert _create(10, 10, 2, 5, 5, size=4)[0] == nmd.EINVAL
-    assert _create(10, 10, 2, 5, 5, flags=8)[0] == nmd.EINVAL  # unknown option flag
-    for f in (nmd.FLAG_ASYNC, nmd.FLAG_TIMING, nmd.FLAG_SPLIT_BF16):
+    assert _create(10, 10, 2, 5, 5, flags=32)[0] == nmd.EINVAL  # unknown option flag
+    assert _create(10, 10, 2, 5, 5, guard_tol=-0.1)[0] == nmd.EINVAL
+    assert _create(10, 10, 2, 5, 5, eta_min=float("inf"))[0] == nmd.EINVAL
+    assert _create(10, 10, 2, 5, 5, size=16)[0] == nmd.EINVAL  # shorter than five fields
+    for f in (nmd.FLAG_ASYNC, nmd.FLAG_TIMING, nmd.FLAG_SPLIT_BF16, nmd.FLAG_SWEEP_OBJECTIVE,
+              nmd.FLAG_GUARD):
         rc, p = _create(10, 10, 2, 5, 5, flags=f)
         assert rc == 0
         L.nmd_destroy(p)
+    # a caller of the five-field options struct (size 20) is accepted, later fields default
+    rc, p = _create(10, 10, 2, 5, 5, size=20, eta=0.5)
+    assert rc == 0
+    eta = C.c_float()
+    rej = C.c_int64(7)
+    assert L.nmd_get_step_size(p, C.byref(eta), C.byref(rej)) == 0
+    assert eta.value == 0.5 and rej.value == 0
+    L.nmd_destroy(p)
     # deterministic mode accepts r above the block size
     rc, p = _create(100, 100, 30, 25, 25, mode=nmd.DETERMINISTIC)
     assert rc == 0

@@ -1,11 +1,13 @@
 """GPU parity at the full workload sizes, in the launch configuration the benchmark times.
 
-The 32768 x 32768 planted problem is small enough for the oracle to run a whole sweep.  For
-the 139,255 x 139,255 graph workload the oracle instead checks every step of a full stochastic
-sweep on a sample of rows: before each step the GPU state is copied to the host, and the
-oracle recomputes the step for the sampled rows from that state (a row of the update depends
-only on its own row, the block of the other factor, the block of S and the momentum of that
-row).
+The 32768 x 32768 planted problem and the 139,255 x 139,255 graph workload are each checked
+over one whole sweep end to end: the GPU runs the sweep in one call and the oracle runs the same
+steps on its own fp64 state (for the graph workload a few steps per test, about three minutes
+in all on 16 host threads).  Both large workloads are also checked step by step on a sample of
+rows: before each step the GPU state is copied to the host, and the oracle recomputes the step
+for the sampled rows from that state (a row of the update depends only on its own row, the
+block of the other factor, the block of S and the momentum of that row), which locates a
+discrepancy to the step.
 """
 
 import numpy as np
@@ -143,6 +145,81 @@ def test_config4_full_sweep_stepwise_sampled(config4):
     p, S, ST = config4
     _say("config 4 full sweep, every step checked on sampled rows")
     stepwise_sampled(p, S, ST)
+
+
+# One full stochastic sweep of the graph workload end to end: the GPU runs it in one
+# nmd_als_block_sweep call from the start; the oracle runs the same 34 steps on its own state,
+# a few steps per test so that progress shows; the last tests compare W, H and the objective.
+_E2E = {}
+_E2E_CHUNK = 3
+
+
+def test_config4_full_sweep_end_to_end_gpu(config4):
+    p, S, ST = config4
+    _say("config 4 full size: one sweep end to end on the GPU")
+    ctx = nmd.Context(p.m, p.n, p.r, p.block_m, p.block_n, seed=p.seed, mode=p.mode, eta=p.eta,
+                      momentum=p.momentum)
+    ctx.set_sparse_csr(p.row_ptr, p.col, p.val)
+    W, H = dev(p.W0), dev(p.H0)
+    ctx.sweep(W, H, 1)
+    _E2E["f_gpu"] = ctx.objective(W, H)
+    _E2E["W"], _E2E["H"] = W.cpu().numpy(), H.cpu().numpy()
+    _E2E["steps"] = ctx.schedule(0)
+    _E2E["state"] = salsa.State(p.W0, p.H0)
+    ctx.close()
+    assert len(_E2E["steps"]) == 34
+
+
+@pytest.mark.parametrize("chunk", range((34 + _E2E_CHUNK - 1) // _E2E_CHUNK))
+def test_config4_full_sweep_end_to_end_oracle_steps(config4, chunk):
+    p, S, ST = config4
+    if "state" not in _E2E:
+        pytest.skip("the GPU sweep did not run")
+    codes = _E2E["steps"][chunk * _E2E_CHUNK:(chunk + 1) * _E2E_CHUNK]
+    _say("config 4 oracle steps", codes)
+    salsa.run_steps(S, ST, _E2E["state"], codes, p.block_m, p.block_n, p.eta, p.momentum)
+    _E2E["done"] = _E2E.get("done", 0) + len(codes)
+
+
+def test_config4_full_sweep_end_to_end_factors(config4):
+    """W and H after one full sweep of the 139255 x 139255 graph workload, GPU (one call)
+    against the oracle (the same sweep on its own fp64 state): relative Frobenius error."""
+    if _E2E.get("done") != 34:
+        pytest.skip("the oracle sweep did not complete")
+    st = _E2E["state"]
+    ew, eh = rel(_E2E["W"], st.W), rel(_E2E["H"], st.H)
+    print(f"config 4 one sweep end to end: rel err W {ew:.2e} H {eh:.2e}")
+    assert ew < TOL and eh < TOL
+
+
+@pytest.mark.parametrize("part", range(4))
+def test_config4_full_sweep_end_to_end_objective_part(config4, part):
+    """The oracle's objective of its own factors after the sweep, summed over four row ranges
+    (eq. SLloss: the squared objective is a sum over rows)."""
+    p, S, ST = config4
+    if _E2E.get("done") != 34:
+        pytest.skip("the oracle sweep did not complete")
+    st = _E2E["state"]
+    r0, r1 = part * p.m // 4, (part + 1) * p.m // 4
+    _say("config 4 oracle objective rows", r0, r1)
+    Sp = S[r0:r1]
+    fp = salsa.objective(Sp, st.W[r0:r1], st.H)
+    _E2E.setdefault("q", []).append((fp * sp_norm(Sp)) ** 2)
+
+
+def test_config4_full_sweep_end_to_end_objective(config4):
+    p, S, ST = config4
+    if len(_E2E.get("q", [])) != 4:
+        pytest.skip("the oracle objective did not complete")
+    f_orc = float(np.sqrt(sum(_E2E["q"])) / sp_norm(S))
+    f_gpu = _E2E["f_gpu"]
+    print(f"config 4 objective after one sweep: gpu {f_gpu:.7f} oracle {f_orc:.7f}")
+    assert abs(f_gpu - f_orc) <= TOL * f_orc
+    _E2E.clear()
+
+
+def sp_norm(M):
+    return float(np.sqrt(M.multiply(M).sum()))
 
 
 def test_config4_split_bf16_first_steps_sampled(config4):

@@ -208,6 +208,28 @@ def test_graph_tenth_two_sweeps_gathered_second_product():
     assert abs(f - salsa.objective(S, Wg, Hg)) <= TOL * f
 
 
+def test_graph_tenth_block_grid_17x17_two_sweeps():
+    """The graph workload at a tenth of its size with the full workload's block grid: 13926 x
+    13926 split into 17 x 17 blocks of 819-820 rows and columns (r = 256, the workload's step
+    size and momentum), two stochastic sweeps of 34 steps each, end to end.  W, H and the
+    objective against the oracle."""
+    p = gen.config(4, scale=0.1)
+    p.block_m = p.block_n = -(-p.m // 17)
+    assert partition.num_blocks(p.m, p.block_m) == 17
+    _say("graph workload at scale 0.1, 17 x 17 blocks, two sweeps", p.m, p.nnz, p.block_m)
+    ctx = make_ctx(p)
+    W, H = dev(p.W0), dev(p.H0)
+    ctx.sweep(W, H, 2)
+    Wg, Hg = W.cpu().numpy(), H.cpu().numpy()
+    Wo, Ho, S = oracle_run(p, 2)
+    ew, eh = rel(Wg, Wo), rel(Hg, Ho)
+    f_gpu, f_orc = ctx.objective(W, H), salsa.objective(S, Wo, Ho)
+    print(f"17 x 17 blocks, two sweeps: rel err W {ew:.2e} H {eh:.2e}; f gpu {f_gpu:.6f} "
+          f"oracle {f_orc:.6f} (start {salsa.objective(S, p.W0, p.H0):.6f})")
+    assert ew < TOL and eh < TOL
+    assert abs(f_gpu - f_orc) <= TOL * f_orc
+
+
 # ---------------------------------------------- split-bf16 products (both products, bf16x3)
 # Each product carries a relative error of about 2^-16 of the sum of the magnitudes of its terms
 # (three bf16 products of two-term splits).  Against the fp64 oracle that is of order 1e-5 on Y
