@@ -257,6 +257,21 @@ int nmd_rectified_contraction_bf16x3(const float* A, int64_t rows, const float* 
                                      int32_t r, float* work, float* Y, void* hip_stream);
 
 /*
+ * nmd_rectified_contraction_bf16x3_noalloc - nmd_rectified_contraction_bf16x3 for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same product with the same kernels and results, but the split
+ * panel goes to a static workspace of 4 Mi floats (16 MiB) that the library keeps on every
+ * device it runs on until the process ends, so no `work` argument is taken.  A, B, Y, r and
+ * the errors as for nmd_rectified_contraction_bf16x3; a panel whose
+ * nmd_bf16x3_workspace_floats(blk, r) exceeds 4 Mi floats (blk > 8192 at r = 512, > 16384 at
+ * r = 256) is rejected with NMD_EINVAL before any launch.  Calls no allocating routine.  All
+ * calls on one device share its workspace: calls that overlap on one device (other streams,
+ * other threads) race and must be ordered by the caller.  Asynchronous on hip_stream.
+ */
+int nmd_rectified_contraction_bf16x3_noalloc(const float* A, int64_t rows, const float* B,
+                                             int64_t blk, int32_t r, float* Y, void* hip_stream);
+
+/*
  * nmd_bf16x3_workspace_floats - floats of workspace nmd_rectified_contraction_bf16x3 needs for
  * a blk-row panel at rank r: blk r + 32 ceil(blk / 32) max(r, 32) for r <= 128, blk r for
  * r = 256 and 512 (whose kernels read the row-major copy transposed in LDS).  -1 if blk < 1 or

@@ -882,6 +882,18 @@ int sweeps_tracked(nmd_ctx* c, float* W, float* H, int32_t n_sweeps, hipStream_t
 
 }  // namespace
 
+int nmd::set_static_error(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_create_error = buf;
+  return code;
+}
+
+void nmd::clear_static_error() { g_create_error.clear(); }
+
 // =================================================================================== ABI ==
 extern "C" {
 

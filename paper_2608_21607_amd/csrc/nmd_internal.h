@@ -123,4 +123,9 @@ hipError_t launch_sum(const double* partial, int64_t count, double* out, hipStre
 
 int dense_max_wgs(int64_t rows, int rp, int nsplit);
 
+// The message nmd_last_error(NULL) returns for the entry points without a context: sets it and
+// returns `code`, or clears it.
+int set_static_error(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_static_error();
+
 }  // namespace nmd
