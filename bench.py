@@ -297,12 +297,22 @@ def main():
     # gathered entry.
     g2_run, g2_total, g2_entries = ctx.dense_blocks()
     g2_frac = g2_run / g2_total if g2_total else 1.0
-    dense_alg_flops = dense["flops"] * (0.5 + 0.5 * g2_frac) + 2.0 * p.r * g2_entries
+    split = args.split_bf16 and rp in (16, 32, 64, 128, 256, 512)
+    # Executed-work rate: the first product plus the second product's live slices (the fp32
+    # kernel's whole slices; every 16 x 4 slice of a live 16 x 32 tile for the split kernels).
+    live_flops = dense["flops"] * (0.5 + 0.5 * g2_frac)
+    if split and rp >= 256:
+        # the method's own work: the first product plus 2 r per positive entry of max(0, L),
+        # which the split kernels at r_p = 256 and 512 count (here g2_entries)
+        dense_alg_flops = dense["flops"] * 0.5 + 2.0 * p.r * g2_entries
+    elif split:
+        dense_alg_flops = live_flops  # r_p <= 128: no entry count, the live-tile work
+    else:
+        dense_alg_flops = live_flops + 2.0 * p.r * g2_entries
     dense_s = dense["ms"] / 1e3
     dense_tflops = dense_alg_flops / dense_s / 1e12 if dense_s > 0 else 0.0
     dense_equiv_kernel = dense["flops"] / dense_s / 1e12 if dense_s > 0 else 0.0
     sparse_gbs = sparse["bytes"] / (sparse["ms"] / 1e3) / 1e9 if sparse["ms"] > 0 else 0.0
-    split = args.split_bf16 and rp in (16, 32, 64, 128, 256, 512)
     # The split option runs both products as three bf16 products each: every algorithmic flop
     # costs three bf16 flops, so its roofline peak is a third of the bf16 MFMA peak.
     peak = PEAK_BF16_MFMA / 3.0 if split else PEAK_FP32_MFMA
@@ -358,7 +368,9 @@ def main():
             "avg_launch_ms": dense["ms"] / max(1, dense["launches"]),
             "flops_per_launch": dense_alg_flops / max(1, dense["launches"]),
             "second_product_fraction_run": g2_frac,
-            "second_product_entries_gathered_per_launch": g2_entries / max(1, dense["launches"]),
+            ("positive_entries_per_launch" if split else
+             "second_product_entries_gathered_per_launch"): g2_entries / max(1, dense["launches"]),
+            "live_tile_rate_tflops": live_flops / dense_s / 1e12 if dense_s > 0 else 0.0,
             "dense_equiv_kernel_tflops": dense_equiv_kernel,
         },
     }

@@ -9,7 +9,7 @@
  *   least-squares factor updates A <- Z B (B^T B)^-1, B <- Z^T A (A^T A)^-1 (eqs. lsqA, lsqB),
  *   their stochastic form on a column mini-batch J, A <- A + eta Delta_{:J} B_J [B_J^T B_J]^-1
  *   (eqs. Shat_sto, Delta_sto, lsqA_sto), the analogous update of B on a row mini-batch I, and a
- *   momentum term that adds gamma times the previously executed update (Sec. 4.1).
+ *   heavy-ball momentum term, gamma times the last step taken (Sec. 4.1).
  *   Objective: ||Z - L||_F / ||S||_F (eq. auxCost) with Z eliminated as in eq. SLloss.
  *
  * Every entry point returns an int status (NMD_OK or a negative code); no C++ exception

@@ -12,7 +12,7 @@ Readings of the paper used here (each is also listed in the design notes):
     1_S o (S + S_hat - A B^T).  Substituting eq. updateZ into eq. Delta gives Delta = S - L on
     the nonzeros of S, which is the "+" form, so that form is used everywhere.
   * The superscript J in eq. Delta_sto restricts to the columns in J.
-  * Momentum (Sec. 4.1, "a multiple of the previously executed update"): heavy ball,
+  * Momentum (Sec. 4.1: a heavy-ball term, gamma times the last step taken): heavy ball,
     V <- gamma V + eta Delta_{:J} B_J [B_J^T B_J]^{-1}, A <- A + V, one buffer per factor,
     zero at the start.
   * The r x r systems are solved by a Cholesky factorisation of the Gram matrix.

@@ -19,7 +19,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnmd.so")
 SOURCES = ["host.cpp", "dense.hip", "dense_bf16.hip", "dense_large.hip", "dense_bf16_large.hip",
-           "objective.hip", "sparse.hip", "solve.hip", "layout.hip", "noalloc.hip"]
+           "objective.hip", "sparse.hip", "solve.hip", "chol.hip", "layout.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 # Packed-fp32 instructions are kept out of the generated code on purpose.

@@ -1,0 +1,353 @@
+// The r x r solve of every update through a Cholesky factorisation, on fp64 MFMA.
+//
+// The least-squares step needs (P_J^T P_J)^-1 (eqs. lsqA, lsqA_sto).  With G = P_J^T P_J
+// symmetric positive definite, G = L L^T (Cholesky), and G^-1 = M^T M with M = L^-1.  The
+// apply multiplies by -G^-1 as one matrix product, so that is what is formed here:
+//
+//   1. L by blocks of NB columns, left-looking: launch k has one workgroup per block row
+//      i >= k.  Each computes the updated diagonal block A_kk - sum_{l<k} L_kl L_kl^T, factors
+//      it (every workgroup of the launch does so, which removes any dependence between them),
+//      forms D_k = L_kk^-1 and, for i > k, L_ik = (A_ik - sum_{l<k} L_il L_kl^T) D_k^T.
+//   2. M = L^-1 by block columns (one workgroup each): M_jj = D_j and, for i > j,
+//      M_ij = -D_i sum_{l=j}^{i-1} L_il M_lj.
+//   3. -G^-1 = -M^T M by 64 x 64 tiles: tile (a, b) = -sum_{l >= max(a, b)} M_la^T M_lb.
+//
+// A pivot that is not positive (or not finite) flags the step as not positive definite; the
+// apply then writes nothing.  Blocks of NB x NB doubles are staged in LDS with row stride
+// NB + 1; fp64 MFMA v_mfma_f64_16x16x4f64: srcA lane l = A[l % 16][l / 16], srcB lane
+// l = B[l / 16][l % 16], accumulator register v of lane l = D[4 v + l / 16][l % 16].
+
+#include "nmd_internal.h"
+
+namespace nmd {
+
+typedef double dx4 __attribute__((ext_vector_type(4)));
+
+namespace {
+
+constexpr int kThreads = 1024;
+
+__device__ __forceinline__ void flag_notpd(int* status, int step_id) {
+  if (*(volatile int*)status == 0) {
+    atomicOr(&status[0], (int)STATUS_NOTPD);
+    atomicMin(&status[1], step_id);
+  }
+}
+
+// Copies the NB x NB block at (bi, bj) of a row-major matrix with leading dimension ld into LDS.
+template <int NB>
+__device__ __forceinline__ void stage(double* dst, const double* __restrict__ src, int ld, int bi,
+                                      int bj) {
+  constexpr int LS = NB + 1;
+  for (int e = threadIdx.x; e < NB * NB; e += kThreads) {
+    const int r = e / NB, c = e - r * NB;
+    dst[r * LS + c] = src[(int64_t)(bi * NB + r) * ld + bj * NB + c];
+  }
+}
+
+// acc += A B^T for two NB x NB blocks in LDS: (A B^T)[r][c] = sum_m A[r][m] B[c][m]; wave w
+// owns the 16 x 16 output sub-tile (w / (NB / 16), w % (NB / 16)).
+template <int NB>
+__device__ __forceinline__ void mma_abt(dx4& acc, const double* A, const double* B, int ri,
+                                        int ci, int q, int l16) {
+  constexpr int LS = NB + 1;
+#pragma unroll 4
+  for (int m0 = 0; m0 < NB; m0 += 4) {
+    const double a = A[(16 * ri + l16) * LS + m0 + q];
+    const double b = B[(16 * ci + l16) * LS + m0 + q];
+    acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+  }
+}
+
+// acc += A^T B: (A^T B)[r][c] = sum_m A[m][r] B[m][c].
+template <int NB>
+__device__ __forceinline__ void mma_atb(dx4& acc, const double* A, const double* B, int ri,
+                                        int ci, int q, int l16) {
+  constexpr int LS = NB + 1;
+#pragma unroll 4
+  for (int m0 = 0; m0 < NB; m0 += 4) {
+    const double a = A[(m0 + q) * LS + 16 * ri + l16];
+    const double b = B[(m0 + q) * LS + 16 * ci + l16];
+    acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+  }
+}
+
+// acc += A B: (A B)[r][c] = sum_m A[r][m] B[m][c].
+template <int NB>
+__device__ __forceinline__ void mma_ab(dx4& acc, const double* A, const double* B, int ri, int ci,
+                                       int q, int l16) {
+  constexpr int LS = NB + 1;
+#pragma unroll 4
+  for (int m0 = 0; m0 < NB; m0 += 4) {
+    const double a = A[(16 * ri + l16) * LS + m0 + q];
+    const double b = B[(m0 + q) * LS + 16 * ci + l16];
+    acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+  }
+}
+
+// Writes s * acc (the wave's sub-tile) into an LDS block.
+template <int NB>
+__device__ __forceinline__ void put_tile(double* dst, const dx4& acc, double s, int ri, int ci,
+                                         int q, int l16) {
+  constexpr int LS = NB + 1;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) dst[(16 * ri + 4 * v + q) * LS + 16 * ci + l16] = s * acc[v];
+}
+
+// In-place Cholesky of the NB x NB block in LDS (lower triangle), then D = L^-1 into `inv`.
+// Thread t owns row t / (NB / 4) and the columns (t % (NB / 4)) + (NB / 4) u, u = 0..3.  Step j
+// reads the unscaled column j (no thread writes it in that step) and updates the columns right
+// of it, so one barrier per step suffices; the scaling by the pivots is applied at the end.
+// Returns false if a pivot was not positive.
+template <int NB>
+__device__ bool factor_block(double* A, double* inv) {
+  constexpr int LS = NB + 1;
+  constexpr int TPR = NB / 4;
+  const int tid = threadIdx.x;
+  const bool act = tid < NB * TPR;
+  const int r = act ? tid / TPR : 0;
+  const int c0 = act ? tid % TPR : 0;
+  bool ok = true;
+  __syncthreads();
+  for (int j = 0; j < NB; ++j) {
+    double piv = A[j * LS + j];
+    if (!(piv > 0.0) || !isfinite(piv)) {
+      ok = false;
+      piv = 1.0;
+    }
+    const double rinv = 1.0 / piv;
+    if (act && r > j) {
+      const double arj = A[r * LS + j] * rinv;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = c0 + TPR * u;
+        if (c > j && c <= r) A[r * LS + c] -= arj * A[c * LS + j];
+      }
+    }
+    __syncthreads();
+  }
+  // L[r][c] = a_rc / sqrt(piv_c), L[c][c] = sqrt(piv_c); zero above the diagonal
+  double lv[4];
+  if (act) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = c0 + TPR * u;
+      double pc = A[c * LS + c];
+      pc = (pc > 0.0 && isfinite(pc)) ? pc : 1.0;
+      lv[u] = c <= r ? A[r * LS + c] / sqrt(pc) : 0.0;
+    }
+  }
+  __syncthreads();
+  if (act) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = c0 + TPR * u;
+      A[r * LS + c] = lv[u];
+      inv[r * LS + c] = (r == c) ? 1.0 : 0.0;
+    }
+  }
+  // D = L^-1 by a forward sweep over the rows of L applied to the identity: step m scales row m
+  // of D by 1 / L_mm (lazily, when it is read) and removes L_rm times it from the rows below.
+  for (int m = 0; m < NB; ++m) {
+    __syncthreads();
+    const double dm = 1.0 / A[m * LS + m];
+    if (act && r > m) {
+      const double f = A[r * LS + m] * dm;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = c0 + TPR * u;
+        if (c <= m) inv[r * LS + c] -= f * inv[m * LS + c];
+      }
+    }
+  }
+  __syncthreads();
+  if (act) {
+    const double dr = 1.0 / A[r * LS + r];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) inv[r * LS + c0 + TPR * u] *= dr;
+  }
+  __syncthreads();
+  return ok;
+}
+
+}  // namespace
+
+// Launch k of step 1: block row i = k + blockIdx.x.
+template <int NB>
+__global__ __launch_bounds__(kThreads) void chol_col_kernel(const double* __restrict__ G,
+                                                            double* __restrict__ L,
+                                                            double* __restrict__ D, int rp,
+                                                            int k, int* status, int step_id) {
+  constexpr int LS = NB + 1;
+  constexpr int NT = NB / 16;  // sub-tiles per dimension
+  __shared__ double sA[NB * LS], sB[NB * LS], s1[NB * LS], s2[NB * LS];
+  const int i = k + blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane >> 4, l16 = lane & 15;
+  const bool mw = wave < NT * NT;  // waves with an output sub-tile
+  const int ri = wave / NT, ci = wave % NT;
+  dx4 akk = {0.0, 0.0, 0.0, 0.0}, aik = {0.0, 0.0, 0.0, 0.0};
+  for (int l = 0; l < k; ++l) {
+    __syncthreads();
+    stage<NB>(s1, L, rp, k, l);
+    if (i != k) stage<NB>(s2, L, rp, i, l);
+    __syncthreads();
+    if (mw) {
+      mma_abt<NB>(akk, s1, s1, ri, ci, q, l16);
+      if (i != k) mma_abt<NB>(aik, s2, s1, ri, ci, q, l16);
+    }
+  }
+  stage<NB>(sA, G, rp, k, k);
+  if (i != k) stage<NB>(sB, G, rp, i, k);
+  __syncthreads();
+  if (mw) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int o = (16 * ri + 4 * v + q) * LS + 16 * ci + l16;
+      sA[o] -= akk[v];
+      if (i != k) sB[o] -= aik[v];
+    }
+  }
+  const bool ok = factor_block<NB>(sA, s1);  // s1 = D_k = L_kk^-1
+  if (!ok && blockIdx.x == 0 && threadIdx.x == 0) flag_notpd(status, step_id);
+  if (i == k) {
+    for (int e = threadIdx.x; e < NB * NB; e += kThreads) {
+      const int r = e / NB, c = e - r * NB;
+      L[(int64_t)(k * NB + r) * rp + k * NB + c] = sA[r * LS + c];
+      D[(int64_t)k * NB * NB + e] = s1[r * LS + c];
+    }
+    return;
+  }
+  // L_ik = A_ik D_k^T
+  dx4 o = {0.0, 0.0, 0.0, 0.0};
+  if (mw) mma_abt<NB>(o, sB, s1, ri, ci, q, l16);
+  if (mw) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      L[(int64_t)(i * NB + 16 * ri + 4 * v + q) * rp + k * NB + 16 * ci + l16] = o[v];
+  }
+}
+
+// Step 2: block column j = blockIdx.x of M = L^-1 into Mb (rows i >= j).
+template <int NB>
+__global__ __launch_bounds__(kThreads) void chol_trinv_kernel(const double* __restrict__ L,
+                                                              const double* __restrict__ D,
+                                                              double* __restrict__ Mb, int rp) {
+  constexpr int LS = NB + 1;
+  constexpr int NT = NB / 16;
+  __shared__ double sL[NB * LS], sM[NB * LS], sT[NB * LS], sD[NB * LS];
+  const int nb = rp / NB;
+  const int j = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane >> 4, l16 = lane & 15;
+  const bool mw = wave < NT * NT;
+  const int ri = wave / NT, ci = wave % NT;
+  for (int e = threadIdx.x; e < NB * NB; e += kThreads) {
+    const int r = e / NB, c = e - r * NB;
+    Mb[(int64_t)(j * NB + r) * rp + j * NB + c] = D[(int64_t)j * NB * NB + e];
+  }
+  for (int i = j + 1; i < nb; ++i) {
+    dx4 t = {0.0, 0.0, 0.0, 0.0};
+    for (int l = j; l < i; ++l) {
+      __syncthreads();  // Mb writes of the previous block row are visible; LDS is free
+      stage<NB>(sL, L, rp, i, l);
+      stage<NB>(sM, Mb, rp, l, j);
+      __syncthreads();
+      if (mw) mma_ab<NB>(t, sL, sM, ri, ci, q, l16);
+    }
+    __syncthreads();
+    if (mw) put_tile<NB>(sT, t, 1.0, ri, ci, q, l16);
+    for (int e = threadIdx.x; e < NB * NB; e += kThreads) {
+      const int r = e / NB, c = e - r * NB;
+      sD[r * LS + c] = D[(int64_t)i * NB * NB + e];
+    }
+    __syncthreads();
+    dx4 o = {0.0, 0.0, 0.0, 0.0};
+    if (mw) mma_ab<NB>(o, sD, sT, ri, ci, q, l16);
+    if (mw) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        Mb[(int64_t)(i * NB + 16 * ri + 4 * v + q) * rp + j * NB + 16 * ci + l16] = -o[v];
+    }
+  }
+}
+
+// Step 3: tile (a, b), a <= b, of -G^-1 = -M^T M, written to both (a, b) and (b, a).
+template <int NB>
+__global__ __launch_bounds__(kThreads) void chol_gram_kernel(const double* __restrict__ Mb,
+                                                             double* __restrict__ Gneg, int rp,
+                                                             const int* status) {
+  constexpr int LS = NB + 1;
+  constexpr int NT = NB / 16;
+  __shared__ double s1[NB * LS], s2[NB * LS];
+  const int nb = rp / NB;
+  int p = blockIdx.x, a = 0;  // pair index -> (a <= b)
+  while (p >= nb - a) {
+    p -= nb - a;
+    ++a;
+  }
+  const int b = a + p;
+  if (*(volatile const int*)status != 0) return;  // factorisation failed: the apply skips
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane >> 4, l16 = lane & 15;
+  const bool mw = wave < NT * NT;
+  const int ri = wave / NT, ci = wave % NT;
+  dx4 acc = {0.0, 0.0, 0.0, 0.0};
+  for (int l = b; l < nb; ++l) {
+    __syncthreads();
+    stage<NB>(s1, Mb, rp, l, a);
+    stage<NB>(s2, Mb, rp, l, b);
+    __syncthreads();
+    if (mw) mma_atb<NB>(acc, s1, s2, ri, ci, q, l16);
+  }
+  if (mw) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int r = 16 * ri + 4 * v + q, c = 16 * ci + l16;
+      Gneg[(int64_t)(a * NB + r) * rp + b * NB + c] = -acc[v];
+      if (a != b) Gneg[(int64_t)(b * NB + c) * rp + a * NB + r] = -acc[v];
+    }
+  }
+}
+
+int64_t chol_work_doubles(int rp) {
+  const int NB = rp < 64 ? rp : 64;
+  return 3 * (int64_t)rp * rp + (int64_t)(rp / NB) * NB * NB;
+}
+
+hipError_t launch_chol_inverse(const double* G, double* work, int rp, int* status, int step_id,
+                               double** result, hipStream_t st) {
+  const int NB = rp < 64 ? rp : 64;
+  const int nb = rp / NB;
+  double* L = work;
+  double* M = work + (int64_t)rp * rp;
+  double* Gneg = work + 2 * (int64_t)rp * rp;
+  double* D = work + 3 * (int64_t)rp * rp;
+#define CHOL_NB(B)                                                                           \
+  case B: {                                                                                  \
+    for (int k = 0; k < nb; ++k) {                                                           \
+      hipLaunchKernelGGL((chol_col_kernel<B>), dim3(nb - k), dim3(kThreads), 0, st, G, L, D, rp, \
+                         k, status, step_id);                                                \
+      hipError_t e = hipGetLastError();                                                      \
+      if (e != hipSuccess) return e;                                                         \
+    }                                                                                        \
+    hipLaunchKernelGGL((chol_trinv_kernel<B>), dim3(nb), dim3(kThreads), 0, st, L, D, M, rp); \
+    hipError_t e = hipGetLastError();                                                        \
+    if (e != hipSuccess) return e;                                                           \
+    hipLaunchKernelGGL((chol_gram_kernel<B>), dim3(nb * (nb + 1) / 2), dim3(kThreads), 0, st, M, \
+                       Gneg, rp, status);                                                    \
+    break;                                                                                   \
+  }
+  switch (NB) {
+    CHOL_NB(16)
+    CHOL_NB(32)
+    CHOL_NB(48)
+    CHOL_NB(64)
+    default: return hipErrorInvalidValue;
+  }
+#undef CHOL_NB
+  *result = Gneg;
+  return hipGetLastError();
+}
+
+}  // namespace nmd

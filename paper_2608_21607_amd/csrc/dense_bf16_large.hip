@@ -222,6 +222,7 @@ __global__ __launch_bounds__(64 * CfgL<RP>::WAVES) void bxl_kernel(
 
   const int64_t nblk = (jb1 - jb0 + 31) / 32;
   unsigned ran = 0;
+  unsigned pos = 0;  // positive entries of max(0, L) this lane saw
   if (nblk > 0) {
     // stage h of block b goes to slot (H b + h) mod 4: at H = 2 the ring holds this block and
     // the next, at H = 1 the block and the next three slots
@@ -259,6 +260,7 @@ __global__ __launch_bounds__(64 * CfgL<RP>::WAVES) void bxl_kernel(
       for (int v = 0; v < 4; ++v) {
         m0[v] = 4 * q + v < valid ? l0[v] : 0.f;
         m1[v] = 16 + 4 * q + v < valid ? l1[v] : 0.f;
+        pos += (m0[v] > 0.f ? 1u : 0u) + (m1[v] > 0.f ? 1u : 0u);
       }
       u32x4 zh, zl;
       if (zsplit(m0, m1, zh, zl)) {
@@ -278,8 +280,14 @@ __global__ __launch_bounds__(64 * CfgL<RP>::WAVES) void bxl_kernel(
       for (int cb = 0; cb < C::CB; ++cb) Y[row * C::RP + 16 * cb + l16] = sgn * y[cb][v];
     }
   }
-  // a live 16 x 32 tile counts as its eight 16 x 4 slices of max(0, L)
-  if (live_slices && lane == 0 && ran) atomicAdd(live_slices, 8ull * ran);
+  // a live 16 x 32 tile counts as its eight 16 x 4 slices of max(0, L); [1] counts the positive
+  // entries (rows of X past `rows` are zero and add none)
+  if (live_slices) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) pos += __shfl_xor(pos, off, 64);
+    if (lane == 0 && ran) atomicAdd(live_slices, 8ull * ran);
+    if (lane == 0 && pos) atomicAdd(live_slices + 1, (unsigned long long)pos);
+  }
 }
 
 }  // namespace bx

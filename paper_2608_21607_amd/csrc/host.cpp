@@ -242,7 +242,7 @@ struct nmd_ctx {
   float* scratch = nullptr;
   int64_t scratch_floats = 0;
 
-  double *G = nullptr, *Gtmp = nullptr, *Gpart = nullptr;
+  double *G = nullptr, *Gwork = nullptr, *Gpart = nullptr;
   int gram_chunks_max = 64;
   double* objpart = nullptr;
   int64_t objpart_count = 0;
@@ -333,7 +333,7 @@ void free_device(nmd_ctx* c) {
   dfree(c->Ypart);
   dfree(c->Pbx);
   dfree(c->G);
-  dfree(c->Gtmp);
+  dfree(c->Gwork);
   dfree(c->Gpart);
   dfree(c->objout);
   dfree(c->fhist);
@@ -409,7 +409,7 @@ int ensure_device(nmd_ctx* c) {
         dalloc(&c->VA, mpad * rp) != hipSuccess || dalloc(&c->VB, npad * rp) != hipSuccess ||
         dalloc(&c->A2, mpad * rp) != hipSuccess || dalloc(&c->B2, npad * rp) != hipSuccess ||
         dalloc(&c->VA2, mpad * rp) != hipSuccess || dalloc(&c->VB2, npad * rp) != hipSuccess ||
-        dalloc(&c->G, rp * rp) != hipSuccess || dalloc(&c->Gtmp, rp * rp + 64 * 64) != hipSuccess ||
+        dalloc(&c->G, rp * rp) != hipSuccess || dalloc(&c->Gwork, nmd::chol_work_doubles((int)rp)) != hipSuccess ||
         dalloc(&c->Gpart, (int64_t)c->gram_chunks_max * rp * rp) != hipSuccess ||
         dalloc(&c->objout, 8) != hipSuccess || dalloc(&c->status, 2) != hipSuccess ||
         dalloc(&c->g2, 2) != hipSuccess) {
@@ -585,9 +585,10 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
   HIP_TRY(c, hipEventRecord(c->ev_fork, st));
   HIP_TRY(c, hipStreamWaitEvent(c->side, c->ev_fork, 0));
   {
-    Scope sc(c, c->side, K_FACTOR, 2.0 * blk * (double)c->r * c->r + 2.0 * (double)rp * rp * rp, 0.0);
+    // Gram 2 blk r^2; Cholesky, inverse of the factor and the product M^T M r^3 / 3 each
+    Scope sc(c, c->side, K_FACTOR, 2.0 * blk * (double)c->r * c->r + (double)rp * rp * rp, 0.0);
     HIP_TRY(c, nmd::launch_gram(PJ, blk, c->r, rp, c->Gpart, gram_chunks(blk), c->G, c->side));
-    HIP_TRY(c, nmd::launch_inverse(c->G, c->Gtmp, rp, c->status, step_id, &Gneg, c->side));
+    HIP_TRY(c, nmd::launch_chol_inverse(c->G, c->Gwork, rp, c->status, step_id, &Gneg, c->side));
   }
   HIP_TRY(c, hipEventRecord(c->ev_join, c->side));
   const int64_t ns = nsplit_for(rows, blk, rp, c->dense_slots);

@@ -80,9 +80,11 @@ hipError_t launch_fixup(const Split* splits, int64_t nsplits, const float* scrat
 // Gram matrix G = P^T P (fp64, rp x rp, identity on the padded diagonal) of `blk` rows.
 hipError_t launch_gram(const float* P, int64_t blk, int r, int rp, double* Gpart, int nchunks,
                        double* G, hipStream_t st);
-// Gsw <- -G^-1 by block sweeps; flags status on a non-positive pivot.  Gtmp: scratch rp x rp.
-hipError_t launch_inverse(double* G, double* Gtmp, int rp, int* status, int step_id,
-                          double** result, hipStream_t st);
+// -G^-1 through the Cholesky factorisation G = L L^T (chol.hip): *result receives -G^-1
+// (rp x rp, inside `work`, chol_work_doubles(rp) doubles); a non-positive pivot flags status.
+int64_t chol_work_doubles(int rp);
+hipError_t launch_chol_inverse(const double* G, double* work, int rp, int* status, int step_id,
+                               double** result, hipStream_t st);
 // Vout = gamma Vin + eta U (-Gneg), Xout = Xin + Vout, where U = Delta P_J is the sum (fp64)
 // of the nsplit partial outputs plus, when Ysp is not NULL, a separate correction buffer
 // (rows x rp), and -Gneg = (P_J^T P_J)^-1.  The outputs are other buffers than the inputs, so

@@ -3,11 +3,7 @@
 //   1. Gram matrix G = P_J^T P_J of the panel rows of the block (fp32 inputs, products exact in
 //      fp64, sums in fp64), computed in row chunks by many workgroups and reduced in a fixed
 //      order (deterministic).  Padded columns (beyond r) are zero, so their diagonal is set to 1.
-//   2. G^-1 by block sweeps (in-place Gauss-Jordan elimination by pivot blocks of 64): sweeping
-//      pivot block k maps [[P, Q], [Q^T, T]] to [[-P^-1, P^-1 Q], [Q^T P^-1, T - Q^T P^-1 Q]];
-//      after every block has been swept the matrix holds -G^-1.  For a symmetric positive
-//      definite G every pivot (a Schur complement) is positive definite, so no pivoting is
-//      needed; a non-positive pivot flags the step as not positive definite.
+//   2. -G^-1 through the Cholesky factorisation G = L L^T (chol.hip).
 //   3. Apply: with U = Delta_{:J} P_J (the sum of the partial outputs), the step is U G^-1
 //      (eqs. spLsqA, lsqA_sto), then V <- gamma V + eta U G^-1, A <- A + V (heavy-ball
 //      momentum; eta = 1, gamma = 0 gives the exact least-squares update).
@@ -118,200 +114,6 @@ hipError_t launch_gram(const float* P, int64_t blk, int r, int rp, double* Gpart
   hipLaunchKernelGGL(gram_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                      Gpart, nchunks, r, rp, T, G);
   return hipGetLastError();
-}
-
-// -------------------------------------------------------------------------- block sweeps --
-// Inverse of one NB x NB pivot block by Gauss-Jordan elimination without pivoting.  Thread
-// (i = tid % 64, jq = tid / 64) keeps row i, columns jq*CPT .. jq*CPT+CPT-1 in registers; the
-// pivot row and the pivot column are broadcast through double-buffered LDS, so each pivot
-// costs one barrier.  For an s.p.d. block every pivot is positive; a non-positive or
-// non-finite pivot flags the step as not positive definite.
-template <int NB>
-__global__ __launch_bounds__(256) void pivot_inverse_kernel(const double* __restrict__ G, int rp,
-                                                            int k, double* __restrict__ D,
-                                                            int* status, int step_id) {
-  constexpr int CPT = NB / 4;
-  __shared__ double prow[2][NB];
-  __shared__ double colp[2][64];
-  const int tid = threadIdx.x;
-  const int i = tid & 63, jq = tid >> 6;
-  const bool live = i < NB;
-  double a[CPT];
-#pragma unroll
-  for (int c = 0; c < CPT; ++c)
-    a[c] = live ? G[(int64_t)(k * NB + i) * rp + k * NB + jq * CPT + c] : 0.0;
-  bool bad = false;
-#pragma unroll
-  for (int p = 0; p < NB; ++p) {
-    const int buf = p & 1;
-    if (jq == p / CPT) {
-      if (i == p) {
-#pragma unroll
-        for (int c = 0; c < CPT; ++c) prow[buf][jq * CPT + c] = a[c];
-      }
-      colp[buf][i] = a[p % CPT];
-    }
-    // the row owners of the other column quarters publish their part of the pivot row
-    if (i == p && jq != p / CPT) {
-#pragma unroll
-      for (int c = 0; c < CPT; ++c) prow[buf][jq * CPT + c] = a[c];
-    }
-    __syncthreads();
-    double piv = prow[buf][p];
-    if (!(piv > 0.0) || !isfinite(piv)) {
-      bad = true;
-      piv = 1.0;
-    }
-    const double inv = 1.0 / piv;
-    const double f = colp[buf][i];
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int j = jq * CPT + c;
-      const double r = prow[buf][j] * inv;
-      if (i == p)
-        a[c] = (j == p) ? inv : r;
-      else
-        a[c] = (j == p) ? -f * inv : fma(-f, r, a[c]);
-    }
-  }
-  // only the first failing step is recorded (a failure leaves later steps skipped)
-  if (tid == 0 && bad && *(volatile int*)status == 0) flag(status, STATUS_NOTPD, step_id);
-  if (live) {
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) D[(int64_t)i * NB + jq * CPT + c] = a[c];
-  }
-}
-
-// One block sweep over pivot block k; grid (nblk, nblk), one NB x NB output tile per WG, on
-// fp64 MFMA.  Wave w owns the 16-row block w of the tile (NB = 64) and its four 16 x 16 output
-// blocks.  Tiles live in LDS with row stride NB + 1.
-template <int NB>
-__device__ __forceinline__ void tile_mm(doublex4 (&acc)[NB / 16], const double* L,
-                                        const double* R, int rb, int q, int l16) {
-  constexpr int LS = NB + 1;
-  for (int k0 = 0; k0 < NB; k0 += 4) {
-    const double av = L[(16 * rb + l16) * LS + k0 + q];
-#pragma unroll
-    for (int cb = 0; cb < NB / 16; ++cb) {
-      const double bv = R[(k0 + q) * LS + 16 * cb + l16];
-      acc[cb] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[cb], 0, 0, 0);
-    }
-  }
-}
-
-template <int NB>
-__global__ __launch_bounds__(256) void sweep_kernel(const double* __restrict__ Gin,
-                                                    double* __restrict__ Gout, int rp, int k,
-                                                    const double* __restrict__ D) {
-  constexpr int LS = NB + 1;
-  constexpr int NCB = NB / 16;
-  __shared__ double s1[NB * LS];
-  __shared__ double s2[NB * LS];
-  const int tj = blockIdx.x, ti = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int q = lane >> 4, l16 = lane & 15;
-  auto load = [&](double* dst, int bi, int bj) {
-    for (int e = tid; e < NB * NB; e += 256) {
-      const int r = e / NB, c = e - r * NB;
-      dst[r * LS + c] = Gin[(int64_t)(bi * NB + r) * rp + bj * NB + c];
-    }
-  };
-  auto loadD = [&](double* dst) {
-    for (int e = tid; e < NB * NB; e += 256) {
-      const int r = e / NB, c = e - r * NB;
-      dst[r * LS + c] = D[e];
-    }
-  };
-  // output element of accumulator (cb, v): row 16 wave + 4v + q, column 16 cb + l16
-  auto out_index = [&](int cb, int v) {
-    return (int64_t)(ti * NB + 16 * wave + 4 * v + q) * rp + tj * NB + 16 * cb + l16;
-  };
-  const bool active = wave < NB / 16;
-  doublex4 acc[NCB];
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) acc[cb] = doublex4{0.0, 0.0, 0.0, 0.0};
-  if (ti == k && tj == k) {
-    for (int e = tid; e < NB * NB; e += 256) {
-      const int r = e / NB, c = e - r * NB;
-      Gout[(int64_t)(k * NB + r) * rp + k * NB + c] = -D[e];
-    }
-    return;
-  }
-  if (ti == k) {  // D G_kj
-    loadD(s1);
-    load(s2, k, tj);
-    __syncthreads();
-    if (active) tile_mm<NB>(acc, s1, s2, wave, q, l16);
-  } else if (tj == k) {  // G_ik D
-    load(s1, ti, k);
-    loadD(s2);
-    __syncthreads();
-    if (active) tile_mm<NB>(acc, s1, s2, wave, q, l16);
-  } else {  // G_ij - (G_ik D) G_kj
-    load(s1, ti, k);
-    loadD(s2);
-    __syncthreads();
-    if (active) tile_mm<NB>(acc, s1, s2, wave, q, l16);
-    __syncthreads();
-    if (active) {
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) s1[(16 * wave + 4 * v + q) * LS + 16 * cb + l16] = acc[cb][v];
-    }
-    load(s2, k, tj);
-    __syncthreads();
-    if (active) {
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) acc[cb] = doublex4{0.0, 0.0, 0.0, 0.0};
-      tile_mm<NB>(acc, s1, s2, wave, q, l16);
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int64_t o = out_index(cb, v);
-          Gout[o] = Gin[o] - acc[cb][v];
-        }
-    }
-    return;
-  }
-  if (active) {
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) Gout[out_index(cb, v)] = acc[cb][v];
-  }
-}
-
-hipError_t launch_inverse(double* G, double* Gtmp, int rp, int* status, int step_id,
-                          double** result, hipStream_t st) {
-  const int NB = rp < 64 ? rp : 64;
-  const int nblk = rp / NB;
-  double* D = Gtmp + (int64_t)rp * rp;  // NB x NB scratch after the ping-pong buffer
-  double* bufs[2] = {G, Gtmp};
-  int cur = 0;
-  for (int k = 0; k < nblk; ++k) {
-    switch (NB) {
-      case 16: hipLaunchKernelGGL((pivot_inverse_kernel<16>), dim3(1), dim3(256), 0, st, bufs[cur], rp, k, D, status, step_id); break;
-      case 32: hipLaunchKernelGGL((pivot_inverse_kernel<32>), dim3(1), dim3(256), 0, st, bufs[cur], rp, k, D, status, step_id); break;
-      case 48: hipLaunchKernelGGL((pivot_inverse_kernel<48>), dim3(1), dim3(256), 0, st, bufs[cur], rp, k, D, status, step_id); break;
-      case 64: hipLaunchKernelGGL((pivot_inverse_kernel<64>), dim3(1), dim3(256), 0, st, bufs[cur], rp, k, D, status, step_id); break;
-      default: return hipErrorInvalidValue;
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    switch (NB) {
-      case 16: hipLaunchKernelGGL((sweep_kernel<16>), dim3(nblk, nblk), dim3(256), 0, st, bufs[cur], bufs[cur ^ 1], rp, k, D); break;
-      case 32: hipLaunchKernelGGL((sweep_kernel<32>), dim3(nblk, nblk), dim3(256), 0, st, bufs[cur], bufs[cur ^ 1], rp, k, D); break;
-      case 48: hipLaunchKernelGGL((sweep_kernel<48>), dim3(nblk, nblk), dim3(256), 0, st, bufs[cur], bufs[cur ^ 1], rp, k, D); break;
-      case 64: hipLaunchKernelGGL((sweep_kernel<64>), dim3(nblk, nblk), dim3(256), 0, st, bufs[cur], bufs[cur ^ 1], rp, k, D); break;
-    }
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    cur ^= 1;
-  }
-  *result = bufs[cur];
-  return hipSuccess;
 }
 
 // --------------------------------------------------------------------------------- apply --

@@ -370,7 +370,7 @@ def test_one_block_stochastic_sweep_is_deterministic_sweep():
 
 
 def test_momentum_is_heavy_ball():
-    """Momentum adds a multiple gamma of the previously executed update (Sec. 4.1): two
+    """Heavy-ball momentum adds gamma times the last step taken (Sec. 4.1): two
     consecutive steps on the same block with gamma give A2 - A1 = gamma (A1 - A0) + eta D1."""
     m, n, r = 40, 30, 4
     S, W, H = _rand_problem(m, n, r, 0.2, 2)
