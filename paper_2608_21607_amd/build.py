@@ -18,7 +18,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnmd.so")
-SOURCES = ["host.cpp", "dense.hip", "dense_bf16.hip", "dense_large.hip", "dense_bf16_large.hip",
+SOURCES = ["host.cpp", "ingest.cpp", "dense.hip", "dense_bf16.hip", "dense_large.hip", "dense_bf16_large.hip",
            "objective.hip", "sparse.hip", "solve.hip", "chol.hip", "layout.hip", "noalloc.hip"]
 ARCH = "gfx950"
 

@@ -24,12 +24,13 @@
 
 using nmd::Item;
 using nmd::Split;
+using nmd::balanced_bounds;
+using nmd::make_schedule;
 
 namespace {
 
 thread_local std::string g_create_error;
 
-constexpr int kItemChunk = 128;    // entries per sparse work item
 constexpr int kMaxSplits = 16;     // partial outputs of the dense kernel
 constexpr int64_t kSplitRows = 8192;  // at most this many panel rows per fp32 accumulation
 constexpr int64_t kTargetWgs = 2048;  // dense workgroups wanted per launch (256 CUs)
@@ -38,166 +39,15 @@ constexpr int kObjSubMax = 16;        // sub-splits of a column block in the obj
 
 enum { K_DENSE = 0, K_SPARSE = 1, K_FACTOR = 2, K_APPLY = 3, K_COUNT = 4 };
 
-// ------------------------------------------------------------------------------ schedule --
-// SplitMix64 (Steele, Lea and Flood 2014), Lemire's bounded integers (2019), Fisher-Yates
-// (Durstenfeld order), and a proportional merge of column-block and row-block steps.
-struct SplitMix64 {
-  uint64_t s;
-  uint64_t next() {
-    s += 0x9E3779B97F4A7C15ULL;
-    uint64_t z = s;
-    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
-    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
-    return z ^ (z >> 31);
-  }
-};
-
-uint64_t bounded(SplitMix64& g, uint64_t k) {
-  unsigned __int128 prod = (unsigned __int128)g.next() * k;
-  uint64_t low = (uint64_t)prod;
-  if (low < k) {
-    const uint64_t thresh = (0 - k) % k;  // (2^64 - k) mod k
-    while (low < thresh) {
-      prod = (unsigned __int128)g.next() * k;
-      low = (uint64_t)prod;
-    }
-  }
-  return (uint64_t)(prod >> 64);
-}
-
-std::vector<int32_t> permutation(SplitMix64& g, int32_t k) {
-  std::vector<int32_t> a(k);
-  for (int32_t i = 0; i < k; ++i) a[i] = i;
-  for (int32_t i = k - 1; i > 0; --i) {
-    const int32_t j = (int32_t)bounded(g, (uint64_t)i + 1);
-    std::swap(a[i], a[j]);
-  }
-  return a;
-}
-
-std::vector<int32_t> make_schedule(uint64_t seed, int64_t t, int32_t R, int32_t C,
-                                   bool stochastic) {
-  std::vector<int32_t> out;
-  out.reserve((size_t)R + C);
-  if (!stochastic) {
-    for (int32_t k = 0; k < C; ++k) out.push_back(k + 1);
-    for (int32_t k = 0; k < R; ++k) out.push_back(-(k + 1));
-    return out;
-  }
-  SplitMix64 g{seed ^ ((uint64_t)t * 0x9E3779B97F4A7C15ULL)};
-  const std::vector<int32_t> sigma = permutation(g, C);
-  const std::vector<int32_t> pi = permutation(g, R);
-  int64_t w = 0, h = 0;
-  while (w < C || h < R) {
-    if (h == R || (w < C && (2 * w + 1) * (int64_t)R <= (2 * h + 1) * (int64_t)C)) {
-      out.push_back(sigma[w] + 1);
-      ++w;
-    } else {
-      out.push_back(-(pi[h] + 1));
-      ++h;
-    }
-  }
-  return out;
-}
-
-std::vector<int64_t> balanced_bounds(int64_t size, int64_t block) {
-  const int64_t K = (size + block - 1) / block;
-  std::vector<int64_t> b(K + 1);
-  for (int64_t k = 0; k <= K; ++k) b[k] = (int64_t)(((__int128)k * size) / K);
-  return b;
-}
-
-// ---------------------------------------------------------------------------- one side --
-// The entries of S arranged for the updates of one factor.  For the W side the "rows" are the
-// m rows of S and the blocks split the n columns; for the H side the rows are the n columns of S
-// and the blocks split its m rows (the transposed problem).
-struct Side {
-  int64_t rows = 0, other = 0;
-  std::vector<int64_t> bounds;           // block bounds over `other`
-  std::vector<int64_t> entry_off;        // entries of block b: [entry_off[b], entry_off[b+1])
-  std::vector<int32_t> idx;              // index into `other`
-  std::vector<float> val;
-  std::vector<int64_t> item_off;         // items of block b
-  std::vector<Item> items;
-  std::vector<int64_t> split_off;        // split rows of block b
-  std::vector<Split> splits;
-  std::vector<int64_t> rowptr;           // block b, row i: entries [rowptr[b(rows+1)+i], ..+1])
-  int64_t max_slots = 0;
-  // device copies
+// The arrangement of S for one factor (ingest.h) and its device copies.
+struct Side : nmd::SideHost {
   int32_t* d_idx = nullptr;
   float* d_val = nullptr;
   Item* d_items = nullptr;
   Split* d_splits = nullptr;
   int64_t* d_rowptr = nullptr;
   int64_t* d_bounds = nullptr;
-
-  int32_t nblk() const { return (int32_t)bounds.size() - 1; }
 };
-
-// ptr/idx/val: the rows of this side in compressed form (entries sorted within a row).
-void build_side(Side& sd, int64_t rows, int64_t other, const std::vector<int64_t>& bounds,
-                const int64_t* ptr, const int32_t* idx, const float* val) {
-  sd.rows = rows;
-  sd.other = other;
-  sd.bounds = bounds;
-  const int32_t nb = sd.nblk();
-  std::vector<int32_t> blk_of(other);
-  for (int32_t b = 0; b < nb; ++b)
-    for (int64_t j = bounds[b]; j < bounds[b + 1]; ++j) blk_of[j] = b;
-  std::vector<int64_t> cnt(nb, 0);
-  const int64_t nnz = ptr[rows];
-  for (int64_t e = 0; e < nnz; ++e) ++cnt[blk_of[idx[e]]];
-  sd.entry_off.assign(nb + 1, 0);
-  for (int32_t b = 0; b < nb; ++b) sd.entry_off[b + 1] = sd.entry_off[b] + cnt[b];
-  sd.idx.resize(nnz);
-  sd.val.resize(nnz);
-  std::vector<int64_t> cur(sd.entry_off.begin(), sd.entry_off.end() - 1);
-  std::vector<std::vector<Item>> items(nb);
-  std::vector<std::vector<Split>> splits(nb);
-  std::vector<int32_t> slots(nb, 0);
-  sd.rowptr.assign((size_t)nb * (rows + 1), 0);
-  for (int32_t b = 0; b < nb; ++b) sd.rowptr[(size_t)b * (rows + 1)] = sd.entry_off[b];
-  for (int64_t i = 0; i < rows; ++i) {
-    int64_t e = ptr[i];
-    const int64_t e1 = ptr[i + 1];
-    while (e < e1) {
-      const int32_t b = blk_of[idx[e]];
-      int64_t f = e;
-      while (f < e1 && idx[f] < bounds[b + 1]) ++f;
-      const int64_t count = f - e;
-      const int64_t base = cur[b];
-      std::memcpy(&sd.idx[base], idx + e, count * sizeof(int32_t));
-      std::memcpy(&sd.val[base], val + e, count * sizeof(float));
-      cur[b] += count;
-      if (count <= kItemChunk) {
-        items[b].push_back(Item{base, (int32_t)count, (int32_t)i, -1, 0});
-      } else {
-        const int32_t pieces = (int32_t)((count + kItemChunk - 1) / kItemChunk);
-        splits[b].push_back(Split{(int32_t)i, slots[b], pieces, 0});
-        for (int32_t p = 0; p < pieces; ++p) {
-          const int64_t s0 = (int64_t)p * kItemChunk;
-          const int64_t c = std::min<int64_t>(kItemChunk, count - s0);
-          items[b].push_back(Item{base + s0, (int32_t)c, (int32_t)i, slots[b] + p, 0});
-        }
-        slots[b] += pieces;
-      }
-      e = f;
-    }
-    for (int32_t b = 0; b < nb; ++b) sd.rowptr[(size_t)b * (rows + 1) + i + 1] = cur[b];
-  }
-  sd.item_off.assign(nb + 1, 0);
-  sd.split_off.assign(nb + 1, 0);
-  sd.items.clear();
-  sd.splits.clear();
-  sd.max_slots = 0;
-  for (int32_t b = 0; b < nb; ++b) {
-    sd.item_off[b + 1] = sd.item_off[b] + (int64_t)items[b].size();
-    sd.split_off[b + 1] = sd.split_off[b] + (int64_t)splits[b].size();
-    sd.items.insert(sd.items.end(), items[b].begin(), items[b].end());
-    sd.splits.insert(sd.splits.end(), splits[b].begin(), splits[b].end());
-    sd.max_slots = std::max<int64_t>(sd.max_slots, slots[b]);
-  }
-}
 
 struct TimerRec {
   hipEvent_t a, b;
@@ -967,66 +817,20 @@ int nmd_set_sparse_csr(nmd_ctx* c, int64_t nnz, const int64_t* row_ptr, const in
     return fail(c, NMD_EINVAL, "col_idx and values must be non-NULL when nnz > 0");
   if (nnz >= INT32_MAX) return fail(c, NMD_EINVAL, "nnz must be < 2^31-1");
   const int64_t m = c->m, n = c->n;
-  if (row_ptr[0] != 0) return fail(c, NMD_EINVAL, "row_ptr[0] = %lld, expected 0", (long long)row_ptr[0]);
-  for (int64_t i = 0; i < m; ++i)
-    if (row_ptr[i + 1] < row_ptr[i])
-      return fail(c, NMD_EINVAL, "row_ptr decreases at row %lld", (long long)i);
-  if (row_ptr[m] != nnz)
-    return fail(c, NMD_EINVAL, "row_ptr[m] = %lld differs from nnz = %lld", (long long)row_ptr[m],
-                (long long)nnz);
-  for (int64_t i = 0; i < m; ++i) {
-    for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
-      const int32_t j = col_idx[e];
-      if (j < 0 || j >= n)
-        return fail(c, NMD_EINVAL, "column index %d out of range in row %lld", j, (long long)i);
-      if (e > row_ptr[i] && j <= col_idx[e - 1])
-        return fail(c, NMD_EINVAL, "column indices not strictly increasing in row %lld",
-                    (long long)i);
-      const float v = values[e];
-      if (!std::isfinite(v) || v < 0.0f)
-        return fail(c, NMD_EINVAL, "value at row %lld, column %d is negative or not finite",
-                    (long long)i, j);
-    }
-  }
-  // keep the positive entries only (the mask of the Z-update is S_ij > 0)
-  std::vector<int64_t> ptr(m + 1, 0);
-  std::vector<int32_t> col;
-  std::vector<float> val;
-  col.reserve(nnz);
-  val.reserve(nnz);
+  nmd::Compressed rows, cols;
   double s2 = 0.0;
-  for (int64_t i = 0; i < m; ++i) {
-    for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
-      if (values[e] > 0.0f) {
-        col.push_back(col_idx[e]);
-        val.push_back(values[e]);
-        s2 += (double)values[e] * values[e];
-      }
-    }
-    ptr[i + 1] = (int64_t)col.size();
+  try {
+    const std::string why = nmd::ingest_csr(m, n, nnz, row_ptr, col_idx, values, rows, cols, &s2);
+    if (!why.empty()) return fail(c, NMD_EINVAL, "%s", why.c_str());
+  } catch (const std::bad_alloc&) {
+    return fail(c, NMD_ENOMEM, "host allocation failed while arranging S");
   }
-  const int64_t nz = (int64_t)col.size();
-  if (nz == 0) return fail(c, NMD_EINVAL, "S has no positive entry");
-  // column-compressed copy for the H side (rows ascending inside each column)
-  std::vector<int64_t> cptr(n + 1, 0);
-  for (int64_t e = 0; e < nz; ++e) ++cptr[col[e] + 1];
-  for (int64_t j = 0; j < n; ++j) cptr[j + 1] += cptr[j];
-  std::vector<int32_t> crow(nz);
-  std::vector<float> cval(nz);
-  {
-    std::vector<int64_t> cur(cptr.begin(), cptr.end() - 1);
-    for (int64_t i = 0; i < m; ++i)
-      for (int64_t e = ptr[i]; e < ptr[i + 1]; ++e) {
-        const int64_t d = cur[col[e]]++;
-        crow[d] = (int32_t)i;
-        cval[d] = val[e];
-      }
-  }
+  const int64_t nz = (int64_t)rows.idx.size();
   free_sparse_device(c);
   c->has_S = false;
   try {
-    build_side(c->ws, m, n, c->cb, ptr.data(), col.data(), val.data());
-    build_side(c->hs, n, m, c->rb, cptr.data(), crow.data(), cval.data());
+    nmd::build_side(c->ws, m, n, c->cb, rows.ptr.data(), rows.idx.data(), rows.val.data());
+    nmd::build_side(c->hs, n, m, c->rb, cols.ptr.data(), cols.idx.data(), cols.val.data());
   } catch (const std::bad_alloc&) {
     return fail(c, NMD_ENOMEM, "host allocation failed while arranging S");
   }

@@ -4,29 +4,12 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "ingest.h"
+
 namespace nmd {
 
 // Device status word: status[0] holds flag bits, status[1] the first failing step id.
 enum { STATUS_NOTPD = 1, STATUS_NONFINITE = 2, STATUS_RISE = 4 };
-
-// One unit of sparse work: `count` consecutive entries (begin .. begin+count) of one row of a
-// block.  slot < 0: the row has a single item and its result is added to Y directly; else the
-// partial result goes to scratch row `slot` and a fix-up pass adds the row's slots in order.
-struct Item {
-  int64_t begin;
-  int32_t count;
-  int32_t row;
-  int32_t slot;
-  int32_t pad;
-};
-
-// A row whose entries were split over several items: slots first .. first+nslots-1.
-struct Split {
-  int32_t row;
-  int32_t first;
-  int32_t nslots;
-  int32_t pad;
-};
 
 // Padded rank: the kernels work on r_p columns (zeros beyond r).
 int padded_rank(int r);
