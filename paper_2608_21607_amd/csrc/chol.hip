@@ -94,11 +94,22 @@ __device__ __forceinline__ void put_tile(double* dst, const dx4& acc, double s, 
   for (int v = 0; v < 4; ++v) dst[(16 * ri + 4 * v + q) * LS + 16 * ci + l16] = s * acc[v];
 }
 
-// In-place Cholesky of the NB x NB block in LDS (lower triangle), then D = L^-1 into `inv`.
-// Thread t owns row t / (NB / 4) and the columns (t % (NB / 4)) + (NB / 4) u, u = 0..3.  Step j
-// reads the unscaled column j (no thread writes it in that step) and updates the columns right
-// of it, so one barrier per step suffices; the scaling by the pivots is applied at the end.
-// Returns false if a pivot was not positive.
+// 1 / x to full double precision: the fp32 reciprocal estimate refined by two Newton steps
+// (each doubles the correct bits: 2^-23 -> 2^-46 -> beyond 2^-53).
+__device__ __forceinline__ double recip(double x) {
+  double y = (double)(1.0f / (float)x);
+  y = y * (2.0 - x * y);
+  return y * (2.0 - x * y);
+}
+
+// In-place Cholesky of the NB x NB block in LDS (lower triangle) and D = L^-1 into `inv`, in one
+// elimination: step j removes (a_rj / a_jj) times row j from every row r > j, in the columns
+// right of j of A (the trailing update) and in the columns up to j of E (which starts as I).  So
+// E A = U with U upper triangular and E unit lower triangular; with p_j = a_jj at step j,
+// L[r][c] = a_rc / sqrt(p_c) and L^-1 = diag(1 / sqrt(p)) E.  Thread t owns row t / (NB / 4) and
+// columns (t % (NB / 4)) + (NB / 4) u, u = 0..3, of both.  Step j reads column j of A and row j
+// of E, which no thread writes in that step, so one barrier per step suffices.  Returns false if
+// a pivot was not positive (or not finite).
 template <int NB>
 __device__ bool factor_block(double* A, double* inv) {
   constexpr int LS = NB + 1;
@@ -107,6 +118,10 @@ __device__ bool factor_block(double* A, double* inv) {
   const bool act = tid < NB * TPR;
   const int r = act ? tid / TPR : 0;
   const int c0 = act ? tid % TPR : 0;
+  if (act) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) inv[r * LS + c0 + TPR * u] = (r == c0 + TPR * u) ? 1.0 : 0.0;
+  }
   bool ok = true;
   __syncthreads();
   for (int j = 0; j < NB; ++j) {
@@ -115,56 +130,42 @@ __device__ bool factor_block(double* A, double* inv) {
       ok = false;
       piv = 1.0;
     }
-    const double rinv = 1.0 / piv;
     if (act && r > j) {
-      const double arj = A[r * LS + j] * rinv;
+      const double f = A[r * LS + j] * recip(piv);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int c = c0 + TPR * u;
-        if (c > j && c <= r) A[r * LS + c] -= arj * A[c * LS + j];
+        if (c > j) {
+          if (c <= r) A[r * LS + c] -= f * A[c * LS + j];
+        } else {
+          inv[r * LS + c] -= f * inv[j * LS + c];
+        }
       }
     }
     __syncthreads();
   }
-  // L[r][c] = a_rc / sqrt(piv_c), L[c][c] = sqrt(piv_c); zero above the diagonal
-  double lv[4];
+  // L[r][c] = a_rc / sqrt(p_c) (zero above the diagonal), L^-1[r][c] = E[r][c] / sqrt(p_r)
+  double lv[4], dv[4];
   if (act) {
+    double pr = A[r * LS + r];
+    pr = (pr > 0.0 && isfinite(pr)) ? pr : 1.0;
+    const double sr = 1.0 / sqrt(pr);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int c = c0 + TPR * u;
       double pc = A[c * LS + c];
       pc = (pc > 0.0 && isfinite(pc)) ? pc : 1.0;
       lv[u] = c <= r ? A[r * LS + c] / sqrt(pc) : 0.0;
+      dv[u] = c <= r ? inv[r * LS + c] * sr : 0.0;
     }
   }
   __syncthreads();
   if (act) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int c = c0 + TPR * u;
-      A[r * LS + c] = lv[u];
-      inv[r * LS + c] = (r == c) ? 1.0 : 0.0;
+      A[r * LS + c0 + TPR * u] = lv[u];
+      inv[r * LS + c0 + TPR * u] = dv[u];
     }
-  }
-  // D = L^-1 by a forward sweep over the rows of L applied to the identity: step m scales row m
-  // of D by 1 / L_mm (lazily, when it is read) and removes L_rm times it from the rows below.
-  for (int m = 0; m < NB; ++m) {
-    __syncthreads();
-    const double dm = 1.0 / A[m * LS + m];
-    if (act && r > m) {
-      const double f = A[r * LS + m] * dm;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int c = c0 + TPR * u;
-        if (c <= m) inv[r * LS + c] -= f * inv[m * LS + c];
-      }
-    }
-  }
-  __syncthreads();
-  if (act) {
-    const double dr = 1.0 / A[r * LS + r];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) inv[r * LS + c0 + TPR * u] *= dr;
   }
   __syncthreads();
   return ok;
