@@ -80,23 +80,43 @@ __global__ __launch_bounds__(256) void sparse_kernel(const Item* __restrict__ it
   const int t = threadIdx.x % T;
   if (team >= nitems) return;
   const Item it = items[team];
-  float x[E], acc[E];
-  load_row<T, E, CONTIG>(x, X + (int64_t)it.row * RP, t);
-#pragma unroll
-  for (int e = 0; e < E; ++e) acc[e] = 0.f;
   const int64_t b = it.begin;
   const int cnt = it.count;
+  // Everything that depends only on the item is requested at once: the factor row, the output
+  // row it adds to, and the first U entries.  The gathers then wait for a single round trip.
+  const bool rmw = it.slot < 0 && accumulate;
+  float* const yrow = it.slot < 0 ? Y + (int64_t)it.row * RP : scratch + (int64_t)it.slot * RP;
+  float x[E], acc[E], yv[E];
+  load_row<T, E, CONTIG>(x, X + (int64_t)it.row * RP, t);
+  if (rmw) load_row<T, E, CONTIG>(yv, yrow, t);
+  int32_t jn[U];
+  float sn[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const bool in = u < cnt;
+    jn[u] = in ? idx[b + u] : 0;
+    sn[u] = in ? val[b + u] : 0.f;
+  }
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
   int p = 0;
   for (; p + U <= cnt; p += U) {
     int32_t j[U];
     float s[U], pv[U][E], d[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      j[u] = idx[b + p + u];
-      s[u] = val[b + p + u];
+      j[u] = jn[u];
+      s[u] = sn[u];
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) load_row<T, E, CONTIG>(pv[u], P + (int64_t)j[u] * RP, t);
+    // the next group's entries, in flight during this group's arithmetic
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool in = p + U + u < cnt;
+      jn[u] = in ? idx[b + p + U + u] : 0;
+      sn[u] = in ? val[b + p + U + u] : 0.f;
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       float dd = 0.f;
@@ -115,24 +135,26 @@ __global__ __launch_bounds__(256) void sparse_kernel(const Item* __restrict__ it
       for (int e = 0; e < E; ++e) acc[e] = fmaf(c, pv[u][e], acc[e]);
     }
   }
-  for (; p < cnt; ++p) {
-    const int32_t j = idx[b + p];
-    const float s = val[b + p];
+  // the last cnt - p (< U) entries are in jn / sn
+#pragma unroll
+  for (int u = 0; u < U - 1; ++u) {
+    if (p + u >= cnt) break;
     float pv[E];
-    load_row<T, E, CONTIG>(pv, P + (int64_t)j * RP, t);
+    load_row<T, E, CONTIG>(pv, P + (int64_t)jn[u] * RP, t);
     float dd = 0.f;
 #pragma unroll
     for (int e = 0; e < E; ++e) dd = fmaf(x[e], pv[e], dd);
 #pragma unroll
     for (int off = T / 2; off > 0; off >>= 1) dd += __shfl_xor(dd, off, T);
-    const float c = s - fminf(dd, 0.f);
+    const float c = sn[u] - fminf(dd, 0.f);
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = fmaf(c, pv[e], acc[e]);
   }
-  if (it.slot < 0)
-    store_row<T, E, CONTIG>(Y + (int64_t)it.row * RP, acc, t, accumulate != 0);
-  else
-    store_row<T, E, CONTIG>(scratch + (int64_t)it.slot * RP, acc, t, false);
+  if (rmw) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] += yv[e];
+  }
+  store_row<T, E, CONTIG>(yrow, acc, t, false);
 }
 
 template <int T, int E, bool CONTIG>
