@@ -10,6 +10,8 @@ block of the other factor, the block of S and the momentum of that row), which l
 discrepancy to the step.
 """
 
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -228,6 +230,77 @@ def test_config4_split_bf16_first_steps_sampled(config4):
     p, S, ST = config4
     _say("config 4 split bf16, first steps checked on sampled rows")
     stepwise_sampled(p, S, ST, n_steps=6, flags=nmd.FLAG_SPLIT_BF16)
+
+
+# The same end to end for the 500000 x 50000 co-occurrence workload at rank 512.  Its oracle
+# sweep takes about 15-20 minutes of host fp64 work, so these run only when NMD_SLOW_TESTS=1.
+_slow = pytest.mark.skipif(os.environ.get("NMD_SLOW_TESTS") != "1",
+                           reason="about 20 minutes of host fp64 work; set NMD_SLOW_TESTS=1")
+_E5 = {}
+
+
+@_slow
+def test_config5_full_sweep_end_to_end_gpu(config5):
+    p, S, ST = config5
+    _say("config 5 full size: one sweep end to end on the GPU")
+    ctx = nmd.Context(p.m, p.n, p.r, p.block_m, p.block_n, seed=p.seed, mode=p.mode, eta=p.eta,
+                      momentum=p.momentum)
+    ctx.set_sparse_csr(p.row_ptr, p.col, p.val)
+    W, H = dev(p.W0), dev(p.H0)
+    ctx.sweep(W, H, 1)
+    _E5["f_gpu"] = ctx.objective(W, H)
+    _E5["W"], _E5["H"] = W.cpu().numpy(), H.cpu().numpy()
+    _E5["steps"] = ctx.schedule(0)
+    _E5["state"] = salsa.State(p.W0, p.H0)
+    ctx.close()
+    assert len(_E5["steps"]) == 38
+
+
+@_slow
+@pytest.mark.parametrize("k", range(38))
+def test_config5_full_sweep_end_to_end_oracle_step(config5, k):
+    p, S, ST = config5
+    if "state" not in _E5:
+        pytest.skip("the GPU sweep did not run")
+    code = _E5["steps"][k]
+    _say("config 5 oracle step", k, code)
+    salsa.run_steps(S, ST, _E5["state"], [code], p.block_m, p.block_n, p.eta, p.momentum)
+    _E5["done"] = _E5.get("done", 0) + 1
+
+
+@_slow
+def test_config5_full_sweep_end_to_end_factors(config5):
+    if _E5.get("done") != 38:
+        pytest.skip("the oracle sweep did not complete")
+    st = _E5["state"]
+    ew, eh = rel(_E5["W"], st.W), rel(_E5["H"], st.H)
+    print(f"config 5 one sweep end to end: rel err W {ew:.2e} H {eh:.2e}")
+    assert ew < TOL and eh < TOL
+
+
+@_slow
+@pytest.mark.parametrize("part", range(16))
+def test_config5_full_sweep_end_to_end_objective_part(config5, part):
+    p, S, ST = config5
+    if _E5.get("done") != 38:
+        pytest.skip("the oracle sweep did not complete")
+    st = _E5["state"]
+    r0, r1 = part * p.m // 16, (part + 1) * p.m // 16
+    _say("config 5 oracle objective rows", r0, r1)
+    Sp = S[r0:r1]
+    fp = salsa.objective(Sp, st.W[r0:r1], st.H)
+    _E5.setdefault("q", []).append((fp * sp_norm(Sp)) ** 2)
+
+
+@_slow
+def test_config5_full_sweep_end_to_end_objective(config5):
+    p, S, ST = config5
+    if len(_E5.get("q", [])) != 16:
+        pytest.skip("the oracle objective did not complete")
+    f_orc = float(np.sqrt(sum(_E5["q"])) / sp_norm(S))
+    print(f"config 5 objective after one sweep: gpu {_E5['f_gpu']:.7f} oracle {f_orc:.7f}")
+    assert abs(_E5["f_gpu"] - f_orc) <= TOL * f_orc
+    _E5.clear()
 
 
 @pytest.fixture(scope="module")

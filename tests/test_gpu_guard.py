@@ -180,3 +180,30 @@ def test_sweep_counter_counts_completed_sweeps_after_a_rejected_step():
         ctx.sweep(W, Hz, 3)
     assert e.value.code == nmd.ENOTPD and "sweep 1, step 0" in e.value.message
     assert ctx.sweep_count == 1
+
+
+def test_guard_in_deterministic_mode():
+    """The safeguard with the deterministic half-steps (eqs. spLsqA, spLsqB) at an over-long step
+    (eta = 1.7, momentum 0.9): sweeps 1 and 5 raise the objective in the oracle and are undone;
+    the GPU makes the same decisions (a sweep is the two half-steps here, so the step ids of a
+    sweep differ from the stochastic ones)."""
+    m, n, r, blk, sweeps = 300, 260, 12, 64, 6
+    row_ptr, col, val, W0, H0 = _problem(m, n, r, 0.1, 7)
+    S = salsa.csr_matrix(m, n, row_ptr, col, val)
+    st = salsa.State(W0, H0)
+    eta_o, fo, rej = salsa.guarded_sweeps(S, S.T.tocsr(), st, blk, blk, 3, sweeps,
+                                          "deterministic", 1.7, 0.9, eta_min=1e-3)
+    assert [t for t, _, _ in rej] == [1, 5]
+    assert min(f / fo[t] - 1.0 for t, _, f in rej) > 2e-3
+    assert max(fo[k] / fo[k - 1] - 1.0 for k in range(1, len(fo))) < -1e-2
+    _say("guard, deterministic mode")
+    ctx = _ctx(m, n, r, blk, row_ptr, col, val, nmd.FLAG_GUARD, eta=1.7, mom=0.9, eta_min=1e-3,
+               mode="deterministic")
+    W, H = dev(W0), dev(H0)
+    ctx.sweep(W, H, sweeps)
+    f = ctx.sweep_objectives()
+    print("f gpu   ", np.round(f, 6))
+    print("f oracle", np.round(fo, 6))
+    assert ctx.step_size() == (np.float32(eta_o), len(rej))
+    assert np.max(np.abs(f - fo) / np.asarray(fo)) <= TOL
+    assert rel(W.cpu().numpy(), st.W) <= TOL and rel(H.cpu().numpy(), st.H) <= TOL
