@@ -95,8 +95,10 @@ __device__ __forceinline__ void put_tile(double* dst, const dx4& acc, double s, 
 }
 
 // 1 / x to full double precision: the fp32 reciprocal estimate refined by two Newton steps
-// (each doubles the correct bits: 2^-23 -> 2^-46 -> beyond 2^-53).
+// (each doubles the correct bits: 2^-23 -> 2^-46 -> beyond 2^-53); a plain division where x is
+// outside the range the fp32 estimate covers.
 __device__ __forceinline__ double recip(double x) {
+  if (!(x > 1e-30 && x < 1e30)) return 1.0 / x;  // outside the fp32 estimate's range
   double y = (double)(1.0f / (float)x);
   y = y * (2.0 - x * y);
   return y * (2.0 - x * y);
