@@ -12,8 +12,9 @@
 //      M_ij = -D_i sum_{l=j}^{i-1} L_il M_lj.
 //   3. -G^-1 = -M^T M by 64 x 64 tiles: tile (a, b) = -sum_{l >= max(a, b)} M_la^T M_lb.
 //
-// A pivot that is not positive (or not finite) flags the step as not positive definite; the
-// apply then writes nothing.  Blocks of NB x NB doubles are staged in LDS with row stride
+// The launches take a batch of matrices (blockIdx.y), each with its own work area and step id.
+// A pivot that is not positive (or not finite) flags that step as not positive definite; its
+// apply and the later ones then write nothing.  Blocks of NB x NB doubles are staged in LDS with row stride
 // NB + 1; fp64 MFMA v_mfma_f64_16x16x4f64: srcA lane l = A[l % 16][l / 16], srcB lane
 // l = B[l / 16][l % 16], accumulator register v of lane l = D[4 v + l / 16][l % 16].
 
@@ -27,12 +28,17 @@ namespace {
 
 constexpr int kThreads = 1024;
 
-__device__ __forceinline__ void flag_notpd(int* status, int step_id) {
-  if (*(volatile int*)status == 0) {
-    atomicOr(&status[0], (int)STATUS_NOTPD);
-    atomicMin(&status[1], step_id);
+// Work area of matrix b: L, M = L^-1, -G^-1 (rp x rp each) and the diagonal blocks D_k.
+struct Work {
+  double *L, *M, *Gneg, *D;
+  __host__ __device__ Work(double* base, int64_t per, int b, int rp) {
+    double* w = base + per * b;
+    L = w;
+    M = w + (int64_t)rp * rp;
+    Gneg = w + 2 * (int64_t)rp * rp;
+    D = w + 3 * (int64_t)rp * rp;
   }
-}
+};
 
 // Copies the NB x NB block at (bi, bj) of a row-major matrix with leading dimension ld into LDS.
 template <int NB>
@@ -175,15 +181,19 @@ __device__ bool factor_block(double* A, double* inv) {
 
 }  // namespace
 
-// Launch k of step 1: block row i = k + blockIdx.x.
+// Launch k of step 1: block row i = k + blockIdx.x of matrix blockIdx.y.
 template <int NB>
-__global__ __launch_bounds__(kThreads) void chol_col_kernel(const double* __restrict__ G,
-                                                            double* __restrict__ L,
-                                                            double* __restrict__ D, int rp,
-                                                            int k, int* status, int step_id) {
+__global__ __launch_bounds__(kThreads) void chol_col_kernel(const double* __restrict__ Gall,
+                                                            double* __restrict__ work,
+                                                            int64_t per, int rp, int k,
+                                                            int* status, SolveBatch sb) {
   constexpr int LS = NB + 1;
   constexpr int NT = NB / 16;  // sub-tiles per dimension
   __shared__ double sA[NB * LS], sB[NB * LS], s1[NB * LS], s2[NB * LS];
+  const Work wk(work, per, blockIdx.y, rp);
+  const double* __restrict__ G = Gall + (int64_t)blockIdx.y * rp * rp;
+  double* __restrict__ L = wk.L;
+  double* __restrict__ D = wk.D;
   const int i = k + blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int q = lane >> 4, l16 = lane & 15;
@@ -212,7 +222,8 @@ __global__ __launch_bounds__(kThreads) void chol_col_kernel(const double* __rest
     }
   }
   const bool ok = factor_block<NB>(sA, s1);  // s1 = D_k = L_kk^-1
-  if (!ok && blockIdx.x == 0 && threadIdx.x == 0) flag_notpd(status, step_id);
+  if (!ok && blockIdx.x == 0 && threadIdx.x == 0)
+    flag_status(status, STATUS_NOTPD, sb.step_id[blockIdx.y]);
   if (i == k) {
     for (int e = threadIdx.x; e < NB * NB; e += kThreads) {
       const int r = e / NB, c = e - r * NB;
@@ -231,14 +242,17 @@ __global__ __launch_bounds__(kThreads) void chol_col_kernel(const double* __rest
   }
 }
 
-// Step 2: block column j = blockIdx.x of M = L^-1 into Mb (rows i >= j).
+// Step 2: block column j = blockIdx.x of M = L^-1 (rows i >= j) of matrix blockIdx.y.
 template <int NB>
-__global__ __launch_bounds__(kThreads) void chol_trinv_kernel(const double* __restrict__ L,
-                                                              const double* __restrict__ D,
-                                                              double* __restrict__ Mb, int rp) {
+__global__ __launch_bounds__(kThreads) void chol_trinv_kernel(double* __restrict__ work,
+                                                              int64_t per, int rp) {
   constexpr int LS = NB + 1;
   constexpr int NT = NB / 16;
   __shared__ double sL[NB * LS], sM[NB * LS], sT[NB * LS], sD[NB * LS];
+  const Work wk(work, per, blockIdx.y, rp);
+  const double* __restrict__ L = wk.L;
+  const double* __restrict__ D = wk.D;
+  double* __restrict__ Mb = wk.M;
   const int nb = rp / NB;
   const int j = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -275,14 +289,18 @@ __global__ __launch_bounds__(kThreads) void chol_trinv_kernel(const double* __re
   }
 }
 
-// Step 3: tile (a, b), a <= b, of -G^-1 = -M^T M, written to both (a, b) and (b, a).
+// Step 3: tile (a, b), a <= b, of -G^-1 = -M^T M of matrix blockIdx.y, written to both (a, b)
+// and (b, a).
 template <int NB>
-__global__ __launch_bounds__(kThreads) void chol_gram_kernel(const double* __restrict__ Mb,
-                                                             double* __restrict__ Gneg, int rp,
-                                                             const int* status) {
+__global__ __launch_bounds__(kThreads) void chol_gram_kernel(double* __restrict__ work,
+                                                             int64_t per, int rp,
+                                                             const int* status, SolveBatch sb) {
   constexpr int LS = NB + 1;
   constexpr int NT = NB / 16;
   __shared__ double s1[NB * LS], s2[NB * LS];
+  const Work wk(work, per, blockIdx.y, rp);
+  const double* __restrict__ Mb = wk.M;
+  double* __restrict__ Gneg = wk.Gneg;
   const int nb = rp / NB;
   int p = blockIdx.x, a = 0;  // pair index -> (a <= b)
   while (p >= nb - a) {
@@ -290,7 +308,7 @@ __global__ __launch_bounds__(kThreads) void chol_gram_kernel(const double* __res
     ++a;
   }
   const int b = a + p;
-  if (*(volatile const int*)status != 0) return;  // factorisation failed: the apply skips
+  if (step_blocked(status, sb.step_id[blockIdx.y])) return;  // its apply writes nothing
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int q = lane >> 4, l16 = lane & 15;
   const bool mw = wave < NT * NT;
@@ -318,27 +336,27 @@ int64_t chol_work_doubles(int rp) {
   return 3 * (int64_t)rp * rp + (int64_t)(rp / NB) * NB * NB;
 }
 
-hipError_t launch_chol_inverse(const double* G, double* work, int rp, int* status, int step_id,
-                               double** result, hipStream_t st) {
+hipError_t launch_chol_inverse(const double* G, double* work, int rp, int* status,
+                               const SolveBatch& sb, double** result, hipStream_t st) {
+  if (sb.n < 1 || sb.n > kSolveBatch) return hipErrorInvalidValue;
   const int NB = rp < 64 ? rp : 64;
   const int nb = rp / NB;
-  double* L = work;
-  double* M = work + (int64_t)rp * rp;
-  double* Gneg = work + 2 * (int64_t)rp * rp;
-  double* D = work + 3 * (int64_t)rp * rp;
+  const int64_t per = chol_work_doubles(rp);
+  const unsigned nm = (unsigned)sb.n;
 #define CHOL_NB(B)                                                                           \
   case B: {                                                                                  \
     for (int k = 0; k < nb; ++k) {                                                           \
-      hipLaunchKernelGGL((chol_col_kernel<B>), dim3(nb - k), dim3(kThreads), 0, st, G, L, D, rp, \
-                         k, status, step_id);                                                \
+      hipLaunchKernelGGL((chol_col_kernel<B>), dim3(nb - k, nm), dim3(kThreads), 0, st, G, work, \
+                         per, rp, k, status, sb);                                            \
       hipError_t e = hipGetLastError();                                                      \
       if (e != hipSuccess) return e;                                                         \
     }                                                                                        \
-    hipLaunchKernelGGL((chol_trinv_kernel<B>), dim3(nb), dim3(kThreads), 0, st, L, D, M, rp); \
+    hipLaunchKernelGGL((chol_trinv_kernel<B>), dim3(nb, nm), dim3(kThreads), 0, st, work, per, \
+                       rp);                                                                  \
     hipError_t e = hipGetLastError();                                                        \
     if (e != hipSuccess) return e;                                                           \
-    hipLaunchKernelGGL((chol_gram_kernel<B>), dim3(nb * (nb + 1) / 2), dim3(kThreads), 0, st, M, \
-                       Gneg, rp, status);                                                    \
+    hipLaunchKernelGGL((chol_gram_kernel<B>), dim3(nb * (nb + 1) / 2, nm), dim3(kThreads), 0, st, \
+                       work, per, rp, status, sb);                                           \
     break;                                                                                   \
   }
   switch (NB) {
@@ -349,7 +367,7 @@ hipError_t launch_chol_inverse(const double* G, double* work, int rp, int* statu
     default: return hipErrorInvalidValue;
   }
 #undef CHOL_NB
-  *result = Gneg;
+  for (int b = 0; b < sb.n; ++b) result[b] = Work(work, per, b, rp).Gneg;
   return hipGetLastError();
 }
 

@@ -93,6 +93,7 @@ struct nmd_ctx {
   int64_t scratch_floats = 0;
 
   double *G = nullptr, *Gwork = nullptr, *Gpart = nullptr;
+  double* Gneg[nmd::kSolveBatch] = {};  // -G^-1 of each step of the current run (in Gwork)
   int gram_chunks_max = 64;
   double* objpart = nullptr;
   int64_t objpart_count = 0;
@@ -259,7 +260,8 @@ int ensure_device(nmd_ctx* c) {
         dalloc(&c->VA, mpad * rp) != hipSuccess || dalloc(&c->VB, npad * rp) != hipSuccess ||
         dalloc(&c->A2, mpad * rp) != hipSuccess || dalloc(&c->B2, npad * rp) != hipSuccess ||
         dalloc(&c->VA2, mpad * rp) != hipSuccess || dalloc(&c->VB2, npad * rp) != hipSuccess ||
-        dalloc(&c->G, rp * rp) != hipSuccess || dalloc(&c->Gwork, nmd::chol_work_doubles((int)rp)) != hipSuccess ||
+        dalloc(&c->G, nmd::kSolveBatch * rp * rp) != hipSuccess ||
+        dalloc(&c->Gwork, nmd::kSolveBatch * nmd::chol_work_doubles((int)rp)) != hipSuccess ||
         dalloc(&c->Gpart, (int64_t)c->gram_chunks_max * rp * rp) != hipSuccess ||
         dalloc(&c->objout, 8) != hipSuccess || dalloc(&c->status, 2) != hipSuccess ||
         dalloc(&c->g2, 2) != hipSuccess) {
@@ -416,8 +418,45 @@ void swap_side(nmd_ctx* c, bool wside) {
   }
 }
 
+// The Gram matrices of a run of consecutive steps of one side and their -G^-1: they depend only
+// on the panel rows of each step's block, and the run's steps change only the other factor, so
+// the whole run's solves are formed in one set of launches on the side stream while the first
+// step's contraction runs on the caller's stream; every apply of the run waits for them.
+// blocks[i] < 0 (deterministic mode) takes every block of the side as one step.
+int factor_run(nmd_ctx* c, bool wstep, const int32_t* blocks, int n, int first_step_id,
+               hipStream_t st) {
+  const Side& sd = wstep ? c->ws : c->hs;
+  const float* P = wstep ? c->B : c->A;
+  nmd::SolveBatch sb{};
+  sb.n = n;
+  double flops = 0.0;
+  int64_t blk_max = 0;
+  for (int b = 0; b < n; ++b) {
+    const int32_t block = blocks[b];
+    const int64_t j0 = block >= 0 ? sd.bounds[block] : 0;
+    const int64_t j1 = block >= 0 ? sd.bounds[block + 1] : sd.other;
+    sb.step_id[b] = first_step_id + b;
+    sb.j0[b] = j0;
+    sb.blk[b] = j1 - j0;
+    blk_max = std::max(blk_max, j1 - j0);
+    // Gram 2 blk r^2; Cholesky, inverse of the factor and the product M^T M r^3 / 3 each
+    flops += 2.0 * (j1 - j0) * (double)c->r * c->r + (double)c->rp * c->rp * c->rp;
+  }
+  const int nchunks = std::max(1, std::min(gram_chunks(blk_max), c->gram_chunks_max / n));
+  HIP_TRY(c, hipEventRecord(c->ev_fork, st));
+  HIP_TRY(c, hipStreamWaitEvent(c->side, c->ev_fork, 0));
+  {
+    Scope sc(c, c->side, K_FACTOR, flops, 0.0);
+    HIP_TRY(c, nmd::launch_gram(P, sb, c->r, c->rp, c->Gpart, nchunks, c->G, c->side));
+    HIP_TRY(c, nmd::launch_chol_inverse(c->G, c->Gwork, c->rp, c->status, sb, c->Gneg, c->side));
+  }
+  HIP_TRY(c, hipEventRecord(c->ev_join, c->side));
+  return NMD_OK;
+}
+
+// One update step with the -G^-1 that factor_run formed for it.
 int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, int step_id,
-                hipStream_t st) {
+                const double* Gneg, hipStream_t st) {
   Side& sd = wstep ? c->ws : c->hs;
   float* X = wstep ? c->A : c->B;
   const float* P = wstep ? c->B : c->A;
@@ -429,18 +468,6 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
   const int rp = c->rp;
   const float* PJ = P + j0 * rp;
 
-  // Gram matrix and its inverse depend only on the panel rows of the block: they run on the
-  // side stream while the contraction runs on the caller's stream, and the solve joins both.
-  double* Gneg = nullptr;
-  HIP_TRY(c, hipEventRecord(c->ev_fork, st));
-  HIP_TRY(c, hipStreamWaitEvent(c->side, c->ev_fork, 0));
-  {
-    // Gram 2 blk r^2; Cholesky, inverse of the factor and the product M^T M r^3 / 3 each
-    Scope sc(c, c->side, K_FACTOR, 2.0 * blk * (double)c->r * c->r + (double)rp * rp * rp, 0.0);
-    HIP_TRY(c, nmd::launch_gram(PJ, blk, c->r, rp, c->Gpart, gram_chunks(blk), c->G, c->side));
-    HIP_TRY(c, nmd::launch_chol_inverse(c->G, c->Gwork, rp, c->status, step_id, &Gneg, c->side));
-  }
-  HIP_TRY(c, hipEventRecord(c->ev_join, c->side));
   const int64_t ns = nsplit_for(rows, blk, rp, c->dense_slots);
   const int64_t y_stride = rows * rp;
   if (ns * y_stride > c->ypart_floats)
@@ -536,7 +563,7 @@ int conclude(nmd_ctx* c, float* W, float* H, hipStream_t st, int64_t first_sweep
     HIP_TRY(c, hipStreamSynchronize(st));
     return NMD_OK;
   }
-  const int step = c->h_status[1];
+  const int step = nmd::status_step(c->h_status[1]);
   c->last_fail_step = step;
   for (auto it = c->enqueued.rbegin(); it != c->enqueued.rend(); ++it)
     if (it->first >= step) swap_side(c, it->second);  // undo the steps from the rejected one on
@@ -546,7 +573,7 @@ int conclude(nmd_ctx* c, float* W, float* H, hipStream_t st, int64_t first_sweep
   HIP_TRY(c, hipMemsetAsync(c->status + 1, 0x7f, sizeof(int), st));
   HIP_TRY(c, hipStreamSynchronize(st));
   const std::string where = describe_step(c, step, first_sweep, steps_per);
-  if (flags & 1)
+  if (nmd::status_kind(c->h_status[1]) == nmd::STATUS_NOTPD)
     return fail(c, NMD_ENOTPD, "Gram matrix not positive definite at %s; later steps skipped",
                 where.c_str());
   return fail(c, NMD_ENONFINITE, "non-finite factor entry produced at %s; later steps skipped",
@@ -602,17 +629,33 @@ int enqueue_sweep(nmd_ctx* c, const std::vector<int32_t>& list, bool full_halves
                   hipStream_t st) {
   int rc;
   if (full_halves) {
-    if ((rc = factor_step(c, true, -1, c->opt.eta, c->opt.momentum, *step_id, st))) return rc;
-    *step_id += (int)c->ws.nblk();
-    if ((rc = factor_step(c, false, -1, c->opt.eta, c->opt.momentum, *step_id, st))) return rc;
-    *step_id += (int)c->hs.nblk();
+    const int32_t all = -1;
+    for (const bool w : {true, false}) {
+      if ((rc = factor_run(c, w, &all, 1, *step_id, st))) return rc;
+      if ((rc = factor_step(c, w, -1, c->opt.eta, c->opt.momentum, *step_id, c->Gneg[0], st)))
+        return rc;
+      *step_id += (int)(w ? c->ws.nblk() : c->hs.nblk());
+    }
     return NMD_OK;
   }
-  for (int32_t code : list) {
-    const bool w = code > 0;
-    const int32_t b = (w ? code : -code) - 1;
-    if ((rc = factor_step(c, w, b, c->opt.eta, c->opt.momentum, *step_id, st))) return rc;
-    ++*step_id;
+  // runs of consecutive steps of one side, at most kSolveBatch long
+  size_t i = 0;
+  while (i < list.size()) {
+    const bool w = list[i] > 0;
+    int32_t blocks[nmd::kSolveBatch];
+    int n = 0;
+    while (i + n < list.size() && n < nmd::kSolveBatch && (list[i + n] > 0) == w) {
+      blocks[n] = (w ? list[i + n] : -list[i + n]) - 1;
+      ++n;
+    }
+    if ((rc = factor_run(c, w, blocks, n, *step_id, st))) return rc;
+    for (int b = 0; b < n; ++b) {
+      if ((rc = factor_step(c, w, blocks[b], c->opt.eta, c->opt.momentum, *step_id, c->Gneg[b],
+                            st)))
+        return rc;
+      ++*step_id;
+    }
+    i += n;
   }
   return NMD_OK;
 }
@@ -693,9 +736,9 @@ int sweeps_tracked(nmd_ctx* c, float* W, float* H, int32_t n_sweeps, hipStream_t
       done = n_sweeps;
       break;
     }
-    const int step = c->h_status[1];
+    const int step = nmd::status_step(c->h_status[1]);
     const int32_t bad = done + step / steps_per;  // the sweep of the first failure
-    if (flags == nmd::STATUS_RISE) {
+    if (nmd::status_kind(c->h_status[1]) == nmd::STATUS_RISE) {
       // every step after the rise wrote nothing: the copies hold the factors before sweep `bad`
       HIP_TRY(c, hipMemcpyAsync(c->A, c->SA, (size_t)ma * sizeof(float), hipMemcpyDeviceToDevice, st));
       HIP_TRY(c, hipMemcpyAsync(c->B, c->SB, (size_t)nb * sizeof(float), hipMemcpyDeviceToDevice, st));

@@ -87,8 +87,7 @@ __global__ void guard_kernel(const double* __restrict__ q_old, const double* __r
                              double tol2, int* status, int step_id) {
   if (threadIdx.x != 0 || *(volatile const int*)status != 0) return;
   if (!(*q_new <= tol2 * *q_old)) {
-    atomicOr(&status[0], (int)STATUS_RISE);
-    atomicMin(&status[1], step_id);
+    flag_status(status, STATUS_RISE, step_id);
   }
 }
 

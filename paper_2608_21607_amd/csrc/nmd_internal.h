@@ -8,8 +8,33 @@
 
 namespace nmd {
 
-// Device status word: status[0] holds flag bits, status[1] the first failing step id.
+// Device status word: status[0] is the union of the flag bits raised; status[1] the smallest
+// step_id * 8 + bit among them, so it names the first failing step and why it failed.  A
+// failure stops the step that raised it and every step after it (step_blocked), but not the
+// steps before it, whose work may be enqueued behind the check that failed (the solves of a run
+// of steps are formed ahead of their applies).
 enum { STATUS_NOTPD = 1, STATUS_NONFINITE = 2, STATUS_RISE = 4 };
+inline int status_step(int word) { return word >> 3; }
+inline int status_kind(int word) { return word & 7; }
+__device__ __forceinline__ void flag_status(int* status, int bit, int step_id) {
+  atomicOr(&status[0], bit);
+  atomicMin(&status[1], step_id * 8 + bit);
+}
+__device__ __forceinline__ bool step_blocked(const int* status, int step_id) {
+  return *(volatile const int*)status != 0 &&
+         (*(volatile const int*)(status + 1) >> 3) <= step_id;
+}
+
+// The solves of up to kSolveBatch consecutive steps of one side, formed in one set of
+// launches: matrix b is the Gram matrix of panel rows j0[b] .. j0[b] + blk[b] of step
+// step_id[b].
+constexpr int kSolveBatch = 8;
+struct SolveBatch {
+  int n;
+  int step_id[kSolveBatch];
+  int64_t j0[kSolveBatch];
+  int64_t blk[kSolveBatch];
+};
 
 // Padded rank: the kernels work on r_p columns (zeros beyond r).
 int padded_rank(int r);
@@ -60,19 +85,22 @@ hipError_t launch_sparse(const Item* items, int64_t nitems, const int32_t* idx, 
 hipError_t launch_fixup(const Split* splits, int64_t nsplits, const float* scratch, int rp,
                         float* Y, int accumulate, hipStream_t st);
 
-// Gram matrix G = P^T P (fp64, rp x rp, identity on the padded diagonal) of `blk` rows.
-hipError_t launch_gram(const float* P, int64_t blk, int r, int rp, double* Gpart, int nchunks,
-                       double* G, hipStream_t st);
-// -G^-1 through the Cholesky factorisation G = L L^T (chol.hip): *result receives -G^-1
-// (rp x rp, inside `work`, chol_work_doubles(rp) doubles); a non-positive pivot flags status.
+// Gram matrices G_b = P_b^T P_b (fp64, rp x rp, identity on the padded diagonal) of the panel
+// row ranges of a batch, G_b at G + b rp^2; Gpart holds sb.n * nchunks * rp^2 doubles.
+hipError_t launch_gram(const float* P, const SolveBatch& sb, int r, int rp, double* Gpart,
+                       int nchunks, double* G, hipStream_t st);
+// -G_b^-1 through the Cholesky factorisation G_b = L L^T (chol.hip) for each matrix of a batch
+// (G_b at G + b rp^2): result[b] receives -G_b^-1 (rp x rp, inside `work`, which holds
+// sb.n * chol_work_doubles(rp) doubles); a non-positive pivot flags status with the step id of
+// its matrix.
 int64_t chol_work_doubles(int rp);
-hipError_t launch_chol_inverse(const double* G, double* work, int rp, int* status, int step_id,
-                               double** result, hipStream_t st);
+hipError_t launch_chol_inverse(const double* G, double* work, int rp, int* status,
+                               const SolveBatch& sb, double** result, hipStream_t st);
 // Vout = gamma Vin + eta U (-Gneg), Xout = Xin + Vout, where U = Delta P_J is the sum (fp64)
 // of the nsplit partial outputs plus, when Ysp is not NULL, a separate correction buffer
 // (rows x rp), and -Gneg = (P_J^T P_J)^-1.  The outputs are other buffers than the inputs, so
 // a step that a later check rejects leaves its inputs intact.  Nothing is written once status
-// holds a failure from an earlier kernel.
+// holds a failure of this step or an earlier one.
 hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const float* Ysp,
                         const double* Gneg, const float* Xin, const float* Vin, float* Xout,
                         float* Vout, int64_t rows, int rp, float eta, float gamma, int* status,

@@ -12,11 +12,6 @@
 
 namespace nmd {
 
-// status[0]: flag bits; status[1]: first failing step id.
-__device__ __forceinline__ void flag(int* status, int bit, int step_id) {
-  atomicOr(&status[0], bit);
-  atomicMin(&status[1], step_id);
-}
 
 typedef double doublex4 __attribute__((ext_vector_type(4)));
 
@@ -26,8 +21,13 @@ typedef double doublex4 __attribute__((ext_vector_type(4)));
 // 16-row block w of the tile; srcA lane l = P[k + l/16][ti T + 16 w + l%16], srcB lane l =
 // P[k + l/16][tj T + 16 cb + l%16] (fp32 inputs widened exactly to fp64).
 template <int T>
-__global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ P, int64_t blk, int rp,
-                                                   double* __restrict__ Gpart, int nchunks) {
+__global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ Pbase, SolveBatch sb,
+                                                   int rp, double* __restrict__ Gpart_all,
+                                                   int nchunks) {
+  // matrix blockIdx.z of the batch: panel rows j0 .. j0 + blk of Pbase, partials at its slot
+  const float* __restrict__ P = Pbase + sb.j0[blockIdx.z] * rp;
+  const int64_t blk = sb.blk[blockIdx.z];
+  double* __restrict__ Gpart = Gpart_all + (int64_t)blockIdx.z * nchunks * rp * rp;
   constexpr int NCB = T / 16;
   constexpr int KB = 64;
   __shared__ float si[KB][T + 1];
@@ -82,9 +82,11 @@ __global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ P, 
 }
 
 // G[i][j] = sum over chunks of the upper-tile partial (mirrored), identity on padded diagonal.
-__global__ __launch_bounds__(256) void gram_reduce_kernel(const double* __restrict__ Gpart,
+__global__ __launch_bounds__(256) void gram_reduce_kernel(const double* __restrict__ Gpart_all,
                                                           int nchunks, int r, int rp, int T,
-                                                          double* __restrict__ G) {
+                                                          double* __restrict__ G_all) {
+  const double* __restrict__ Gpart = Gpart_all + (int64_t)blockIdx.y * nchunks * rp * rp;
+  double* __restrict__ G = G_all + (int64_t)blockIdx.y * rp * rp;
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (e >= (int64_t)rp * rp) return;
   const int i = (int)(e / rp), j = (int)(e % rp);
@@ -96,22 +98,24 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const double* __restri
   G[e] = s;
 }
 
-hipError_t launch_gram(const float* P, int64_t blk, int r, int rp, double* Gpart, int nchunks,
-                       double* G, hipStream_t st) {
+hipError_t launch_gram(const float* P, const SolveBatch& sb, int r, int rp, double* Gpart,
+                       int nchunks, double* G, hipStream_t st) {
+  if (sb.n < 1 || sb.n > kSolveBatch) return hipErrorInvalidValue;
   const int T = rp < 64 ? rp : 64;
   const int nt = rp / T;
   const int npairs = nt * (nt + 1) / 2;
+  const dim3 grid(npairs, nchunks, sb.n);
   switch (T) {
-    case 16: hipLaunchKernelGGL((gram_kernel<16>), dim3(npairs, nchunks), dim3(256), 0, st, P, blk, rp, Gpart, nchunks); break;
-    case 32: hipLaunchKernelGGL((gram_kernel<32>), dim3(npairs, nchunks), dim3(256), 0, st, P, blk, rp, Gpart, nchunks); break;
-    case 48: hipLaunchKernelGGL((gram_kernel<48>), dim3(npairs, nchunks), dim3(256), 0, st, P, blk, rp, Gpart, nchunks); break;
-    case 64: hipLaunchKernelGGL((gram_kernel<64>), dim3(npairs, nchunks), dim3(256), 0, st, P, blk, rp, Gpart, nchunks); break;
+    case 16: hipLaunchKernelGGL((gram_kernel<16>), grid, dim3(256), 0, st, P, sb, rp, Gpart, nchunks); break;
+    case 32: hipLaunchKernelGGL((gram_kernel<32>), grid, dim3(256), 0, st, P, sb, rp, Gpart, nchunks); break;
+    case 48: hipLaunchKernelGGL((gram_kernel<48>), grid, dim3(256), 0, st, P, sb, rp, Gpart, nchunks); break;
+    case 64: hipLaunchKernelGGL((gram_kernel<64>), grid, dim3(256), 0, st, P, sb, rp, Gpart, nchunks); break;
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t n = (int64_t)rp * rp;
-  hipLaunchKernelGGL(gram_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+  hipLaunchKernelGGL(gram_reduce_kernel, dim3((unsigned)((n + 255) / 256), sb.n), dim3(256), 0, st,
                      Gpart, nchunks, r, rp, T, G);
   return hipGetLastError();
 }
@@ -149,7 +153,7 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Yp
   constexpr int LS = RP + 1;
   constexpr int PD = 2;  // prefetch distance in k-steps
   __shared__ double ys[RW * LS];
-  if (*(volatile const int*)status != 0) return;  // an earlier step failed: factors stay
+  if (step_blocked(status, step_id)) return;  // this or an earlier step failed: factors stay
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int q = lane >> 4, l16 = lane & 15;
@@ -236,7 +240,7 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Yp
           Vout[o] = vf;
         }
       }
-  if (bad) flag(status, STATUS_NONFINITE, step_id);
+  if (bad) flag_status(status, STATUS_NONFINITE, step_id);
 }
 
 // Apply for r_p >= 64: a workgroup takes RW rows; each of its 4 waves computes all RW rows for
@@ -271,7 +275,7 @@ __global__ __launch_bounds__(256, 2) void apply_wide_kernel(const float* __restr
   constexpr int LS = RP + 1;
   constexpr int PD = 2;  // prefetch distance in k-steps
   __shared__ float ys[RW * LS];
-  if (*(volatile const int*)status != 0) return;  // an earlier step failed: factors stay
+  if (step_blocked(status, step_id)) return;  // this or an earlier step failed: factors stay
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int q = lane >> 4, l16 = lane & 15;
@@ -356,7 +360,7 @@ __global__ __launch_bounds__(256, 2) void apply_wide_kernel(const float* __restr
           Vout[o] = vf;
         }
       }
-  if (bad) flag(status, STATUS_NONFINITE, step_id);
+  if (bad) flag_status(status, STATUS_NONFINITE, step_id);
 }
 
 hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const float* Ysp,
