@@ -246,7 +246,7 @@ def main():
         ctx.sweep(W, H, 1)
         log(f"warmup sweep {k + 1}/{args.warmup} done")
     torch.cuda.synchronize()
-    for kern in range(4):
+    for kern in range(5):
         ctx.kernel_timing(kern, reset=True)
     ctx.dense_blocks(reset=True)
 
@@ -285,8 +285,8 @@ def main():
     log(f"objective per sweep: {' '.join(f'{x:.4f}' for x in traj)} ({rises} rises)")
 
     rp = ((p.r + 15) // 16) * 16 if p.r <= 64 else ((p.r + 63) // 64) * 64  # padded rank
-    kt = [ctx.kernel_timing(k) for k in range(4)]
-    dense, sparse, factor, apply_ = kt
+    kt = [ctx.kernel_timing(k) for k in range(5)]
+    dense, sparse, factor, apply_, join = kt
     sweeps_per_s = args.steps / (ms / 1e3)
     dense_equiv = 4.0 * p.m * p.n * p.r * sweeps_per_s / 1e12
     dense_equiv_8mnr = 8.0 * p.m * p.n * p.r * sweeps_per_s / 1e12
@@ -350,6 +350,9 @@ def main():
         "kernel_ms_per_sweep": {
             "dense": dense["ms"] / args.steps, "sparse": sparse["ms"] / args.steps,
             "gram_inverse": factor["ms"] / args.steps, "solve_apply": apply_["ms"] / args.steps,
+            # span of the side stream's Gram and inverse work (beside the dense kernel), and the
+            # part of it the updates waited for
+            "side_stream_wait": join["ms"] / args.steps,
         },
         "objective_before_after": [f0, f1],
         "objective_per_sweep": traj,

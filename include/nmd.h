@@ -298,7 +298,9 @@ int nmd_get_dense_blocks(nmd_ctx* ctx, int64_t* run, int64_t* total, int64_t* en
  * stream the work ran on) and launch count of one kernel class since the last reset of the
  * timers, plus the algorithmic work of those launches.  kernel: 0 = fused dense contraction
  * (flops = 4 rows blk r per launch), 1 = sparse correction (bytes = algorithmic HBM bytes),
- * 2 = Gram matrix and inverse, 3 = solve and update.  Synchronises the recorded events.
+ * 2 = Gram matrices and inverses (side stream; one entry per run of same-side steps), 3 = solve
+ * and update, 4 = the time the caller's stream waited for the side stream before an update
+ * (zero when the solve was ready; no work).  Synchronises the recorded events.
  * reset != 0 clears the timers after reading.  Any output pointer may be NULL.
  */
 int nmd_get_kernel_timing(nmd_ctx* ctx, int32_t kernel, double* total_ms, int64_t* launches,

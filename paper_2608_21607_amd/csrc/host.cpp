@@ -37,7 +37,7 @@ constexpr int64_t kTargetWgs = 2048;  // dense workgroups wanted per launch (256
 constexpr int64_t kWgFixedRows = 32;  // per-workgroup set-up and write-back, in panel rows
 constexpr int kObjSubMax = 16;        // sub-splits of a column block in the objective
 
-enum { K_DENSE = 0, K_SPARSE = 1, K_FACTOR = 2, K_APPLY = 3, K_COUNT = 4 };
+enum { K_DENSE = 0, K_SPARSE = 1, K_FACTOR = 2, K_APPLY = 3, K_JOIN = 4, K_COUNT = 5 };
 
 // The arrangement of S for one factor (ingest.h) and its device copies.
 struct Side : nmd::SideHost {
@@ -115,10 +115,10 @@ struct nmd_ctx {
   // timing
   std::vector<TimerRec> pending;
   std::vector<hipEvent_t> event_pool;
-  double t_ms[K_COUNT] = {0, 0, 0, 0};
-  int64_t t_launch[K_COUNT] = {0, 0, 0, 0};
-  double t_flops[K_COUNT] = {0, 0, 0, 0};
-  double t_bytes[K_COUNT] = {0, 0, 0, 0};
+  double t_ms[K_COUNT] = {};
+  int64_t t_launch[K_COUNT] = {};
+  double t_flops[K_COUNT] = {};
+  double t_bytes[K_COUNT] = {};
 };
 
 namespace {
@@ -510,7 +510,11 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
     HIP_TRY(c, nmd::launch_fixup(sd.d_splits + sd.split_off[b], nsp, c->scratch, rp, c->Ypart, 1,
                                  st));
   }
-  HIP_TRY(c, hipStreamWaitEvent(st, c->ev_join, 0));
+  {
+    // the time the caller's stream waits here for the side stream (zero once it is ahead)
+    Scope sc(c, st, K_JOIN, 0.0, 0.0);
+    HIP_TRY(c, hipStreamWaitEvent(st, c->ev_join, 0));
+  }
   {
     Scope sc(c, st, K_APPLY, 2.0 * rows * (double)rp * rp, 4.0 * rows * rp * (ns + 4));
     float* Xout = wstep ? c->A2 : c->B2;

@@ -121,14 +121,134 @@ hipError_t launch_gram(const float* P, const SolveBatch& sb, int r, int rp, doub
 }
 
 // --------------------------------------------------------------------------------- apply --
-// step = U (-Gneg) = U G^-1 on fp64 MFMA (v_mfma_f64_16x16x4f64), then the momentum update.
-// A workgroup owns RW rows: their fp64 sums over the nsplit partial outputs are staged in LDS.
-// For RP >= 64 wave w owns the output column blocks w, w+4, ... over all RW/16 row blocks, so
-// each Gneg operand feeds RW/16 MFMAs; for RP < 64 wave w owns row block w and every column
-// block.  Gneg operands (L2-resident) are prefetched two k-steps ahead in registers.
-// srcA lane l = Ysum[16 rb + l%16][k + l/16], srcB lane l = Gneg[k + l/16][16 cb + l%16];
-// accumulator lane l, register v = X[16 rb + 4 v + l/16][16 cb + l%16] (the fp64 MFMA
-// interleaves accumulator rows, unlike the fp32 16x16x4 form).
+// U for rows r0 .. r0 + RW - 1: the fp64 sums of the nsplit partial outputs (and of Ysp when not
+// NULL), stored into the LDS tile ys (row stride LS) as T.  Each thread owns NE float4 groups,
+// taken EC (at most 8) at a time; the EC loads of one partial are issued before any is used, so
+// a thread waits for one round trip per partial and chunk rather than one per group.
+template <int RP, int RW, int LS, typename T>
+__device__ __forceinline__ void stage_u(T* ys, const float* __restrict__ Ypart, int64_t y_stride,
+                                        int nsplit, const float* __restrict__ Ysp, int64_t r0,
+                                        int64_t rows, int tid) {
+  constexpr int NE = RW * RP / 4 / 256;
+  constexpr int EC = NE <= 8 ? NE : (NE % 8 == 0 ? 8 : (NE % 7 == 0 ? 7 : (NE % 6 == 0 ? 6 : 5)));
+  static_assert(NE >= 1 && NE * 256 == RW * RP / 4 && NE % EC == 0, "staging shape");
+#pragma unroll
+  for (int e0 = 0; e0 < NE; e0 += EC) {
+    double s[EC][4];
+#pragma unroll
+    for (int e = 0; e < EC; ++e) s[e][0] = s[e][1] = s[e][2] = s[e][3] = 0.0;
+    // rows past the end read the last row (no branch around the load) and count zero
+    auto add = [&](const float* __restrict__ base) {
+      float4 v[EC];
+#pragma unroll
+      for (int e = 0; e < EC; ++e) {
+        const int f = tid + 256 * (e0 + e);
+        const int i = f / (RP / 4), c4 = f - i * (RP / 4);
+        const int64_t row = r0 + i;
+        const float4 t =
+            *reinterpret_cast<const float4*>(base + (row < rows ? row : rows - 1) * RP + 4 * c4);
+        const bool in = row < rows;
+        v[e] = make_float4(in ? t.x : 0.f, in ? t.y : 0.f, in ? t.z : 0.f, in ? t.w : 0.f);
+      }
+#pragma unroll
+      for (int e = 0; e < EC; ++e) {
+        s[e][0] += (double)v[e].x;
+        s[e][1] += (double)v[e].y;
+        s[e][2] += (double)v[e].z;
+        s[e][3] += (double)v[e].w;
+      }
+    };
+    for (int sp = 0; sp < nsplit; ++sp) add(Ypart + (int64_t)sp * y_stride);
+    if (Ysp) add(Ysp);
+#pragma unroll
+    for (int e = 0; e < EC; ++e) {
+      const int f = tid + 256 * (e0 + e);
+      const int i = f / (RP / 4), c4 = f - i * (RP / 4);
+      T* d = &ys[i * LS + 4 * c4];
+      d[0] = (T)s[e][0];
+      d[1] = (T)s[e][1];
+      d[2] = (T)s[e][2];
+      d[3] = (T)s[e][3];
+    }
+  }
+}
+
+// The momentum update of a wave's output elements: element (a, b, v) of lane (q, l16) is row
+// r0 + rowof(a) + 4 v + q, column colof(b) + l16, with step = -acc[a][b][v].  X and V are read
+// in groups of GU = 2 (a, b) blocks (8 elements per lane), rows past the end clamped to the last
+// one, each group's loads issued before the previous group is updated.
+template <int RP, int NRB, int NCB, typename RowOf, typename ColOf>
+struct MomentumUpdate {
+  static constexpr int NU = NRB * NCB;  // (a, b) blocks, u = b * NRB + a
+  static constexpr int GU = NU < 2 ? NU : 2;
+  static constexpr int NG = (NU + GU - 1) / GU;
+  const float* __restrict__ Xin;
+  const float* __restrict__ Vin;
+  int64_t r0, rows;
+  int q, l16;
+  RowOf rowof;
+  ColOf colof;
+  float xv[2][GU][4], vv[2][GU][4];
+
+  __device__ __forceinline__ void load(int grp, int buf) {
+#pragma unroll
+    for (int g = 0; g < GU; ++g) {
+      const int u0 = grp * GU + g;
+      const int u = u0 < NU ? u0 : NU - 1;  // a last group may be short
+      const int a = u % NRB, b = u / NRB;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        int64_t row = r0 + rowof(a) + 4 * v + q;
+        row = row < rows ? row : rows - 1;
+        const int64_t o = row * RP + colof(b) + l16;
+        xv[buf][g][v] = u0 < NU ? Xin[o] : 0.f;
+        vv[buf][g][v] = u0 < NU ? Vin[o] : 0.f;
+      }
+    }
+  }
+  // Writes Xout and Vout; returns true if a result was not finite.
+  __device__ __forceinline__ bool finish(const doublex4 (&acc)[NRB][NCB], float* __restrict__ Xout,
+                                         float* __restrict__ Vout, float eta, float gamma) {
+    bool bad = false;
+    load(0, 0);
+#pragma unroll
+    for (int grp = 0; grp < NG; ++grp) {
+      if (grp + 1 < NG) load(grp + 1, (grp + 1) & 1);
+      const int buf = grp & 1;
+#pragma unroll
+      for (int g = 0; g < GU; ++g) {
+        const int u0 = grp * GU + g;
+        if (u0 >= NU) continue;
+        const int u = u0 < NU ? u0 : NU - 1;
+        const int a = u % NRB, b = u / NRB;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int64_t row = r0 + rowof(a) + 4 * v + q;
+          if (row < rows) {
+            const int64_t o = row * RP + colof(b) + l16;
+            const double stepv = -acc[a][b][v];
+            const double vn = (double)gamma * (double)vv[buf][g][v] + (double)eta * stepv;
+            const float xf = (float)((double)xv[buf][g][v] + vn);
+            const float vf = (float)vn;
+            bad |= !isfinite(xf) || !isfinite(vf);
+            Xout[o] = xf;
+            Vout[o] = vf;
+          }
+        }
+      }
+    }
+    return bad;
+  }
+};
+
+template <int RP, int NRB, int NCB, typename RowOf, typename ColOf>
+__device__ __forceinline__ MomentumUpdate<RP, NRB, NCB, RowOf, ColOf> momentum_io(
+    const float* __restrict__ Xin, const float* __restrict__ Vin, int64_t r0, int64_t rows, int q,
+    int l16, RowOf rowof, ColOf colof) {
+  MomentumUpdate<RP, NRB, NCB, RowOf, ColOf> m{Xin, Vin, r0, rows, q, l16, rowof, colof, {}, {}};
+  return m;
+}
+
 template <int RP>
 struct ApplyCfg {
   static constexpr int RW = RP <= 64 ? 64 : (RP <= 128 ? 32 : 16);
@@ -158,36 +278,13 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Yp
   const int lane = tid & 63, wave = tid >> 6;
   const int q = lane >> 4, l16 = lane & 15;
   const int64_t r0 = (int64_t)blockIdx.x * RW;
-  for (int e = tid; e < RW * RP / 4; e += 256) {
-    const int i = e / (RP / 4), c4 = e - i * (RP / 4);
-    const int64_t row = r0 + i;
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-    if (row < rows) {
-      const float* src = Ypart + row * RP + 4 * c4;
-      for (int sp = 0; sp < nsplit; ++sp) {
-        const float4 v = *reinterpret_cast<const float4*>(src + (int64_t)sp * y_stride);
-        s0 += (double)v.x;
-        s1 += (double)v.y;
-        s2 += (double)v.z;
-        s3 += (double)v.w;
-      }
-      if (Ysp) {
-        const float4 w = *reinterpret_cast<const float4*>(Ysp + row * RP + 4 * c4);
-        s0 += (double)w.x;
-        s1 += (double)w.y;
-        s2 += (double)w.z;
-        s3 += (double)w.w;
-      }
-    }
-    double* d = &ys[i * LS + 4 * c4];
-    d[0] = s0;
-    d[1] = s1;
-    d[2] = s2;
-    d[3] = s3;
-  }
+  stage_u<RP, RW, LS, double>(ys, Ypart, y_stride, nsplit, Ysp, r0, rows, tid);
   __syncthreads();
   auto rblock = [&](int a) { return C::COLS ? a : wave; };
   auto cblock = [&](int b) { return C::COLS ? wave + 4 * b : b; };
+  auto io = momentum_io<RP, NRB, NCB>(Xin, Vin, r0, rows, q, l16,
+                                      [=](int a) { return 16 * rblock(a); },
+                                      [=](int b) { return 16 * cblock(b); });
   doublex4 acc[NRB][NCB];
 #pragma unroll
   for (int a = 0; a < NRB; ++a)
@@ -220,26 +317,7 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ Yp
       }
     }
   }
-  bool bad = false;
-#pragma unroll
-  for (int a = 0; a < NRB; ++a)
-#pragma unroll
-    for (int b = 0; b < NCB; ++b)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int64_t row = r0 + 16 * rblock(a) + 4 * v + q;
-        if (row < rows) {
-          const int64_t o = row * RP + 16 * cblock(b) + l16;
-          const double stepv = -acc[a][b][v];
-          const double xa = (double)Xin[o];
-          const double vn = (double)gamma * (double)Vin[o] + (double)eta * stepv;
-          const float xf = (float)(xa + vn);
-          const float vf = (float)vn;
-          bad |= !isfinite(xf) || !isfinite(vf);
-          Xout[o] = xf;
-          Vout[o] = vf;
-        }
-      }
+  const bool bad = io.finish(acc, Xout, Vout, eta, gamma);
   if (bad) flag_status(status, STATUS_NONFINITE, step_id);
 }
 
@@ -280,39 +358,15 @@ __global__ __launch_bounds__(256, 2) void apply_wide_kernel(const float* __restr
   const int lane = tid & 63, wave = tid >> 6;
   const int q = lane >> 4, l16 = lane & 15;
   const int64_t r0 = (int64_t)blockIdx.x * RW;
-  for (int e = tid; e < RW * RP / 4; e += 256) {
-    const int i = e / (RP / 4), c4 = e - i * (RP / 4);
-    const int64_t row = r0 + i;
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-    if (row < rows) {
-      const float* src = Ypart + row * RP + 4 * c4;
-      for (int sp = 0; sp < nsplit; ++sp) {
-        const float4 v = *reinterpret_cast<const float4*>(src + (int64_t)sp * y_stride);
-        s0 += (double)v.x;
-        s1 += (double)v.y;
-        s2 += (double)v.z;
-        s3 += (double)v.w;
-      }
-      if (Ysp) {
-        const float4 w = *reinterpret_cast<const float4*>(Ysp + row * RP + 4 * c4);
-        s0 += (double)w.x;
-        s1 += (double)w.y;
-        s2 += (double)w.z;
-        s3 += (double)w.w;
-      }
-    }
-    float* d = &ys[i * LS + 4 * c4];
-    d[0] = (float)s0;
-    d[1] = (float)s1;
-    d[2] = (float)s2;
-    d[3] = (float)s3;
-  }
+  stage_u<RP, RW, LS, float>(ys, Ypart, y_stride, nsplit, Ysp, r0, rows, tid);
   __syncthreads();
   doublex4 acc[NRB][NCB];
 #pragma unroll
   for (int a = 0; a < NRB; ++a)
 #pragma unroll
     for (int b = 0; b < NCB; ++b) acc[a][b] = doublex4{0.0, 0.0, 0.0, 0.0};
+  auto io = momentum_io<RP, NRB, NCB>(Xin, Vin, r0, rows, q, l16, [](int a) { return 16 * a; },
+                                      [=](int b) { return 16 * (wave + 4 * b); });
   const double* gcol = Gneg + 16 * wave + l16;  // column block b of this wave: + 64 b
   double pre[PD][NCB];
 #pragma unroll
@@ -340,26 +394,7 @@ __global__ __launch_bounds__(256, 2) void apply_wide_kernel(const float* __restr
       }
     }
   }
-  bool bad = false;
-#pragma unroll
-  for (int a = 0; a < NRB; ++a)
-#pragma unroll
-    for (int b = 0; b < NCB; ++b)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int64_t row = r0 + 16 * a + 4 * v + q;
-        if (row < rows) {
-          const int64_t o = row * RP + 16 * (wave + 4 * b) + l16;
-          const double stepv = -acc[a][b][v];
-          const double xa = (double)Xin[o];
-          const double vn = (double)gamma * (double)Vin[o] + (double)eta * stepv;
-          const float xf = (float)(xa + vn);
-          const float vf = (float)vn;
-          bad |= !isfinite(xf) || !isfinite(vf);
-          Xout[o] = xf;
-          Vout[o] = vf;
-        }
-      }
+  const bool bad = io.finish(acc, Xout, Vout, eta, gamma);
   if (bad) flag_status(status, STATUS_NONFINITE, step_id);
 }
 

@@ -175,6 +175,18 @@ def test_dense_blocks_before_device_use(L):
     ctx.close()
 
 
+def test_kernel_timing_classes_before_device_use(L):
+    """Five timing classes (dense, sparse, Gram and inverse, update, wait for the side stream)
+    read zero before any work; a sixth is rejected."""
+    ctx = nmd.Context(40, 30, 4, 16, 16)
+    for k in range(5):
+        assert ctx.kernel_timing(k) == {"ms": 0.0, "launches": 0, "flops": 0.0, "bytes": 0.0}
+    ms = C.c_double()
+    assert L.nmd_get_kernel_timing(ctx._p, 5, C.byref(ms), None, None, None, 0) == nmd.EINVAL
+    assert L.nmd_get_kernel_timing(ctx._p, -1, C.byref(ms), None, None, None, 0) == nmd.EINVAL
+    ctx.close()
+
+
 def test_schedule_matches_golden_and_oracle(L):
     with open(os.path.join(HERE, "golden", "schedules.json")) as f:
         cases = json.load(f)

@@ -625,6 +625,70 @@ def test_rejected_step_keeps_last_completed_step():
     assert np.array_equal(H2.cpu().numpy(), H3.cpu().numpy())
 
 
+@pytest.mark.parametrize("codes,bad,first_fail", [
+    ((1, 2, 3), (3,), 2),       # the last step of a run of three W-steps
+    ((1, 3, 2, 4), (3,), 1),    # a step inside a run: the one before it is kept
+    ((3, 1, 4), (3, 4), 0),     # two singular steps in one run: the first is reported
+    ((-1, -3, -2), (-3,), 1),   # the same on the H side (a zero row block of W)
+])
+def test_singular_gram_inside_a_run_of_steps(codes, bad, first_fail):
+    """Consecutive steps of one side have their Gram matrices and solves formed together,
+    ahead of their updates.  A step whose Gram matrix is singular stops itself and every later
+    step, but the steps before it in the same run are kept: W and H come back exactly as after
+    those steps alone."""
+    p = gen.config(1)
+    _say("singular Gram inside a run", codes, bad)
+    bn, bm = partition.bounds(p.n, p.block_n), partition.bounds(p.m, p.block_m)
+    W0, H0 = p.W0.copy(), p.H0.copy()
+    for k in bad:
+        if k > 0:
+            H0[:, bn[k - 1]:bn[k]] = 0.0  # W-steps on column block k see a zero panel
+        else:
+            W0[bm[-k - 1]:bm[-k], :] = 0.0  # H-steps on row block -k see a zero panel
+    kw = dict(mode="stochastic", eta=1.0, mom=0.9)
+    ref = make_ctx(p, **kw)
+    Wr, Hr = dev(W0), dev(H0)
+    if first_fail:
+        ref.run_steps(Wr, Hr, list(codes[:first_fail]))
+    ctx = make_ctx(p, **kw)
+    W, H = dev(W0), dev(H0)
+    with pytest.raises(nmd.NmdError) as e:
+        ctx.run_steps(W, H, list(codes))
+    assert e.value.code == -4 and f"step {first_fail};" in e.value.message
+    assert np.array_equal(W.cpu().numpy(), Wr.cpu().numpy())
+    assert np.array_equal(H.cpu().numpy(), Hr.cpu().numpy())
+
+
+def _solve_batches(codes, batch=8):
+    """Runs of consecutive same-side steps, cut into pieces of at most `batch` steps."""
+    n, i = 0, 0
+    while i < len(codes):
+        j = i
+        while j < len(codes) and j - i < batch and (codes[j] > 0) == (codes[i] > 0):
+            j += 1
+        n, i = n + 1, j
+    return n
+
+
+def test_kernel_timing_counts_steps_and_runs():
+    """With timing on, one sweep records a dense, sparse, update and join entry per step and one
+    Gram-and-inverse entry per run of consecutive same-side steps (at most eight)."""
+    p = gen.config(1)
+    p.block_m, p.block_n = 64, 500  # 16 row blocks, 2 column blocks: runs of H-steps
+    _say("kernel timing classes, 1000 x 1000 with 16 x 2 blocks")
+    ctx = make_ctx(p, mode="stochastic", flags=nmd.FLAG_TIMING)
+    W, H = dev(p.W0), dev(p.H0)
+    ctx.sweep(W, H, 1)
+    codes = list(ctx.schedule(0))
+    assert len(codes) == 18
+    t = [ctx.kernel_timing(k) for k in range(5)]
+    for k in (0, 3, 4):
+        assert t[k]["launches"] == len(codes), (k, t[k])
+    assert t[1]["launches"] >= len(codes)  # one per block's share of the nonzeros
+    assert t[2]["launches"] == _solve_batches(codes) < len(codes), (t[2], codes)
+    assert t[0]["ms"] > 0 and t[2]["ms"] > 0 and t[4]["ms"] >= 0
+
+
 def gen_first_w_block(p):
     R, C = partition.num_blocks(p.m, p.block_m), partition.num_blocks(p.n, p.block_n)
     code = schedule.sweep_schedule(p.seed, 0, R, C, True)[0]
