@@ -13,8 +13,11 @@
 //   3. -G^-1 = -M^T M by 64 x 64 tiles: tile (a, b) = -sum_{l >= max(a, b)} M_la^T M_lb.
 //
 // The launches take a batch of matrices (blockIdx.y), each with its own work area and step id.
-// A pivot that is not positive (or not finite) flags that step as not positive definite; its
-// apply and the later ones then write nothing.  Blocks of NB x NB doubles are staged in LDS with row stride
+// A second form (chol_fused_kernel) runs all three steps for a matrix in one workgroup, the
+// diagonal block factored once per block column: one launch per batch, slower on an idle GPU
+// but with far fewer launches to queue behind the contraction's workgroups.  A pivot that is
+// not positive (or not finite) flags that step as not positive definite; its apply and the
+// later ones then write nothing.  Blocks of NB x NB doubles are staged in LDS with row stride
 // NB + 1; fp64 MFMA v_mfma_f64_16x16x4f64: srcA lane l = A[l % 16][l / 16], srcB lane
 // l = B[l / 16][l % 16], accumulator register v of lane l = D[4 v + l / 16][l % 16].
 
@@ -242,19 +245,16 @@ __global__ __launch_bounds__(kThreads) void chol_col_kernel(const double* __rest
   }
 }
 
-// Step 2: block column j = blockIdx.x of M = L^-1 (rows i >= j) of matrix blockIdx.y.
+// Step 2 for block column j of M = L^-1 (rows i >= j): M_jj = D_j and, for i > j,
+// M_ij = -D_i sum_{l=j}^{i-1} L_il M_lj.  Four NB x NB LDS blocks; ends with the LDS free once
+// the caller synchronises.
 template <int NB>
-__global__ __launch_bounds__(kThreads) void chol_trinv_kernel(double* __restrict__ work,
-                                                              int64_t per, int rp) {
+__device__ void trinv_column(const double* __restrict__ L, const double* __restrict__ D,
+                             double* __restrict__ Mb, int rp, int j, double* sL, double* sM,
+                             double* sT, double* sD) {
   constexpr int LS = NB + 1;
   constexpr int NT = NB / 16;
-  __shared__ double sL[NB * LS], sM[NB * LS], sT[NB * LS], sD[NB * LS];
-  const Work wk(work, per, blockIdx.y, rp);
-  const double* __restrict__ L = wk.L;
-  const double* __restrict__ D = wk.D;
-  double* __restrict__ Mb = wk.M;
   const int nb = rp / NB;
-  const int j = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int q = lane >> 4, l16 = lane & 15;
   const bool mw = wave < NT * NT;
@@ -289,26 +289,23 @@ __global__ __launch_bounds__(kThreads) void chol_trinv_kernel(double* __restrict
   }
 }
 
-// Step 3: tile (a, b), a <= b, of -G^-1 = -M^T M of matrix blockIdx.y, written to both (a, b)
-// and (b, a).
+// Step 2: block column j = blockIdx.x of matrix blockIdx.y.
 template <int NB>
-__global__ __launch_bounds__(kThreads) void chol_gram_kernel(double* __restrict__ work,
-                                                             int64_t per, int rp,
-                                                             const int* status, SolveBatch sb) {
+__global__ __launch_bounds__(kThreads) void chol_trinv_kernel(double* __restrict__ work,
+                                                              int64_t per, int rp) {
   constexpr int LS = NB + 1;
-  constexpr int NT = NB / 16;
-  __shared__ double s1[NB * LS], s2[NB * LS];
+  __shared__ double sL[NB * LS], sM[NB * LS], sT[NB * LS], sD[NB * LS];
   const Work wk(work, per, blockIdx.y, rp);
-  const double* __restrict__ Mb = wk.M;
-  double* __restrict__ Gneg = wk.Gneg;
+  trinv_column<NB>(wk.L, wk.D, wk.M, rp, blockIdx.x, sL, sM, sT, sD);
+}
+
+// Step 3 for tile (a, b), a <= b, of -G^-1 = -M^T M: -sum_{l >= b} M_la^T M_lb, written to
+// both (a, b) and (b, a).  Two NB x NB LDS blocks.
+template <int NB>
+__device__ void gram_tile(const double* __restrict__ Mb, double* __restrict__ Gneg, int rp, int a,
+                          int b, double* s1, double* s2) {
+  constexpr int NT = NB / 16;
   const int nb = rp / NB;
-  int p = blockIdx.x, a = 0;  // pair index -> (a <= b)
-  while (p >= nb - a) {
-    p -= nb - a;
-    ++a;
-  }
-  const int b = a + p;
-  if (step_blocked(status, sb.step_id[blockIdx.y])) return;  // its apply writes nothing
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int q = lane >> 4, l16 = lane & 15;
   const bool mw = wave < NT * NT;
@@ -328,6 +325,119 @@ __global__ __launch_bounds__(kThreads) void chol_gram_kernel(double* __restrict_
       Gneg[(int64_t)(a * NB + r) * rp + b * NB + c] = -acc[v];
       if (a != b) Gneg[(int64_t)(b * NB + c) * rp + a * NB + r] = -acc[v];
     }
+  }
+}
+
+// Pair index p -> tile (a, b) with a <= b, in the order (0,0), (0,1), ..., (1,1), ...
+__device__ __forceinline__ void tile_pair(int p, int nb, int& a, int& b) {
+  a = 0;
+  while (p >= nb - a) {
+    p -= nb - a;
+    ++a;
+  }
+  b = a + p;
+}
+
+// Step 3: tile pair blockIdx.x of matrix blockIdx.y.
+template <int NB>
+__global__ __launch_bounds__(kThreads) void chol_gram_kernel(double* __restrict__ work,
+                                                             int64_t per, int rp,
+                                                             const int* status, SolveBatch sb) {
+  constexpr int LS = NB + 1;
+  __shared__ double s1[NB * LS], s2[NB * LS];
+  const Work wk(work, per, blockIdx.y, rp);
+  int a, b;
+  tile_pair(blockIdx.x, rp / NB, a, b);
+  if (step_blocked(status, sb.step_id[blockIdx.y])) return;  // its apply writes nothing
+  gram_tile<NB>(wk.M, wk.Gneg, rp, a, b, s1, s2);
+}
+
+// Steps 1-3 for matrix blockIdx.x by a single workgroup: L by block columns (the diagonal
+// block factored once per column, then the blocks below it), M = L^-1 by block columns, then
+// the tiles of -M^T M.  One launch per batch instead of one per block column and two more; a
+// batch's matrices run on separate CUs.
+template <int NB>
+__global__ __launch_bounds__(kThreads) void chol_fused_kernel(const double* __restrict__ Gall,
+                                                              double* __restrict__ work,
+                                                              int64_t per, int rp, int* status,
+                                                              SolveBatch sb) {
+  constexpr int LS = NB + 1;
+  constexpr int NT = NB / 16;
+  __shared__ double s0[NB * LS], s1[NB * LS], s2[NB * LS], s3[NB * LS];
+  const Work wk(work, per, blockIdx.x, rp);
+  const double* __restrict__ G = Gall + (int64_t)blockIdx.x * rp * rp;
+  double* __restrict__ L = wk.L;
+  double* __restrict__ D = wk.D;
+  const int nb = rp / NB;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int q = lane >> 4, l16 = lane & 15;
+  const bool mw = wave < NT * NT;
+  const int ri = wave / NT, ci = wave % NT;
+  bool all_ok = true;
+  for (int k = 0; k < nb; ++k) {
+    // L_kk and D_k = L_kk^-1 from A_kk - sum_{l<k} L_kl L_kl^T
+    dx4 akk = {0.0, 0.0, 0.0, 0.0};
+    for (int l = 0; l < k; ++l) {
+      __syncthreads();
+      stage<NB>(s1, L, rp, k, l);
+      __syncthreads();
+      if (mw) mma_abt<NB>(akk, s1, s1, ri, ci, q, l16);
+    }
+    __syncthreads();
+    stage<NB>(s0, G, rp, k, k);
+    __syncthreads();
+    if (mw) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) s0[(16 * ri + 4 * v + q) * LS + 16 * ci + l16] -= akk[v];
+    }
+    const bool ok = factor_block<NB>(s0, s3);  // s0 = L_kk, s3 = D_k (kept for the column)
+    all_ok = all_ok && ok;
+    for (int e = threadIdx.x; e < NB * NB; e += kThreads) {
+      const int r = e / NB, c = e - r * NB;
+      L[(int64_t)(k * NB + r) * rp + k * NB + c] = s0[r * LS + c];
+      D[(int64_t)k * NB * NB + e] = s3[r * LS + c];
+    }
+    // L_ik = (A_ik - sum_{l<k} L_il L_kl^T) D_k^T for the blocks below
+    for (int i = k + 1; i < nb; ++i) {
+      dx4 aik = {0.0, 0.0, 0.0, 0.0};
+      for (int l = 0; l < k; ++l) {
+        __syncthreads();
+        stage<NB>(s1, L, rp, k, l);
+        stage<NB>(s2, L, rp, i, l);
+        __syncthreads();
+        if (mw) mma_abt<NB>(aik, s2, s1, ri, ci, q, l16);
+      }
+      __syncthreads();
+      stage<NB>(s2, G, rp, i, k);
+      __syncthreads();
+      if (mw) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) s2[(16 * ri + 4 * v + q) * LS + 16 * ci + l16] -= aik[v];
+      }
+      __syncthreads();
+      dx4 o = {0.0, 0.0, 0.0, 0.0};
+      if (mw) mma_abt<NB>(o, s2, s3, ri, ci, q, l16);
+      if (mw) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          L[(int64_t)(i * NB + 16 * ri + 4 * v + q) * rp + k * NB + 16 * ci + l16] = o[v];
+      }
+    }
+    __syncthreads();  // L of this block column is visible to every wave
+  }
+  if (!all_ok) {
+    if (threadIdx.x == 0) flag_status(status, STATUS_NOTPD, sb.step_id[blockIdx.x]);
+    return;  // uniform: every thread saw the same pivots
+  }
+  for (int j = 0; j < nb; ++j) {
+    trinv_column<NB>(L, D, wk.M, rp, j, s0, s1, s2, s3);
+    __syncthreads();
+  }
+  for (int p = 0; p < nb * (nb + 1) / 2; ++p) {
+    int a, b;
+    tile_pair(p, nb, a, b);
+    gram_tile<NB>(wk.M, wk.Gneg, rp, a, b, s0, s1);
+    __syncthreads();
   }
 }
 
@@ -367,6 +477,23 @@ hipError_t launch_chol_inverse(const double* G, double* work, int rp, int* statu
     default: return hipErrorInvalidValue;
   }
 #undef CHOL_NB
+  for (int b = 0; b < sb.n; ++b) result[b] = Work(work, per, b, rp).Gneg;
+  return hipGetLastError();
+}
+
+hipError_t launch_chol_inverse_fused(const double* G, double* work, int rp, int* status,
+                                     const SolveBatch& sb, double** result, hipStream_t st) {
+  if (sb.n < 1 || sb.n > kSolveBatch) return hipErrorInvalidValue;
+  const int NB = rp < 64 ? rp : 64;
+  const int64_t per = chol_work_doubles(rp);
+  const dim3 grid((unsigned)sb.n);
+  switch (NB) {
+    case 16: hipLaunchKernelGGL((chol_fused_kernel<16>), grid, dim3(kThreads), 0, st, G, work, per, rp, status, sb); break;
+    case 32: hipLaunchKernelGGL((chol_fused_kernel<32>), grid, dim3(kThreads), 0, st, G, work, per, rp, status, sb); break;
+    case 48: hipLaunchKernelGGL((chol_fused_kernel<48>), grid, dim3(kThreads), 0, st, G, work, per, rp, status, sb); break;
+    case 64: hipLaunchKernelGGL((chol_fused_kernel<64>), grid, dim3(kThreads), 0, st, G, work, per, rp, status, sb); break;
+    default: return hipErrorInvalidValue;
+  }
   for (int b = 0; b < sb.n; ++b) result[b] = Work(work, per, b, rp).Gneg;
   return hipGetLastError();
 }

@@ -448,7 +448,13 @@ int factor_run(nmd_ctx* c, bool wstep, const int32_t* blocks, int n, int first_s
   {
     Scope sc(c, c->side, K_FACTOR, flops, 0.0);
     HIP_TRY(c, nmd::launch_gram(P, sb, c->r, c->rp, c->Gpart, nchunks, c->G, c->side));
-    HIP_TRY(c, nmd::launch_chol_inverse(c->G, c->Gwork, c->rp, c->status, sb, c->Gneg, c->side));
+    // one workgroup per matrix (one launch) at the large and the small ranks; one launch per
+    // 64-wide block column, then two, in between, where that is faster on its own
+    if (c->rp >= 320 || c->rp <= 64)
+      HIP_TRY(c, nmd::launch_chol_inverse_fused(c->G, c->Gwork, c->rp, c->status, sb, c->Gneg,
+                                                c->side));
+    else
+      HIP_TRY(c, nmd::launch_chol_inverse(c->G, c->Gwork, c->rp, c->status, sb, c->Gneg, c->side));
   }
   HIP_TRY(c, hipEventRecord(c->ev_join, c->side));
   return NMD_OK;

@@ -96,6 +96,9 @@ hipError_t launch_gram(const float* P, const SolveBatch& sb, int r, int rp, doub
 int64_t chol_work_doubles(int rp);
 hipError_t launch_chol_inverse(const double* G, double* work, int rp, int* status,
                                const SolveBatch& sb, double** result, hipStream_t st);
+// The same with one workgroup per matrix doing all three steps in one launch.
+hipError_t launch_chol_inverse_fused(const double* G, double* work, int rp, int* status,
+                                     const SolveBatch& sb, double** result, hipStream_t st);
 // Vout = gamma Vin + eta U (-Gneg), Xout = Xin + Vout, where U = Delta P_J is the sum (fp64)
 // of the nsplit partial outputs plus, when Ysp is not NULL, a separate correction buffer
 // (rows x rp), and -Gneg = (P_J^T P_J)^-1.  The outputs are other buffers than the inputs, so
