@@ -135,7 +135,8 @@ int nmd_set_sparse_csr(nmd_ctx* ctx, int64_t nnz, const int64_t* row_ptr, const 
  * B <- B + Delta^T A (A^T A)^-1 over all rows (eqs. spLsqA, spLsqB), with eta and gamma
  * applied as in the stochastic update.  The sweep counter t and the momentum buffers persist
  * across calls (nmd_reset clears them).  Returns NMD_ESTATE without S, NMD_EINVAL on NULL
- * pointers or n_sweeps < 1, NMD_ENOTPD / NMD_ENONFINITE when the device rejects a step: the
+ * pointers, n_sweeps < 1 or more than 2^27 steps in the call (n_sweeps times the blocks of both
+ * sides), NMD_ENOTPD / NMD_ENONFINITE when the device rejects a step: the
  * later steps are skipped, W and H receive the factors after the last completed step (the
  * momenta are kept at that state too) and nmd_last_error names the sweep and step; the sweep
  * counter then counts only the sweeps that completed.  With NMD_FLAG_GUARD, NMD_ESTEP when the

@@ -36,6 +36,8 @@ constexpr int64_t kSplitRows = 8192;  // at most this many panel rows per fp32 a
 constexpr int64_t kTargetWgs = 2048;  // dense workgroups wanted per launch (256 CUs)
 constexpr int64_t kWgFixedRows = 32;  // per-workgroup set-up and write-back, in panel rows
 constexpr int kObjSubMax = 16;        // sub-splits of a column block in the objective
+// Steps one call may enqueue: the device status word keeps step_id * 8 + flag in an int.
+constexpr int64_t kMaxStepsPerCall = int64_t{1} << 27;
 
 enum { K_DENSE = 0, K_SPARSE = 1, K_FACTOR = 2, K_APPLY = 3, K_JOIN = 4, K_COUNT = 5 };
 
@@ -906,6 +908,9 @@ int nmd_als_block_sweep(nmd_ctx* c, float* W, float* H, int32_t n_sweeps, void* 
   hipStream_t st = (hipStream_t)hip_stream;
   const bool sto = c->opt.mode == NMD_STOCHASTIC;
   const int32_t steps_per = c->hs.nblk() + c->ws.nblk();
+  if ((int64_t)n_sweeps * steps_per > kMaxStepsPerCall)
+    return fail(c, NMD_EINVAL, "%d sweeps of %d steps exceed %lld steps per call; split the call",
+                n_sweeps, steps_per, (long long)kMaxStepsPerCall);
   const bool guard = (c->opt.flags & NMD_FLAG_GUARD) != 0;
   if (!guard && !(c->opt.flags & NMD_FLAG_SWEEP_OBJECTIVE)) {
     std::vector<std::vector<int32_t>> lists;
@@ -927,6 +932,9 @@ int nmd_run_steps(nmd_ctx* c, float* W, float* H, const int32_t* steps, int32_t 
   int rc = check_ready(c, W, H);
   if (rc) return rc;
   if (n_steps < 0 || (n_steps > 0 && !steps)) return fail(c, NMD_EINVAL, "bad step list");
+  if (n_steps > kMaxStepsPerCall)
+    return fail(c, NMD_EINVAL, "%d steps exceed %lld steps per call; split the call", n_steps,
+                (long long)kMaxStepsPerCall);
   for (int32_t k = 0; k < n_steps; ++k) {
     const int32_t code = steps[k];
     if (code == 0 || (code > 0 && code > c->ws.nblk()) || (code < 0 && -code > c->hs.nblk()))

@@ -133,6 +133,12 @@ def test_no_positive_entry_and_state_errors(L):
     assert L.nmd_metrics(ctx._p, fake, fake, None, None) == nmd.EINVAL
     assert L.nmd_metrics(ctx._p, None, fake, out3, None) == nmd.EINVAL
     assert L.nmd_als_block_sweep(ctx._p, fake, fake, 0, None) == nmd.EINVAL
+    # a call enqueues at most 2^27 steps (the device status word holds step id * 8 + flag);
+    # 2 x 2 blocks make 4 steps per sweep.  Rejected before the device or the list is touched.
+    assert L.nmd_als_block_sweep(ctx._p, fake, fake, (1 << 25) + 1, None) == nmd.EINVAL
+    assert "split the call" in nmd.lib().nmd_last_error(ctx._p).decode()
+    one = (C.c_int32 * 1)(1)
+    assert L.nmd_run_steps(ctx._p, fake, fake, one, (1 << 27) + 1, None) == nmd.EINVAL
     steps = (C.c_int32 * 1)(3)
     assert L.nmd_run_steps(ctx._p, fake, fake, steps, 1, None) == nmd.EINVAL
     steps = (C.c_int32 * 1)(0)
