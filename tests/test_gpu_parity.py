@@ -8,6 +8,7 @@ Bars:
 Every test prints the case it runs before touching the GPU.
 """
 
+import itertools
 import math
 
 import numpy as np
@@ -414,6 +415,32 @@ def test_stochastic_planted_reduced(eta, mom):
     assert rel(Wg, Wo) < TOL and rel(Hg, Ho) < TOL
     R, C = partition.num_blocks(p.m, 512), partition.num_blocks(p.n, 512)
     assert ctx.schedule(0) == schedule.sweep_schedule(p.seed, 0, R, C, True)
+
+
+@pytest.mark.parametrize("case", ["r64_fused", "r128_multi", "r320_fused"])
+def test_long_runs_of_same_side_steps(case):
+    """Uneven block grids, so that the schedule has runs of more than eight H-steps (21 or 20
+    row blocks against 2 or 1 column blocks): their solves are formed in batches of up to
+    eight, by the single-workgroup form at r_p = 64 and 320 and the multi-launch form at 128.
+    One sweep, momentum 0.9, against the oracle."""
+    if case == "r320_fused":
+        p = gen.config(4, scale=0.1)  # 13926 x 13926 graph-like counts
+        r, p.block_m, p.block_n = 320, 700, p.n
+    else:
+        p = gen.config(3, scale=0.125)  # 4096 x 4096 planted
+        r, p.block_m, p.block_n = (64 if case == "r64_fused" else 128), 200, 2048
+    if r != p.r:
+        p.r = r
+        p.W0, p.H0 = gen.sign_constrained_init(p.m, p.n, r, float(p.val.mean()), 1003)
+    R, C = partition.num_blocks(p.m, p.block_m), partition.num_blocks(p.n, p.block_n)
+    codes = schedule.sweep_schedule(p.seed, 0, R, C, True)
+    assert max(sum(1 for _ in g) for _, g in itertools.groupby(codes, key=lambda c: c > 0)) > 8
+    _say("long runs of same-side steps", case, p.m, p.n, r, R, C)
+    Wg, Hg, _ = gpu_run(p, 1, mode="stochastic", eta=1.0, mom=0.9)
+    Wo, Ho, _ = oracle_run(p, 1, mode="stochastic", eta=1.0, mom=0.9)
+    ew, eh = rel(Wg, Wo), rel(Hg, Ho)
+    print(f"{case}: rel err W {ew:.2e} H {eh:.2e}")
+    assert ew < TOL and eh < TOL
 
 
 def test_stochastic_planted_reduced_split_bf16():
