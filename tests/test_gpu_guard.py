@@ -182,6 +182,25 @@ def test_sweep_counter_counts_completed_sweeps_after_a_rejected_step():
     assert ctx.sweep_count == 1
 
 
+def test_deterministic_rejection_keeps_factors_and_counter():
+    """Deterministic mode (the exact half-steps): after one sweep, a zero H makes the next W
+    half-step's Gram matrix singular.  The call fails with NMD_ENOTPD at sweep 1, step 0; W and H
+    come back as they were passed, and the counter reads 1."""
+    p = gen.config(1)  # deterministic
+    _say("deterministic rejection")
+    ctx = nmd.Context(p.m, p.n, p.r, p.block_m, p.block_n, seed=p.seed, mode="deterministic")
+    ctx.set_sparse_csr(p.row_ptr, p.col, p.val)
+    W, H = dev(p.W0), dev(p.H0)
+    ctx.sweep(W, H, 1)
+    W1 = W.clone()
+    H.zero_()
+    with pytest.raises(nmd.NmdError) as e:
+        ctx.sweep(W, H, 2)
+    assert e.value.code == nmd.ENOTPD and "sweep 1, step 0" in e.value.message
+    assert ctx.sweep_count == 1
+    assert torch.equal(W, W1) and not torch.any(H != 0).item()
+
+
 def test_guard_in_deterministic_mode():
     """The safeguard with the deterministic half-steps (eqs. spLsqA, spLsqB) at an over-long step
     (eta = 1.7, momentum 0.9): sweeps 1 and 5 raise the objective in the oracle and are undone;
