@@ -437,6 +437,8 @@ def test_long_runs_of_same_side_steps(case):
     assert max(sum(1 for _ in g) for _, g in itertools.groupby(codes, key=lambda c: c > 0)) > 8
     _say("long runs of same-side steps", case, p.m, p.n, r, R, C)
     Wg, Hg, _ = gpu_run(p, 1, mode="stochastic", eta=1.0, mom=0.9)
+    Wg2, Hg2, _ = gpu_run(p, 1, mode="stochastic", eta=1.0, mom=0.9)
+    assert np.array_equal(Wg, Wg2) and np.array_equal(Hg, Hg2)  # batched solves deterministic
     Wo, Ho, _ = oracle_run(p, 1, mode="stochastic", eta=1.0, mom=0.9)
     ew, eh = rel(Wg, Wo), rel(Hg, Ho)
     print(f"{case}: rel err W {ew:.2e} H {eh:.2e}")
