@@ -8,10 +8,10 @@
 // This kernel forms the dense term -S-hat P_J (sgn = -1); the sparse correction adds the first
 // term.  S-hat is mostly zero (the factors start with opposite signs and the fit keeps it sparse,
 // Sec. 4.3), so a wave skips the MFMAs of every 16 x 4 operand slice of S-hat that holds no
-// positive entry, and (at r_p = 256) packs the entries of slices with only a few of them four
-// to a slice (gathered slices, below).  The L tile is produced by MFMA, rectified in registers
-// and consumed by MFMA; neither L nor S-hat reaches memory (the IO-aware fusion of Sec. 4.2,
-// with the raw panel P instead of a pseudo-inverse).
+// positive entry, and (at r_p = 256) runs the second product per 4-row quad-column of S-hat on
+// 4 x 4 x 1 MFMAs, only where one holds a positive entry (below).  The L tile is produced by
+// MFMA, rectified in registers and consumed by MFMA; neither L nor S-hat reaches memory (the
+// IO-aware fusion of Sec. 4.2, with the raw panel P instead of a pseudo-inverse).
 //
 // Data flow (one workgroup = WAVES waves: 8 at r_p = 128 and 256, two per SIMD; 4 elsewhere):
 //   * X: rows x RP row-major (RP = padded rank, zero columns beyond r).  Each wave keeps
@@ -22,9 +22,9 @@
 //   * GEMM1 builds the transposed tile L^T (16 j x 16 i); the accumulator of lane l, register
 //     v holds L[i = l%16][j = 4(l/16) + v], which is exactly the srcA layout of GEMM2 for the
 //     k-slice {4(l/16) + v}: the rectified tile feeds GEMM2 with no data movement.
-//   * GEMM2: Y[i][c] += sum_j max(0, L[i][j]) P[j][c], srcB read from LDS as single floats,
-//     per 16 x 4 slice of max(0, L): skipped when zero, packed into gathered slices when it
-//     holds only a few positive entries (r_p = 256), run whole otherwise.
+//   * GEMM2: Y[i][c] += sum_j max(0, L[i][j]) P[j][c], srcB read from LDS, per 16 x 4 slice
+//     of max(0, L) on 16 x 16 x 4 MFMAs, skipped when zero; at r_p = 256 per quad-column
+//     (4 rows x 1 column) on 4 x 4 x 1 MFMAs with the A operand broadcast from the L tile.
 //   * Split-J: the workgroups of one row tile may be spread over `nsplit` disjoint ranges of P
 //     rows, each writing its own partial Y; the solve kernel sums them in fp64.
 
@@ -43,9 +43,8 @@ typedef __attribute__((address_space(1))) void glb_void;
 // product whose operands are read during the first (4: all of them, where registers allow);
 // DIRECT: direct global->LDS loads into double-buffered tiles (for long rows; register staging
 // there pushes the VGPR budget into spills) instead of register staging through one tile (a
-// direct load moves 64 chunks of one row, so short rows would leave most lanes idle); SPARSE:
-// when nonzero, slices of the second product with at most that many positive entries go
-// through the gathered path below and no operand ring is kept (RING unused).
+// direct load moves 64 chunks of one row, so short rows would leave most lanes idle); QUAD:
+// the second product runs per quad-column (below) and no operand ring is kept (RING unused).
 template <int RP>
 struct DenseLaunch {
   static constexpr int MI = DenseCfg<RP>::MI;
@@ -53,7 +52,7 @@ struct DenseLaunch {
   static constexpr bool DIRECT = RP >= 320;
   static constexpr int NT = DIRECT ? DenseCfg<RP>::NTD : DenseCfg<RP>::NT;
   static constexpr int RING = RP >= 320 ? 4 : 2;
-  static constexpr int SPARSE = 0;
+  static constexpr bool QUAD = false;
 };
 template <>
 struct DenseLaunch<256> {
@@ -62,7 +61,7 @@ struct DenseLaunch<256> {
   static constexpr bool DIRECT = true;
   static constexpr int NT = 64;
   static constexpr int RING = 4;
-  static constexpr int SPARSE = 3;
+  static constexpr bool QUAD = true;
 };
 template <>
 struct DenseLaunch<128> {
@@ -71,7 +70,7 @@ struct DenseLaunch<128> {
   static constexpr bool DIRECT = true;
   static constexpr int NT = 128;
   static constexpr int RING = 4;
-  static constexpr int SPARSE = 0;
+  static constexpr bool QUAD = false;
 };
 
 template <int RP>
@@ -113,67 +112,89 @@ __device__ __forceinline__ void issue_tile(float* dst, const float* __restrict__
   }
 }
 
-// Both products over the panel rows j0 .. min(j0 + NT, jb1) - 1 held in the LDS tile; returns
-// the number of 16 x 4 slices of max(0, L) that ran the second product.
-// Thin slices of the second product.  A 16 x 4 slice (v) of z = max(0, L) with at most
-// SPARSE positive entries does not run its own MFMAs: its entries (row i in the block, panel
-// row j in the tile, value z) are appended to a short per-wave list in LDS, and every four
-// listed entries, whatever their rows and columns, make one gathered srcA slice: lane group k
-// holds entry k, A[i][k] = z_k where i = i_k and 0 elsewhere, with srcB row k = P[j_k].  So
-// the matrix cores spend one slice per four positive entries instead of one per live slice.
-// The list is a ring of ELIST entries (packed i | j << 4, z); a wave appends with one store
-// per slice (ballot prefix counts give the slots) and drains four at a time.
-constexpr int ELIST = 32;
+// Second product by quad-columns on v_mfma_f32_4x4x1f32 (16 blocks of 4 x 4 x 1 each).  A
+// quad-column is 4 rows (4 q4 .. 4 q4 + 3) of one column j of the rectified tile z; it sits in
+// register v = j % 4 of lanes 16 (j / 4) + 4 q4 + 0..3, i.e. in block n = 4 (j / 4) + q4 of the
+// instruction's A operand.  With the broadcast controls set so that all 16 blocks take the A
+// operand of block n (CBSZ = 4, ABID = n), one instruction adds z[4 q4 + 0..3][j] P[j][c] for
+// 64 columns c: block b, column c' of the output is lane 4 b + c' of the B operand, which holds
+// P[j][G lane + g].  So G = RP / 64 instructions cover a quad-column, with no data movement
+// between lanes.  Only quad-columns holding a positive entry run (wave ballots).  An isolated
+// positive entry costs G instructions of 8 cycles; a fully positive 16 x 4 slice (16
+// quad-columns) costs the same matrix-core time as its 16 x 16 x 4 form.
+// Accumulator y[G q4 + g], register v, lane l holds Y[4 q4 + v][G l + g].
+// Returns the number of positive entries of the block.
+template <int RP, int V, int QQ, int Q4>
+__device__ __forceinline__ void quad_mfma(floatx4 (&y)[RP / 16], const floatx4& z,
+                                          const float (&bb)[RP / 64]) {
+  constexpr int G = RP / 64;
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+    y[G * Q4 + g] = __builtin_amdgcn_mfma_f32_4x4x1f32(z[V], bb[g], y[G * Q4 + g], 4, 4 * QQ + Q4, 0);
+}
 
-// Appends the positive entries of slice v of j-block jb (bits = ballot of z > 0) at
-// tail .. tail + popcount(bits) - 1.
-__device__ __forceinline__ void elist_push(uint2* el, unsigned tail, unsigned long long bits,
-                                           float z, int jb, int v, int q, int l16) {
-  if (z > 0.f) {
-    const unsigned below = __builtin_amdgcn_mbcnt_hi((unsigned)(bits >> 32),
-                                                     __builtin_amdgcn_mbcnt_lo((unsigned)bits, 0u));
-    el[(tail + below) % ELIST] =
-        make_uint2((unsigned)l16 | (unsigned)((16 * jb + 4 * q + v) << 4), __float_as_uint(z));
+template <int RP, int V, int QQ>
+__device__ __forceinline__ unsigned quad_group(floatx4 (&y)[RP / 16], const floatx4& z,
+                                               unsigned b16, const float* tile, int jb, int lane) {
+  constexpr int G = RP / 64;
+  const float* prow = &tile[(jb * 16 + 4 * QQ + V) * (RP + 4) + G * lane];
+  float bb[G];
+#pragma unroll
+  for (int h = 0; h < G / 4; ++h) {
+    const float4 t = *reinterpret_cast<const float4*>(prow + 4 * h);
+    bb[4 * h + 0] = t.x;
+    bb[4 * h + 1] = t.y;
+    bb[4 * h + 2] = t.z;
+    bb[4 * h + 3] = t.w;
   }
+  unsigned cnt = 0;
+  if (b16 & 0x000fu) { cnt += __builtin_popcount(b16 & 0x000fu); quad_mfma<RP, V, QQ, 0>(y, z, bb); }
+  if (b16 & 0x00f0u) { cnt += __builtin_popcount(b16 & 0x00f0u); quad_mfma<RP, V, QQ, 1>(y, z, bb); }
+  if (b16 & 0x0f00u) { cnt += __builtin_popcount(b16 & 0x0f00u); quad_mfma<RP, V, QQ, 2>(y, z, bb); }
+  if (b16 & 0xf000u) { cnt += __builtin_popcount(b16 & 0xf000u); quad_mfma<RP, V, QQ, 3>(y, z, bb); }
+  return cnt;
 }
 
-// One gathered slice from the `cnt` (1..4) list entries at head .. head + cnt - 1.
+template <int RP, int V>
+__device__ __forceinline__ unsigned quad_slice(floatx4 (&y)[RP / 16], const floatx4& z,
+                                               const float* tile, int jb, int lane) {
+  const unsigned long long bits = __ballot(z[V] > 0.f);
+  if (!bits) return 0;
+  unsigned cnt = 0;
+  const unsigned lo = (unsigned)bits, hi = (unsigned)(bits >> 32);
+  if (lo & 0xffffu) cnt += quad_group<RP, V, 0>(y, z, lo & 0xffffu, tile, jb, lane);
+  if (lo >> 16) cnt += quad_group<RP, V, 1>(y, z, lo >> 16, tile, jb, lane);
+  if (hi & 0xffffu) cnt += quad_group<RP, V, 2>(y, z, hi & 0xffffu, tile, jb, lane);
+  if (hi >> 16) cnt += quad_group<RP, V, 3>(y, z, hi >> 16, tile, jb, lane);
+  return cnt;
+}
+
 template <int RP>
-__device__ __forceinline__ void elist_slice(floatx4 (&y)[RP / 16], const uint2* el, unsigned head,
-                                            int cnt, const float* tile, int q, int l16) {
-  constexpr int CB = RP / 16;
-  const uint2 e = el[(head + q) % ELIST];
-  const bool valid = q < cnt;
-  const int row = valid ? (int)(e.x >> 4) : 0;
-  const float a = valid && l16 == (int)(e.x & 15u) ? __uint_as_float(e.y) : 0.f;
-  const float* prow = &tile[row * (RP + 4) + l16];
-  float bb[CB];
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb) bb[cb] = prow[16 * cb];
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb)
-    y[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb[cb], y[cb], 0, 0, 0);
+__device__ __forceinline__ unsigned quad_block(floatx4 (&y)[RP / 16], const floatx4& z,
+                                               const float* tile, int jb, int lane) {
+  static_assert(RP == 256 || RP == 512, "quad-column path: r_p = 256 or 512");
+  return quad_slice<RP, 0>(y, z, tile, jb, lane) + quad_slice<RP, 1>(y, z, tile, jb, lane) +
+         quad_slice<RP, 2>(y, z, tile, jb, lane) + quad_slice<RP, 3>(y, z, tile, jb, lane);
 }
 
+// Both products over the panel rows j0 .. min(j0 + NT, jb1) - 1 held in the LDS tile; returns
+// the number of 16 x 4 slices of max(0, L) that ran the second product whole, and adds the
+// positive entries taken by quad-columns to `entries`.
 template <int RP>
 __device__ __forceinline__ unsigned consume_tile(const float* tile, int64_t j0, int64_t jb1,
                                                  const float (&a)[DenseLaunch<RP>::MI][RP / 4],
                                                  floatx4 (&y)[DenseLaunch<RP>::MI][RP / 16],
-                                                 int q, int l16, unsigned& entries, uint2* el) {
+                                                 int q, int l16, unsigned& entries) {
   constexpr int MI = DenseLaunch<RP>::MI;
   constexpr int NT = DenseLaunch<RP>::NT;
   constexpr int CB = RP / 16;
-  constexpr int SPARSE = DenseLaunch<RP>::SPARSE;
   const int left = (int)((jb1 - j0 + 15) / 16);
   const int njb = left < NT / 16 ? left : NT / 16;
   unsigned done = 0;
   float4 pre[l_lookahead<RP>()];
   l_prefetch<RP>(pre, tile, 0, q, l16);
-  if constexpr (SPARSE > 0) {
-    static_assert(MI == 1, "gathered second product: one 16-row block per wave");
-    // at most 3 entries are left after a block, and a block adds at most 4 * SPARSE
-    static_assert(3 + 4 * SPARSE <= ELIST, "entry list length");
-    unsigned head = 0, tail = 0;  // wave-uniform list positions
+  if constexpr (DenseLaunch<RP>::QUAD) {
+    static_assert(MI == 1, "quad-column second product: one 16-row block per wave");
     for (int jb = 0; jb < njb; ++jb) {
       float ring[1][CB];
       floatx4 lt[1];
@@ -181,28 +202,8 @@ __device__ __forceinline__ unsigned consume_tile(const float* tile, int64_t j0, 
 #pragma unroll
       for (int v = 0; v < 4; ++v) lt[0][v] = lt[0][v] > 0.f ? lt[0][v] : 0.f;
       if (jb + 1 < njb) l_prefetch<RP>(pre, tile, jb + 1, q, l16);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const unsigned long long bits = __ballot(lt[0][v] > 0.f);
-        if (!bits) continue;
-        const int cnt = __popcll(bits);
-        if (cnt <= SPARSE) {
-          elist_push(el, tail, bits, lt[0][v], jb, v, q, l16);
-          tail += cnt;
-          entries += cnt;
-        } else {
-          float bb[CB];
-          zb_read<RP>(bb, tile, jb, v, q, l16);
-#pragma unroll
-          for (int cb = 0; cb < CB; ++cb)
-            y[0][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(lt[0][v], bb[cb], y[0][cb], 0, 0, 0);
-          ++done;
-        }
-      }
-      for (; tail - head >= 4; head += 4) elist_slice<RP>(y[0], el, head, 4, tile, q, l16);
+      entries += quad_block<RP>(y[0], lt[0], tile, jb, q * 16 + l16);
     }
-    // the rest refers to this tile's rows: drain it before the buffer is reused
-    if (tail != head) elist_slice<RP>(y[0], el, head, (int)(tail - head), tile, q, l16);
   } else {
     constexpr int NR = DenseLaunch<RP>::RING;
     for (int jb = 0; jb < njb; ++jb) {
@@ -232,9 +233,9 @@ __device__ __forceinline__ unsigned direct_step(
     const float* __restrict__ cur, float* __restrict__ nxt, const float* __restrict__ P,
     int64_t j0, int64_t jb1, const float (&a)[DenseLaunch<RP>::MI][RP / 4],
     floatx4 (&y)[DenseLaunch<RP>::MI][RP / 16], int wave, int lane, int q, int l16,
-    unsigned& entries, uint2* el) {
+    unsigned& entries) {
   if (nxt) issue_tile<RP>(nxt, P, j0 + DenseLaunch<RP>::NT, jb1, wave, lane);
-  return consume_tile<RP>(cur, j0, jb1, a, y, q, l16, entries, el);
+  return consume_tile<RP>(cur, j0, jb1, a, y, q, l16, entries);
 }
 
 template <int RP>
@@ -250,14 +251,11 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
   constexpr int NT = DenseLaunch<RP>::NT;
   static_assert(NT % 16 == 0 && NT % WAVES == 0, "tile shape");
   __shared__ __attribute__((aligned(16))) float smem[(DIRECT ? 2 : 1) * NT * LS];
-  // per-wave lists of the gathered second product (unused where SPARSE is 0)
-  __shared__ uint2 elists[DenseLaunch<RP>::SPARSE > 0 ? WAVES * ELIST : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q = lane >> 4, l16 = lane & 15;
-  uint2* el = &elists[DenseLaunch<RP>::SPARSE > 0 ? wave * ELIST : 0];
 
   const int64_t logical = xcd_logical(blockIdx.x, (int64_t)gridDim.x);
   const int split = (int)(logical / row_tiles);
@@ -276,7 +274,7 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
     for (int cb = 0; cb < CB; ++cb) y[mi][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   unsigned int done = 0;     // 16 x 4 slices of max(0, L) whose second product ran whole
-  unsigned int entries = 0;  // positive entries of max(0, L) taken through gathered slices
+  unsigned int entries = 0;  // positive entries of max(0, L) taken by quad-columns (r_p = 256)
 
   if constexpr (DIRECT) {
     if (jb0 < jb1) issue_tile<RP>(smem, P, jb0, jb1, wave, lane);
@@ -285,7 +283,7 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
       __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the tile have landed
       __syncthreads();                // every wave's have; the other buffer is free again
       done += direct_step<RP>(smem + cur * (NT * LS), j0 + NT < jb1 ? smem + (cur ^ 1) * (NT * LS) : nullptr,
-                              P, j0, jb1, a, y, wave, lane, q, l16, entries, el);
+                              P, j0, jb1, a, y, wave, lane, q, l16, entries);
     }
   } else {
     // register staging: the next tile's global loads are in flight while this one is consumed
@@ -297,12 +295,29 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
       pt.stash(smem, tid);
       __syncthreads();
       if (j0 + NT < jb1) pt.fetch(P, j0 + NT, jb1, tid);
-      done += consume_tile<RP>(smem, j0, jb1, a, y, q, l16, entries, el);
+      done += consume_tile<RP>(smem, j0, jb1, a, y, q, l16, entries);
     }
   }
 
-  // Y block (16 x 16): lane l, register v holds Y[row0 + 16 mi + 4q + v][16 cb + l16].
   float* Y = Ypart + (int64_t)split * y_stride;
+  if constexpr (DenseLaunch<RP>::QUAD) {
+    // quad-column layout: y[G q4 + g], lane l, register v holds Y[row0 + 4 q4 + v][G l + g]
+    constexpr int G = RP / 64;
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t row = row0 + 4 * q4 + v;
+        if (row < rows) {
+#pragma unroll
+          for (int h = 0; h < G / 4; ++h)
+            *reinterpret_cast<float4*>(&Y[row * RP + G * lane + 4 * h]) =
+                make_float4(sgn * y[0][G * q4 + 4 * h + 0][v], sgn * y[0][G * q4 + 4 * h + 1][v],
+                            sgn * y[0][G * q4 + 4 * h + 2][v], sgn * y[0][G * q4 + 4 * h + 3][v]);
+        }
+      }
+  } else {
+  // Y block (16 x 16): lane l, register v holds Y[row0 + 16 mi + 4q + v][16 cb + l16].
 #pragma unroll
   for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
@@ -313,6 +328,7 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
         for (int cb = 0; cb < CB; ++cb) Y[row * RP + 16 * cb + l16] = sgn * y[mi][cb][v];
       }
     }
+  }
   if (gemm2_blocks && lane == 0) {
     atomicAdd(gemm2_blocks, (unsigned long long)done);
     if (entries) atomicAdd(gemm2_blocks + 1, (unsigned long long)entries);

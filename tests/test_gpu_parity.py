@@ -202,11 +202,11 @@ def test_rectified_contraction_cooccurrence_shapes_sampled(rows, blk, split):
     del A, B, Y
 
 
-def test_graph_tenth_two_sweeps_gathered_second_product():
+def test_graph_tenth_two_sweeps_quad_column_second_product():
     """The graph workload at a tenth of its size (13926 x 13926, r = 256, ~1.7M nonzeros), two
     stochastic sweeps.  Sweep 0 starts with S-hat = 0; in sweep 1 S-hat is sparse and positive,
-    and nearly all of the dense kernel's second product goes through gathered slices (the
-    counters show it).  W, H and the objective against the oracle."""
+    and the dense kernel's second product runs per quad-column (4 rows x 1 panel row) holding
+    a positive entry (the counters show it).  W, H and the objective against the oracle."""
     p = gen.config(4, scale=0.1)
     _say("graph workload at scale 0.1, two sweeps", p.m, p.n, p.nnz)
     ctx = make_ctx(p)
@@ -215,7 +215,7 @@ def test_graph_tenth_two_sweeps_gathered_second_product():
     ctx.dense_blocks(reset=True)
     ctx.sweep(W, H, 1)
     run, total, entries = ctx.dense_blocks()
-    print(f"second sweep: {run} of {total} slices run whole, {entries} entries gathered")
+    print(f"second sweep: {run} of {total} slices run whole, {entries} positive entries")
     assert total > 0 and 0 <= run <= total and entries > 0
     assert ctx.dense_blocks(reset=True) == (run, total, entries)
     assert ctx.dense_blocks() == (0, 0, 0)
