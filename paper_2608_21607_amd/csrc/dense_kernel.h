@@ -195,15 +195,32 @@ __device__ __forceinline__ unsigned consume_tile(const float* tile, int64_t j0, 
   l_prefetch<RP>(pre, tile, 0, q, l16);
   if constexpr (DenseLaunch<RP>::QUAD) {
     static_assert(MI == 1, "quad-column second product: one 16-row block per wave");
-    for (int jb = 0; jb < njb; ++jb) {
-      float ring[1][CB];
-      floatx4 lt[1];
-      l_tile<RP, 1, 0>(lt, a, pre, ring, tile, jb, q, l16);
+    // Every j-block of the tile runs (rows past the split end are zero in LDS, so their L is
+    // zero and they add nothing).  A block's second product runs after the next block's first
+    // product has been issued, from the accumulator chains held meanwhile, so that the wave
+    // does not wait for its first product to drain before the branches of the second.
+    static_assert(l_chains<1>() == 2, "two accumulator chains");
+    floatx4 hold[2];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) lt[0][v] = lt[0][v] > 0.f ? lt[0][v] : 0.f;
-      if (jb + 1 < njb) l_prefetch<RP>(pre, tile, jb + 1, q, l16);
-      entries += quad_block<RP>(y[0], lt[0], tile, jb, q * 16 + l16);
+    for (int jb = 0; jb < NT / 16; ++jb) {
+      float ring[1][CB];
+      floatx4 acc[2][1];
+      l_tile_acc<RP, 1, 0>(acc, a, pre, ring, tile, jb, q, l16);
+      if (jb + 1 < NT / 16) l_prefetch<RP>(pre, tile, jb + 1, q, l16);
+      if (jb > 0) {
+        floatx4 z = hold[0] + hold[1];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) z[v] = z[v] > 0.f ? z[v] : 0.f;
+        entries += quad_block<RP>(y[0], z, tile, jb - 1, q * 16 + l16);
+      }
+      hold[0] = acc[0][0];
+      hold[1] = acc[1][0];
     }
+    floatx4 z = hold[0] + hold[1];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) z[v] = z[v] > 0.f ? z[v] : 0.f;
+    entries += quad_block<RP>(y[0], z, tile, NT / 16 - 1, q * 16 + l16);
+    (void)njb;
   } else {
     constexpr int NR = DenseLaunch<RP>::RING;
     for (int jb = 0; jb < njb; ++jb) {

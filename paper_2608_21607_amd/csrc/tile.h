@@ -104,6 +104,10 @@ __device__ __forceinline__ void l_prefetch(float4 (&pre)[l_lookahead<RP>()], con
   for (int t = 0; t < l_lookahead<RP>(); ++t) pre[t] = *reinterpret_cast<const float4*>(brow + 16 * t);
 }
 
+// Accumulator chains of the first product (NA below).
+template <int MI>
+constexpr int l_chains() { return MI >= 2 ? 1 : 2; }
+
 // Transposed L tile of one 16-row j-block: lt[mi] lane l, register v holds
 // L[i = row0 + 16 mi + l16][j = jb*16 + 4q + v] (srcA = panel rows, srcB = X rows, both over
 // the permuted k order 16t + 4q + c, one ds_read_b128 per four k-steps).  `pre` holds the first
@@ -111,18 +115,20 @@ __device__ __forceinline__ void l_prefetch(float4 (&pre)[l_lookahead<RP>()], con
 // group: the read of group t + LA, its share of the srcB operands of the block's second product
 // (the NR slices of `ring`, NR = 0, 2 or 4), then its MFMAs, which take the NA accumulators
 // round-robin per k-step so that dependent MFMAs are at least two apart.
+// l_tile_acc leaves the NA chains unsummed (acc[h][mi], lt[mi] = sum over h), so that a caller
+// can hold them past the next block's MFMAs before it needs their sum.
 template <int RP, int MI, int NR>
-__device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][RP / 4],
-                                       const float4 (&pre)[l_lookahead<RP>()],
-                                       float (&ring)[NR > 0 ? NR : 1][RP / 16], const float* tile,
-                                       int jb, int q, int l16) {
+__device__ __forceinline__ void l_tile_acc(floatx4 (&acc)[l_chains<MI>()][MI],
+                                           const float (&a)[MI][RP / 4],
+                                           const float4 (&pre)[l_lookahead<RP>()],
+                                           float (&ring)[NR > 0 ? NR : 1][RP / 16],
+                                           const float* tile, int jb, int q, int l16) {
   constexpr int LS = RP + 4;
   constexpr int KG = RP / 16;
   constexpr int CB = RP / 16;
   constexpr int LA = l_lookahead<RP>();
-  constexpr int NA = MI >= 2 ? 1 : 2;
+  constexpr int NA = l_chains<MI>();
   constexpr int PER = NR * CB / KG;  // ring values read per k-group (NR * CB = NR * KG)
-  floatx4 acc[NA][MI];
 #pragma unroll
   for (int h = 0; h < NA; ++h)
 #pragma unroll
@@ -151,11 +157,20 @@ __device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][R
     }
     __builtin_amdgcn_sched_barrier(0);
   }
+}
+
+template <int RP, int MI, int NR>
+__device__ __forceinline__ void l_tile(floatx4 (&lt)[MI], const float (&a)[MI][RP / 4],
+                                       const float4 (&pre)[l_lookahead<RP>()],
+                                       float (&ring)[NR > 0 ? NR : 1][RP / 16], const float* tile,
+                                       int jb, int q, int l16) {
+  floatx4 acc[l_chains<MI>()][MI];
+  l_tile_acc<RP, MI, NR>(acc, a, pre, ring, tile, jb, q, l16);
 #pragma unroll
   for (int mi = 0; mi < MI; ++mi) {
     lt[mi] = acc[0][mi];
 #pragma unroll
-    for (int h = 1; h < NA; ++h) lt[mi] += acc[h][mi];
+    for (int h = 1; h < l_chains<MI>(); ++h) lt[mi] += acc[h][mi];
   }
 }
 
