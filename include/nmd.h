@@ -284,10 +284,10 @@ int64_t nmd_bf16x3_workspace_floats(int64_t blk, int32_t r);
  * nmd_get_dense_blocks - how much of the second product of the dense contraction the sweeps
  * ran, since the context was created or last reset here.  The second product is organised in
  * slices of 16 rows x 4 panel rows of max(0, L) (Sec. 4.3: S-hat is sparse): a slice with no
- * positive entry is skipped and the others run their own MFMAs; at r_p = 256 the second
- * product instead runs per quad-column (4 rows x 1 panel row) holding a positive entry.
+ * positive entry is skipped and the others run their own MFMAs; at r_p = 256 and 512 the
+ * second product instead runs per quad-column (4 rows x 1 panel row) holding a positive entry.
  * *run = slices that ran whole, *total = slices examined, *entries = positive entries taken
- * by quad-columns (r_p = 256); the second product's useful work is run/total of its dense
+ * by quad-columns (r_p = 256, 512); the second product's useful work is run/total of its dense
  * count plus 2 r flops per entry.  Synchronises the device.
  * reset != 0 clears all three after reading.  Any output pointer may be NULL.
  */

@@ -8,8 +8,8 @@
 // This kernel forms the dense term -S-hat P_J (sgn = -1); the sparse correction adds the first
 // term.  S-hat is mostly zero (the factors start with opposite signs and the fit keeps it sparse,
 // Sec. 4.3), so a wave skips the MFMAs of every 16 x 4 operand slice of S-hat that holds no
-// positive entry, and (at r_p = 256) runs the second product per 4-row quad-column of S-hat on
-// 4 x 4 x 1 MFMAs, only where one holds a positive entry (below).  The L tile is produced by
+// positive entry, and (at r_p = 256 and 512) runs the second product per 4-row quad-column of
+// S-hat on 4 x 4 x 1 MFMAs, only where one holds a positive entry (below).  The L tile is produced by
 // MFMA, rectified in registers and consumed by MFMA; neither L nor S-hat reaches memory (the
 // IO-aware fusion of Sec. 4.2, with the raw panel P instead of a pseudo-inverse).
 //
@@ -23,8 +23,9 @@
 //     v holds L[i = l%16][j = 4(l/16) + v], which is exactly the srcA layout of GEMM2 for the
 //     k-slice {4(l/16) + v}: the rectified tile feeds GEMM2 with no data movement.
 //   * GEMM2: Y[i][c] += sum_j max(0, L[i][j]) P[j][c], srcB read from LDS, per 16 x 4 slice
-//     of max(0, L) on 16 x 16 x 4 MFMAs, skipped when zero; at r_p = 256 per quad-column
-//     (4 rows x 1 column) on 4 x 4 x 1 MFMAs with the A operand broadcast from the L tile.
+//     of max(0, L) on 16 x 16 x 4 MFMAs, skipped when zero; at r_p = 256 and 512 per
+//     quad-column (4 rows x 1 column) on 4 x 4 x 1 MFMAs with the A operand broadcast from
+//     the L tile.
 //   * Split-J: the workgroups of one row tile may be spread over `nsplit` disjoint ranges of P
 //     rows, each writing its own partial Y; the solve kernel sums them in fp64.
 
@@ -52,7 +53,7 @@ struct DenseLaunch {
   static constexpr bool DIRECT = RP >= 320;
   static constexpr int NT = DIRECT ? DenseCfg<RP>::NTD : DenseCfg<RP>::NT;
   static constexpr int RING = RP >= 320 ? 4 : 2;
-  static constexpr bool QUAD = false;
+  static constexpr bool QUAD = RP == 512;
 };
 template <>
 struct DenseLaunch<256> {
