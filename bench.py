@@ -291,9 +291,9 @@ def main():
     dense_equiv = 4.0 * p.m * p.n * p.r * sweeps_per_s / 1e12
     dense_equiv_8mnr = 8.0 * p.m * p.n * p.r * sweeps_per_s / 1e12
     # The second product of the dense kernel runs its own MFMAs only for the 16 x 4 slices of
-    # max(0, L) with a positive entry, or (r_p = 256) per quad-column holding one, counting the
-    # positive entries (2 r useful flops each).  Its algorithmic flops are the first product's
-    # times the fraction of slices run whole plus 2 r per counted entry.
+    # max(0, L) with a positive entry, or (r_p = 256, 512) per quad-column holding one,
+    # counting the positive entries (2 r useful flops each).  Its algorithmic flops are the
+    # first product's times the fraction of slices run whole plus 2 r per counted entry.
     g2_run, g2_total, g2_entries = ctx.dense_blocks()
     g2_frac = g2_run / g2_total if g2_total else 1.0
     split = args.split_bf16 and rp in (16, 32, 64, 128, 256, 512)

@@ -292,7 +292,7 @@ __global__ __launch_bounds__(64 * DenseLaunch<RP>::WAVES) void dense_kernel(
     for (int cb = 0; cb < CB; ++cb) y[mi][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   unsigned int done = 0;     // 16 x 4 slices of max(0, L) whose second product ran whole
-  unsigned int entries = 0;  // positive entries of max(0, L) taken by quad-columns (r_p = 256)
+  unsigned int entries = 0;  // positive entries of max(0, L) taken by quad-columns
 
   if constexpr (DIRECT) {
     if (jb0 < jb1) issue_tile<RP>(smem, P, jb0, jb1, wave, lane);
