@@ -532,6 +532,33 @@ def test_odd_shapes(case):
     assert abs(f - salsa.objective(S, Wg, Hg)) <= TOL * f
 
 
+# Stochastic sweeps on nearly full and 26% full matrices at the quad-column ranks: many nonzeros
+# on every row of every block, for the sparse correction's long rows (items cut into several
+# parts) and the second product's dense slices.  (At r = 512 the blocks keep 700 panel rows:
+# with 550 the Gram matrices of a nearly full S are conditioned badly enough that fp32 rounding
+# alone moves W and H by 2e-4 from the fp64 oracle.)
+DENSE_ROWS = [(700, 600, 256, 350, 300, 3.0), (700, 600, 256, 350, 300, 0.3),
+              (1400, 1400, 512, 700, 700, 3.0)]
+
+
+@pytest.mark.parametrize("case", DENSE_ROWS,
+                         ids=[f"{c[0]}x{c[1]}r{c[2]}d{c[5]}" for c in DENSE_ROWS])
+def test_dense_rows_sweep(case):
+    m, n, r, bm, bn, density = case
+    _say("dense rows, one stochastic sweep", case)
+    row_ptr, col, val = gen.random_sparse(m, n, density, m + n + r + 11)
+    W0, H0 = gen.sign_constrained_init(m, n, r, float(val.mean()), r + 1)
+    p = gen.Problem("dense rows", m, n, r, row_ptr, col, val, W0, H0, bm, bn, "stochastic", 1.0,
+                    0.9, 7)
+    Wg, Hg, ctx = gpu_run(p, 1)
+    Wo, Ho, S = oracle_run(p, 1)
+    ew, eh = rel(Wg, Wo), rel(Hg, Ho)
+    print(f"nnz {len(col)}: rel err W {ew:.2e} H {eh:.2e}")
+    assert ew < TOL and eh < TOL
+    f = ctx.objective(dev(Wg), dev(Hg))
+    assert abs(f - salsa.objective(S, Wg, Hg)) <= TOL * f
+
+
 # ---------------------------------------------------------- objective and reconstruction metrics
 def test_metrics_calibration_and_fit():
     """eqs. RMSE and WJD: at the sign-constrained start S-hat = 0, so both equal 1 (their
