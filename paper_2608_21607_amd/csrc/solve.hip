@@ -412,11 +412,15 @@ hipError_t launch_apply(const float* Ypart, int64_t y_stride, int nsplit, const 
                        gamma, status, step_id);                                              \
     break;                                                                                   \
   }
-  // row tile: the tallest allowed one that still gives 4096 workgroups, else 16 rows
+  // Row tile: the tallest allowed one that still gives 4096 workgroups (1024 at r_p >= 512),
+  // else 16 rows.  Every workgroup reads all of G^-1 (r_p^2 doubles) from L2 once, so at
+  // r_p = 512 a 16-row tile moves 128 KB of it per row, which saturates the L2; 32 rows halve
+  // that at fewer workgroups.
   const int rw_max = rp >= 64 ? (16384 / rp >= 64 ? 64 : (16384 / rp >= 32 ? 32 : 16)) : 16;
+  const int64_t min_wgs = rp >= 512 ? 1024 : 4096;
   int rw = 16;
   for (int cand = rw_max; cand > 16; cand /= 2)
-    if ((rows + cand - 1) / cand >= 4096) {
+    if ((rows + cand - 1) / cand >= min_wgs) {
       rw = cand;
       break;
     }
