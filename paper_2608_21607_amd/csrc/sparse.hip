@@ -10,7 +10,10 @@
 // columns of the row's factor x_i and of its partial result: the E consecutive columns from
 // t E when E is a multiple of 4 (16-byte accesses; 9% faster than the strided form on the graph
 // workload), else columns t, t + T, ...  Either way a gather of a row p_j is one coalesced run
-// of RP floats.  l_ij = x_i . p_j is reduced across the team with lane shuffles.
+// of RP floats.  l_ij = x_i . p_j is reduced across the team with lane shuffles.  An item's
+// terms and the fix-up's partial results are summed in fp64: on nearly full rows the fp32 sums
+// of hundreds of terms, amplified by an ill-conditioned Gram matrix, had put W 2e-4 from the
+// fp64 oracle after one sweep (7e-5 with fp64 sums; 7% more time for this kernel).
 
 #include "nmd_internal.h"
 
@@ -86,7 +89,8 @@ __global__ __launch_bounds__(256) void sparse_kernel(const Item* __restrict__ it
   // row it adds to, and the first U entries.  The gathers then wait for a single round trip.
   const bool rmw = it.slot < 0 && accumulate;
   float* const yrow = it.slot < 0 ? Y + (int64_t)it.row * RP : scratch + (int64_t)it.slot * RP;
-  float x[E], acc[E], yv[E];
+  float x[E], yv[E];
+  double acc[E];  // a row's terms are summed in fp64 (long rows have hundreds)
   load_row<T, E, CONTIG>(x, X + (int64_t)it.row * RP, t);
   if (rmw) load_row<T, E, CONTIG>(yv, yrow, t);
   int32_t jn[U];
@@ -98,7 +102,7 @@ __global__ __launch_bounds__(256) void sparse_kernel(const Item* __restrict__ it
     sn[u] = in ? val[b + u] : 0.f;
   }
 #pragma unroll
-  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  for (int e = 0; e < E; ++e) acc[e] = 0.0;
   int p = 0;
   for (; p + U <= cnt; p += U) {
     int32_t j[U];
@@ -132,7 +136,7 @@ __global__ __launch_bounds__(256) void sparse_kernel(const Item* __restrict__ it
     for (int u = 0; u < U; ++u) {
       const float c = s[u] - fminf(d[u], 0.f);
 #pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] = fmaf(c, pv[u][e], acc[e]);
+      for (int e = 0; e < E; ++e) acc[e] = fma((double)c, (double)pv[u][e], acc[e]);
     }
   }
   // the last cnt - p (< U) entries are in jn / sn
@@ -148,13 +152,16 @@ __global__ __launch_bounds__(256) void sparse_kernel(const Item* __restrict__ it
     for (int off = T / 2; off > 0; off >>= 1) dd += __shfl_xor(dd, off, T);
     const float c = sn[u] - fminf(dd, 0.f);
 #pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] = fmaf(c, pv[e], acc[e]);
+    for (int e = 0; e < E; ++e) acc[e] = fma((double)c, (double)pv[e], acc[e]);
   }
   if (rmw) {
 #pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] += yv[e];
+    for (int e = 0; e < E; ++e) acc[e] += (double)yv[e];
   }
-  store_row<T, E, CONTIG>(yrow, acc, t, false);
+  float out[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) out[e] = (float)acc[e];
+  store_row<T, E, CONTIG>(yrow, out, t, false);
 }
 
 template <int T, int E, bool CONTIG>
@@ -166,16 +173,19 @@ __global__ __launch_bounds__(256) void fixup_kernel(const Split* __restrict__ sp
   const int t = threadIdx.x % T;
   if (team >= n) return;
   const Split sp = splits[team];
-  float acc[E];
+  double acc[E];
 #pragma unroll
-  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  for (int e = 0; e < E; ++e) acc[e] = 0.0;
   for (int k = 0; k < sp.nslots; ++k) {
     float v[E];
     load_row<T, E, CONTIG>(v, scratch + (int64_t)(sp.first + k) * RP, t);
 #pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] += v[e];
+    for (int e = 0; e < E; ++e) acc[e] += (double)v[e];
   }
-  store_row<T, E, CONTIG>(Y + (int64_t)sp.row * RP, acc, t, accumulate != 0);
+  float out[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) out[e] = (float)acc[e];
+  store_row<T, E, CONTIG>(Y + (int64_t)sp.row * RP, out, t, accumulate != 0);
 }
 
 #define NMD_SPARSE_DISPATCH(rp, LAUNCH) \
