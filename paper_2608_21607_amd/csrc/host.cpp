@@ -111,6 +111,9 @@ struct nmd_ctx {
   int64_t dense_slots = 0;           // dense workgroups resident at once (CUs x per CU)
   hipStream_t side = nullptr;     // Gram and inverse run here, beside the contraction
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  hipStream_t corr = nullptr;     // the sparse correction runs here, beside the contraction
+  hipEvent_t ev_cfork = nullptr, ev_cjoin = nullptr;
+  float* Ysp = nullptr;           // its output there (max(m, n) rows x rp; r_p >= 320, fp32)
   int* h_status = nullptr;   // pinned
   double* h_obj = nullptr;   // pinned
 
@@ -200,6 +203,12 @@ void free_device(nmd_ctx* c) {
   if (c->side) (void)hipStreamDestroy(c->side);
   c->ev_fork = c->ev_join = nullptr;
   c->side = nullptr;
+  if (c->ev_cfork) (void)hipEventDestroy(c->ev_cfork);
+  if (c->ev_cjoin) (void)hipEventDestroy(c->ev_cjoin);
+  if (c->corr) (void)hipStreamDestroy(c->corr);
+  c->ev_cfork = c->ev_cjoin = nullptr;
+  c->corr = nullptr;
+  dfree(c->Ysp);
   if (c->h_status) (void)hipHostFree(c->h_status);
   if (c->h_obj) (void)hipHostFree(c->h_obj);
   c->h_status = nullptr;
@@ -286,6 +295,7 @@ int ensure_device(nmd_ctx* c) {
     // the split-bf16 option covers the padded ranks the bf16x3 kernels support
     const bool bx = (c->opt.flags & NMD_FLAG_SPLIT_BF16) && nmd::bf16x3_rank(rp);
     if (dalloc(&c->Ypart, c->ypart_floats) != hipSuccess ||
+        (rp >= 320 && !bx && dalloc(&c->Ysp, std::max(c->m, c->n) * rp) != hipSuccess) ||
         (bx && dalloc(&c->Pbx, nmd::bf16x3_work_floats(std::max(c->m, c->n), rp)) != hipSuccess)) {
       free_device(c);
       return fail(c, NMD_ENOMEM, "device allocation of %lld partial-output floats failed",
@@ -303,9 +313,12 @@ int ensure_device(nmd_ctx* c) {
     // default priority on purpose: every stream of the library runs at the same priority
     if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess ||
         hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess) {
+        hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess ||
+        hipStreamCreateWithFlags(&c->corr, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&c->ev_cfork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&c->ev_cjoin, hipEventDisableTiming) != hipSuccess) {
       free_device(c);
-      return fail(c, NMD_EDEVICE, "creating the side stream or its events failed");
+      return fail(c, NMD_EDEVICE, "creating the side streams or their events failed");
     }
     HIP_TRY(c, hipMemset(c->status, 0, sizeof(int)));
     HIP_TRY(c, hipMemset(c->status + 1, 0x7f, sizeof(int)));
@@ -480,6 +493,18 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
   const int64_t y_stride = rows * rp;
   if (ns * y_stride > c->ypart_floats)
     return fail(c, NMD_EDEVICE, "internal: partial-output buffer too small");
+  // Where the contraction runs one matrix-core wave per SIMD (r_p >= 320, fp32), the sparse
+  // correction runs beside it, on its own stream, into its own buffer: it is bound by memory
+  // and needs no LDS, so its workgroups fill the register and wave slots the contraction leaves
+  // on every CU (co-occurrence sweep 627 -> 608 ms).  At r_p <= 256 the contraction runs two
+  // waves per SIMD, and the correction beside it slowed it by more than the correction's own
+  // time (graph sweep 202.5 -> 204.5 ms); there it runs after the contraction, on the same
+  // stream, added in place to the first partial output.  X and P are final here.
+  const bool beside = !c->Pbx && rp >= 320;
+  if (beside) {
+    HIP_TRY(c, hipEventRecord(c->ev_cfork, st));
+    HIP_TRY(c, hipStreamWaitEvent(c->corr, c->ev_cfork, 0));
+  }
   {
     // U = Delta_{:J} P_J starts as -max(0, X P_J^T) P_J (eq. updateD off the nonzeros); the
     // second contraction is skipped on the 16 x 4 slices where that rectified tile is zero
@@ -499,24 +524,32 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
     // slices of 16 rows x 4 panel rows examined (those entirely past the last row never run)
     c->g2_total += (rows + 15) / 16 * jblocks * 4;
   }
-  // Sparse correction at the nonzeros (eq. updateD there: s - l = (s - min(0, l)) - max(0, l)),
-  // added in place to the first partial output.  It runs
-  // after the contraction on the same stream: beside it, its gathers would take issue slots
-  // from the single MFMA wave per SIMD of the contraction.
+  // Sparse correction at the nonzeros (eq. updateD there: s - l = (s - min(0, l)) - max(0, l)):
+  // beside the contraction into Ysp (zero off the touched rows), else into the first partial.
+  hipStream_t cs = beside ? c->corr : st;
+  float* Ycorr = beside ? c->Ysp : c->Ypart;
   const int32_t b0 = block >= 0 ? block : 0;
   const int32_t b1 = block >= 0 ? block + 1 : sd.nblk();
+  if (beside) HIP_TRY(c, nmd::launch_zero(c->Ysp, rows * rp, cs));
   for (int32_t b = b0; b < b1; ++b) {
     const int64_t ni = sd.item_off[b + 1] - sd.item_off[b];
     const int64_t nsp = sd.split_off[b + 1] - sd.split_off[b];
     const int64_t nz = sd.entry_off[b + 1] - sd.entry_off[b];
+    // into the partial output it always adds; into Ysp the first block (every block in the
+    // stochastic mode) writes and later ones add
+    const int acc = !beside || b > b0 ? 1 : 0;
     // algorithmic bytes: entries (index + value), each touched row of X and of Y (read x,
-    // read and write y), each panel row of the block once
-    const double bytes = 8.0 * nz + 12.0 * (double)ni * c->r + 4.0 * blk * c->r;
-    Scope sc(c, st, K_SPARSE, 4.0 * nz * c->r, bytes);
+    // write y, and read y where it adds), each panel row of the block once
+    const double bytes = 8.0 * nz + (acc ? 12.0 : 8.0) * (double)ni * c->r + 4.0 * blk * c->r;
+    Scope sc(c, cs, K_SPARSE, 4.0 * nz * c->r, bytes);
     HIP_TRY(c, nmd::launch_sparse(sd.d_items + sd.item_off[b], ni, sd.d_idx, sd.d_val, X, P, rp,
-                                  c->Ypart, c->scratch, 1, st));
-    HIP_TRY(c, nmd::launch_fixup(sd.d_splits + sd.split_off[b], nsp, c->scratch, rp, c->Ypart, 1,
-                                 st));
+                                  Ycorr, c->scratch, acc, cs));
+    HIP_TRY(c, nmd::launch_fixup(sd.d_splits + sd.split_off[b], nsp, c->scratch, rp, Ycorr, acc,
+                                 cs));
+  }
+  if (beside) {
+    HIP_TRY(c, hipEventRecord(c->ev_cjoin, c->corr));
+    HIP_TRY(c, hipStreamWaitEvent(st, c->ev_cjoin, 0));
   }
   {
     // the time the caller's stream waits here for the side stream (zero once it is ahead)
@@ -524,11 +557,12 @@ int factor_step(nmd_ctx* c, bool wstep, int32_t block, float eta, float gamma, i
     HIP_TRY(c, hipStreamWaitEvent(st, c->ev_join, 0));
   }
   {
-    Scope sc(c, st, K_APPLY, 2.0 * rows * (double)rp * rp, 4.0 * rows * rp * (ns + 4));
+    Scope sc(c, st, K_APPLY, 2.0 * rows * (double)rp * rp,
+             4.0 * rows * rp * (ns + (beside ? 5 : 4)));
     float* Xout = wstep ? c->A2 : c->B2;
     float* Vout = wstep ? c->VA2 : c->VB2;
-    HIP_TRY(c, nmd::launch_apply(c->Ypart, y_stride, (int)ns, nullptr, Gneg, X, V, Xout, Vout, rows,
-                                 rp, eta, gamma, c->status, step_id, st));
+    HIP_TRY(c, nmd::launch_apply(c->Ypart, y_stride, (int)ns, beside ? c->Ysp : nullptr, Gneg, X,
+                                 V, Xout, Vout, rows, rp, eta, gamma, c->status, step_id, st));
   }
   swap_side(c, wstep);
   c->enqueued.emplace_back(step_id, wstep);
