@@ -344,8 +344,11 @@ def main():
         # the kernel skips most of that work, so this rate can exceed the peak
         "dense_equiv_8mnr_tflops": dense_equiv_8mnr,
         "dense_equiv_8mnr_frac_of_fp32_peak": dense_equiv_8mnr / PEAK_FP32_MFMA,
+        # the sparse correction's algorithmic bytes over its own time; at r_p >= 320 it runs
+        # beside the dense kernel (off the critical path), so that time is the one it takes there
         "sparse_pass_gbs": sparse_gbs,
         "sparse_pass_frac_of_hbm": sparse_gbs / PEAK_HBM,
+        "sparse_beside_dense": rp >= 320 and not args.split_bf16,
         "kernel_ms_per_sweep": {
             "dense": dense["ms"] / args.steps, "sparse": sparse["ms"] / args.steps,
             "gram_inverse": factor["ms"] / args.steps, "solve_apply": apply_["ms"] / args.steps,
