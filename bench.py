@@ -348,7 +348,7 @@ def main():
         # beside the dense kernel (off the critical path), so that time is the one it takes there
         "sparse_pass_gbs": sparse_gbs,
         "sparse_pass_frac_of_hbm": sparse_gbs / PEAK_HBM,
-        "sparse_beside_dense": rp >= 320 and not args.split_bf16,
+        "sparse_beside_dense": rp >= 320 and not split,
         "kernel_ms_per_sweep": {
             "dense": dense["ms"] / args.steps, "sparse": sparse["ms"] / args.steps,
             "gram_inverse": factor["ms"] / args.steps, "solve_apply": apply_["ms"] / args.steps,
