@@ -515,6 +515,9 @@ ODD = [
     (333, 290, 100, 333, 290, "deterministic", 1.0, 0.0, {"empty_rows": 5}),
     (700, 600, 256, 350, 300, "stochastic", 1.0, 0.9, {}),
     (1100, 900, 512, 550, 900, "stochastic", 1.0, 0.0, {"heavy_row_frac": 0.3}),
+    # deterministic at r_p = 320: the correction beside the dense kernel, a W-step's two column
+    # blocks written and then added into its buffer
+    (600, 500, 320, 200, 250, "deterministic", 1.0, 0.0, {"heavy_row_frac": 0.3}),
 ]
 
 
