@@ -139,20 +139,39 @@ __global__ __launch_bounds__(256) void sparse_kernel(const Item* __restrict__ it
       for (int e = 0; e < E; ++e) acc[e] = fma((double)c, (double)pv[u][e], acc[e]);
     }
   }
-  // the last cnt - p (< U) entries are in jn / sn
+  // the last cnt - p (< U) entries are in jn / sn: their rows are requested together before
+  // any is used (one round trip, not one per entry); a slot past the end holds zeros and
+  // adds nothing
+  if (p < cnt) {
+    float pv[U - 1][E], d[U - 1];
 #pragma unroll
-  for (int u = 0; u < U - 1; ++u) {
-    if (p + u >= cnt) break;
-    float pv[E];
-    load_row<T, E, CONTIG>(pv, P + (int64_t)jn[u] * RP, t);
-    float dd = 0.f;
+    for (int u = 0; u < U - 1; ++u) {
+      if (p + u < cnt) {
+        load_row<T, E, CONTIG>(pv[u], P + (int64_t)jn[u] * RP, t);
+      } else {
 #pragma unroll
-    for (int e = 0; e < E; ++e) dd = fmaf(x[e], pv[e], dd);
+        for (int e = 0; e < E; ++e) pv[u][e] = 0.f;
+      }
+    }
 #pragma unroll
-    for (int off = T / 2; off > 0; off >>= 1) dd += __shfl_xor(dd, off, T);
-    const float c = sn[u] - fminf(dd, 0.f);
+    for (int u = 0; u < U - 1; ++u) {
+      float dd = 0.f;
 #pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] = fma((double)c, (double)pv[e], acc[e]);
+      for (int e = 0; e < E; ++e) dd = fmaf(x[e], pv[u][e], dd);
+      d[u] = dd;
+    }
+#pragma unroll
+    for (int off = T / 2; off > 0; off >>= 1)
+#pragma unroll
+      for (int u = 0; u < U - 1; ++u) d[u] += __shfl_xor(d[u], off, T);
+#pragma unroll
+    for (int u = 0; u < U - 1; ++u) {
+      if (p + u < cnt) {
+        const float c = sn[u] - fminf(d[u], 0.f);
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = fma((double)c, (double)pv[u][e], acc[e]);
+      }
+    }
   }
   if (rmw) {
 #pragma unroll
