@@ -79,7 +79,10 @@ __global__ __launch_bounds__(256) void sparse_kernel(const Item* __restrict__ it
                                                      float* __restrict__ scratch,
                                                      int accumulate) {
   constexpr int RP = T * E;
-  const int64_t team = ((int64_t)blockIdx.x * 256 + threadIdx.x) / T;
+  int64_t team = ((int64_t)blockIdx.x * 256 + threadIdx.x) / T;
+  // a 64-lane team is one wave: its item index is uniform, so the item and its first entries
+  // come through the scalar cache
+  if constexpr (T == 64) team = (int64_t)__builtin_amdgcn_readfirstlane((int)team);
   const int t = threadIdx.x % T;
   if (team >= nitems) return;
   const Item it = items[team];
