@@ -227,7 +227,7 @@ __global__ __launch_bounds__(256) void fixup_kernel(const Split* __restrict__ sp
   }                                     \
   return hipGetLastError();
 
-constexpr int kDepth = 4;  // entries of an item in flight per team (8 measured slower)
+constexpr int kDepth = 4;  // entries of an item in flight per team (8: no faster)
 constexpr bool contig(int E) { return E % 4 == 0; }
 
 static inline unsigned grid_for(int64_t teams, int T) {
