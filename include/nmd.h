@@ -128,7 +128,9 @@ int nmd_set_sparse_csr(nmd_ctx* ctx, int64_t nnz, const int64_t* row_ptr, const 
 /*
  * nmd_als_block_sweep - runs n_sweeps >= 1 sweeps (epochs) in place on W and H.
  *   W: device float[m*r], row-major m x r.  H: device float[r*n], row-major r x n.
- *   hip_stream: a hipStream_t (NULL = the null stream); all work is ordered on it.
+ *   hip_stream: a hipStream_t (NULL = the null stream); all work is ordered on it (the
+ *   library's own streams, for the Gram matrices and inverses and, at r_p >= 320, the sparse
+ *   correction, start from events on it and rejoin it before each update).
  * Stochastic mode: sweep t executes the seeded interleaved list of W-steps (one column block
  * J each, eq. lsqA_sto) and H-steps (one row block I each); see nmd_get_schedule.
  * Deterministic mode: the exact half-steps A <- A + Delta B (B^T B)^-1 over all columns, then
@@ -298,7 +300,8 @@ int nmd_get_dense_blocks(nmd_ctx* ctx, int64_t* run, int64_t* total, int64_t* en
  * nmd_get_kernel_timing - with NMD_FLAG_TIMING set, the summed device time (HIP events on the
  * stream the work ran on) and launch count of one kernel class since the last reset of the
  * timers, plus the algorithmic work of those launches.  kernel: 0 = fused dense contraction
- * (flops = 4 rows blk r per launch), 1 = sparse correction (bytes = algorithmic HBM bytes),
+ * (flops = 4 rows blk r per launch), 1 = sparse correction (bytes = algorithmic HBM bytes; at
+ * r_p >= 320 it runs on its own stream, beside the contraction, and this is its time there),
  * 2 = Gram matrices and inverses (side stream; one entry per run of same-side steps), 3 = solve
  * and update, 4 = the time the caller's stream waited for the side stream before an update
  * (zero when the solve was ready; no work).  Synchronises the recorded events.
