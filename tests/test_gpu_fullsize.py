@@ -233,7 +233,8 @@ def test_config4_split_bf16_first_steps_sampled(config4):
 
 
 # The same end to end for the 500000 x 50000 co-occurrence workload at rank 512.  Its oracle
-# sweep takes about 15-20 minutes of host fp64 work, so these run only when NMD_SLOW_TESTS=1.
+# sweep takes minutes of host fp64 work (about 6 on 16 threads, longer on fewer), so these run
+# only when NMD_SLOW_TESTS=1.
 _slow = pytest.mark.skipif(os.environ.get("NMD_SLOW_TESTS") != "1",
                            reason="about 20 minutes of host fp64 work; set NMD_SLOW_TESTS=1")
 _E5 = {}
